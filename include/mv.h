@@ -1,0 +1,253 @@
+/*
+ * mv.h -- C ABI of libmv: view-masked causal attention and the fused LM-head
+ * token log-prob for scoring a memory-compressed agent trajectory under the
+ * live views it was decoded from (MemoryWalker, arXiv 2609.00865), on AMD
+ * MI355X (gfx950).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Status: every call returns mv_status.  On failure nothing is launched,
+ *    no output is written, and mv_last_error() holds a message for the calling
+ *    thread.  No C++ exception crosses this boundary.
+ *  - Device memory: the library never allocates device memory.  Every device
+ *    buffer (inputs, outputs, the uploaded mask, workspaces) is allocated by
+ *    the caller and sized with the *_bytes queries.  Device pointers must be
+ *    16-byte aligned and live on the current HIP device.
+ *  - Host memory: host arrays owned by a mv_view_mask are freed by
+ *    mv_view_mask_free.  Input arrays passed by the caller are only read
+ *    during the call.
+ *  - Streams: device work is enqueued asynchronously on the given stream
+ *    (0 = the null stream).  Host-only calls are synchronous.
+ *  - Element types: "bf16" is IEEE bfloat16 stored as 16-bit words; fp32 is
+ *    IEEE binary32.  Arithmetic: bf16 matrix products with fp32 accumulation;
+ *    softmax statistics in fp32; one round-to-nearest-even to bf16 per
+ *    stored bf16 output.
+ *  - Thread safety: calls on distinct mask objects are independent; a mask
+ *    object must not be used while it is being uploaded or freed.
+ */
+#ifndef MV_H_
+#define MV_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MV_OK = 0,
+  MV_ERR_INVALID_ARG = 1,  /* null pointer, negative size, misaligned buffer   */
+  MV_ERR_BAD_RECORD = 2,   /* eviction record that no rollout could produce    */
+  MV_ERR_SHAPE = 3,        /* tensor shapes inconsistent with each other        */
+  MV_ERR_UNSUPPORTED = 4,  /* valid request outside what the kernels implement  */
+  MV_ERR_WORKSPACE = 5,    /* workspace or mask buffer smaller than required    */
+  MV_ERR_HIP = 6,          /* a HIP runtime call or kernel launch failed        */
+  MV_ERR_STATE = 7         /* object not ready (e.g. mask not uploaded)         */
+} mv_status;
+
+/* Static name of a status code. */
+const char* mv_status_string(mv_status s);
+/* Message describing the last failure on the calling thread ("" if none). */
+const char* mv_last_error(void);
+/* Library ABI version: (major << 16) | minor. */
+int32_t mv_version(void);
+
+/* ---------------------------------------------------------------------------
+ * Eviction records and the view mask
+ *
+ * A rollout's record is its physical token sequence (the depth-first tape
+ * H_full) plus the ordered edits (J_k, E_k) (Appendix E.1, "one record per
+ * rollout"; Definition "trajectory tree", Appendix B.1).  The live view of row
+ * i is the physical prefix with exactly the edits fired by then applied
+ * (Eq. "live-view", Section 3.2).  Positions are physical rows; the logits
+ * for token y_t come from row t-1, and edit k is applied before row J_k is
+ * evaluated: rows < J_k see E_k, rows >= J_k do not (this reproduces the
+ * per-leaf prefixes of Table "running-prefixes").
+ *
+ * Equivalently every key j has the lifetime [j, omega(j)) of Eq.
+ * "4d-mask-def" (Section 4.2), with omega(j) = J_k if j is in E_k and the end
+ * of its trajectory otherwise: row i sees key j iff j <= i < omega(j).
+ * Several trajectories are packed back to back; a row never sees another
+ * trajectory's keys.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t begin, end;            /* half-open physical positions [begin, end) */
+} mv_span;
+
+typedef struct {
+  int32_t junction;              /* J_k: first row evaluated under the post-edit view */
+  int32_t n_evict;               /* number of spans in E_k (0 allowed)               */
+  const mv_span* evict;          /* E_k: sorted, disjoint spans inside
+                                    [trajectory begin, junction); every token
+                                    must still be live when the edit fires     */
+  mv_span summary;               /* metadata only (begin == end: none); summary
+                                    tokens are ordinary keys born at their row;
+                                    must lie in the trajectory and not meet E_k */
+} mv_edit;
+
+typedef struct {
+  int32_t begin, end;            /* physical rows of this trajectory             */
+  int32_t n_edits;
+  const mv_edit* edits;          /* strictly increasing junctions, begin < J < end */
+} mv_trajectory;
+
+typedef struct mv_view_mask mv_view_mask;   /* opaque */
+
+typedef struct {
+  int64_t visible_pairs;         /* P = sum_j (omega(j) - j): visible (row, key) pairs */
+  int32_t total_tokens;
+  int32_t max_view;              /* largest |View(i)|                                 */
+  int32_t n_segments;            /* maximal runs of consecutive keys sharing omega    */
+  int32_t tiles_full;            /* 128-row x 64-key tiles computed without masking  */
+  int32_t tiles_partial;         /* tiles computed with the per-element predicate    */
+  int32_t tiles_skipped;         /* causal tiles holding no visible pair              */
+  int32_t bwd_items;             /* key-tile work items of the dK/dV pass             */
+  int32_t bwd_partial_slots;     /* fp32 partial tiles the dK/dV pass reduces         */
+} mv_mask_stats;
+
+/*
+ * Build the key-lifetime array omega (Eq. "4d-mask-def") and the block-sparse
+ * tile schedules of the attention passes from the eviction records (host only,
+ * synchronous).  trajs[0..n_traj) must tile [0, total_tokens) in order.
+ * Errors: MV_ERR_INVALID_ARG (null/size), MV_ERR_BAD_RECORD (junction out of
+ * range or not increasing, span outside [begin, junction), overlapping spans,
+ * a token evicted twice, a summary meeting E_k).  *out is owned by the caller
+ * and released with mv_view_mask_free.
+ */
+mv_status mv_build_view_mask(const mv_trajectory* trajs, int32_t n_traj,
+                             int32_t total_tokens, mv_view_mask** out);
+
+/* Bytes of device memory the uploaded mask needs. */
+size_t mv_view_mask_device_bytes(const mv_view_mask* m);
+
+/*
+ * Copy the mask to a caller-owned device buffer (>= device_bytes, 256-byte
+ * aligned) on `stream`; the mask keeps the pointer, so the buffer must outlive
+ * every attention call using it.  Uploading again re-targets the mask.
+ */
+mv_status mv_view_mask_upload(mv_view_mask* m, void* dev_buf, size_t bytes,
+                              hipStream_t stream);
+
+mv_status mv_view_mask_stats(const mv_view_mask* m, mv_mask_stats* out);
+
+/* Copy omega (int32[total_tokens], host memory) out of the mask. */
+mv_status mv_view_mask_death(const mv_view_mask* m, int32_t* host_out);
+
+/*
+ * Write the visibility bits the attention kernels act on for rows
+ * [row_begin, row_end): bit (j % 32) of word (i - row_begin) * ceil(T/32) + j/32
+ * is 1 iff the forward tile schedule visits key j for row i and the shared
+ * predicate admits it.  Device variant: dev_bits is device memory, enqueued on
+ * `stream` (mask must be uploaded).  Host variant: the same schedule walk and
+ * predicate on the CPU.  Both exist so that the schedule and the predicate can
+ * be checked bit-exactly against an independent replay of the record.
+ */
+mv_status mv_view_mask_materialize(const mv_view_mask* m, int32_t row_begin,
+                                   int32_t row_end, uint32_t* dev_bits,
+                                   hipStream_t stream);
+mv_status mv_view_mask_materialize_host(const mv_view_mask* m, int32_t row_begin,
+                                        int32_t row_end, uint32_t* host_bits);
+
+void mv_view_mask_free(mv_view_mask* m);
+
+/* ---------------------------------------------------------------------------
+ * View-masked attention (Section 4.2, the packed single forward; its
+ * equivalence with one causal forward per branch is Theorem "hard_equiv",
+ * Section 4.3 and Appendix C.3).
+ *
+ * Layouts (row-major, bf16): Q, O, dO, dQ are [total_tokens, n_heads_q,
+ * head_dim]; K, V, dK, dV are [total_tokens, n_heads_kv, head_dim].  Query
+ * head h reads KV head h / (n_heads_q / n_heads_kv).  LSE is fp32
+ * [n_heads_q, total_tokens], natural log.  Q and K are taken as given
+ * (already position-encoded).  head_dim in {64, 128}.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t total_tokens;          /* must equal the mask's                          */
+  int32_t n_heads_q, n_heads_kv; /* n_heads_q % n_heads_kv == 0                    */
+  int32_t head_dim;              /* 64 or 128                                      */
+  float softmax_scale;           /* <= 0 selects 1/sqrt(head_dim)                  */
+} mv_attn_shape;
+
+/*
+ * O_i = sum_{j in View(i)} softmax_j(scale * q_i.k_j) v_j and
+ * LSE_i = log sum_{j in View(i)} exp(scale * q_i.k_j), for every row and head.
+ * Tiles with no visible pair are skipped; tiles that are entirely visible skip
+ * the per-element predicate.
+ */
+mv_status mv_attn_fwd(const mv_view_mask* m, const mv_attn_shape* shape,
+                      const void* q, const void* k, const void* v,
+                      void* o, float* lse, hipStream_t stream);
+
+/* Workspace bytes of mv_attn_bwd (row statistics and fp32 dK/dV partials). */
+size_t mv_attn_bwd_workspace_bytes(const mv_view_mask* m, const mv_attn_shape* shape);
+
+/*
+ * Gradients of sum_i <dO_i, O_i> with respect to Q, K and V under the same
+ * views, from the forward's O and LSE: one backward for the whole trajectory
+ * (the 4D method's single backward, Section 4.3 "Cost and deployment splits").
+ * dQ, dK, dV are fully overwritten.  Deterministic: no atomics.
+ */
+mv_status mv_attn_bwd(const mv_view_mask* m, const mv_attn_shape* shape,
+                      const void* q, const void* k, const void* v,
+                      const void* o, const void* dout, const float* lse,
+                      void* dq, void* dk, void* dv,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Fused LM-head token log-prob, importance ratio and clip.
+ *
+ * z_t = W h_t is never stored.  logp_t = z_{t,y_t} - logsumexp_v z_tv is the
+ * log-prob the training pass recomputes under the live view (the left term
+ * of Eq. "logdiff", Section 3.1); ratio_t = exp(logp_t - logp_old_t) and
+ * clipped_t = clamp(ratio_t, 1 - eps_low, 1 + eps_high) are the GRPO
+ * importance ratio and its clip (Appendix C, "Pitfall A, RL view";
+ * Appendix F).  target[t] == -1 marks a token without loss: logp 0, ratio 1,
+ * clipped 1, zero gradient.  Targets must lie in [-1, vocab).
+ *
+ * Layouts: hidden bf16 [n_tokens, hidden]; weight bf16 [vocab, hidden];
+ * target int32 [n_tokens]; per-token fp32 vectors [n_tokens].
+ * Supported: hidden % 64 == 0.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t n_tokens, hidden, vocab;
+  float eps_low, eps_high;       /* clip range (e.g. 0.2 / 0.2, or 0.2 / 0.28)      */
+} mv_logprob_shape;
+
+size_t mv_token_logprob_workspace_bytes(const mv_logprob_shape* shape);
+
+/*
+ * logp and lse are required; ratio and clipped are written iff logp_old is
+ * non-null (then both must be non-null).
+ */
+mv_status mv_token_logprob(const mv_logprob_shape* shape, const void* hidden,
+                           const void* weight, const int32_t* target,
+                           const float* logp_old, float* logp, float* ratio,
+                           float* clipped, float* lse, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
+size_t mv_token_logprob_bwd_workspace_bytes(const mv_logprob_shape* shape);
+
+/*
+ * dhidden_t = dlogp_t * (W[y_t] - sum_v softmax(z_t)_v W[v])  (bf16 out), from
+ * the forward's lse; logits are recomputed, never read back.
+ */
+mv_status mv_token_logprob_bwd(const mv_logprob_shape* shape, const void* hidden,
+                               const void* weight, const int32_t* target,
+                               const float* lse, const float* dlogp, void* dhidden,
+                               void* workspace, size_t workspace_bytes,
+                               hipStream_t stream);
+
+/*
+ * dlogp_t = d/dlogp_t [ -scale * min(ratio_t A_t, clamp(ratio_t) A_t) ]: the
+ * clipped surrogate's gradient, zero where the clipped branch is active.
+ */
+mv_status mv_ppo_clip_dlogp(int32_t n, const float* ratio, const float* adv,
+                            float eps_low, float eps_high, float scale,
+                            float* dlogp, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MV_H_ */

@@ -42,12 +42,15 @@ def _check(q, k, v):
 
 def logittree(trajs: Sequence, q, k, v, scale: Optional[float] = None,
               dtype=torch.float64, dout=None, heads: Optional[Sequence[int]] = None,
-              row_chunk: int = 4096):
+              row_chunk: int = 4096, row_range: Optional[tuple] = None):
     """Forward (and backward when ``dout`` is given) in LogitTree form.
 
     ``heads`` restricts the computation to a subset of query heads (their KV
-    heads follow); rows of other heads are left zero.  Returns
-    (O, LSE) or (O, LSE, dQ, dK, dV), all in ``dtype``.
+    heads follow); ``row_range`` = (r0, r1) keeps only the loss of rows in
+    [r0, r1), exactly as a per-branch loss mask would.  Entries outside the
+    selection are left zero.  Returns (O, LSE) or (O, LSE, dQ, dK, dV), all in
+    ``dtype``.  Because row i only ever reads View(i), restricting the rows to
+    those that see key j yields the exact dK_j and dV_j.
     """
     _check(q, k, v)
     T, hq, d = q.shape
@@ -71,11 +74,15 @@ def logittree(trajs: Sequence, q, k, v, scale: Optional[float] = None,
     O = torch.zeros(T, hq, d, dtype=dtype)
     LSE = torch.zeros(hq, T, dtype=dtype)
     _, trajs = _views.packed(trajs)
+    r0, r1 = (0, T) if row_range is None else (int(row_range[0]), int(row_range[1]))
     for traj in trajs:
+        if traj.end <= r0 or traj.begin >= r1:
+            continue
         for first, end, before in _views.branch_layers(traj):
             nb = len(before)
-            for c0 in range(first, end, row_chunk):
-                c1 = min(end, c0 + row_chunk)
+            lo, hi = max(first, r0), min(end, r1)
+            for c0 in range(lo, hi, row_chunk):
+                c1 = min(hi, c0 + row_chunk)
                 keys = torch.tensor(before + list(range(first, c1)), dtype=torch.long)
                 qs = qf[c0:c1][:, hsel]                 # [n, h, d]
                 ks = kf[keys][:, ksel]                   # [m, h, d]
@@ -174,3 +181,47 @@ def rows(trajs: Sequence, q, k, v, sample_rows: Sequence[int],
             if r == last:
                 break
     return O, LSE
+
+
+def row_grads(trajs: Sequence, q, k, v, dout, sample_rows: Sequence[int],
+              heads: Optional[Sequence[int]] = None, scale: Optional[float] = None,
+              dtype=torch.float64):
+    """dQ of selected rows, each from its own view.
+
+    Row i's output depends on q_i only through its own softmax over View(i),
+    so dQ_i = scale * sum_j P_ij (dP_ij - D_i) k_j with dP_ij = <dO_i, v_j> and
+    D_i = <dO_i, O_i> needs nothing but that view.
+    Returns dQ [len(rows), len(heads), d].
+    """
+    _check(q, k, v)
+    T, hq, d = q.shape
+    G = hq // k.shape[1]
+    heads = list(range(hq)) if heads is None else list(heads)
+    scale = 1.0 / math.sqrt(d) if scale is None or scale <= 0 else scale
+    want = {}
+    for i, r in enumerate(sample_rows):
+        want.setdefault(int(r), []).append(i)
+    dQ = torch.zeros(len(sample_rows), len(heads), d, dtype=dtype)
+    _, trajs = _views.packed(trajs)
+    for traj in trajs:
+        todo = [r for r in want if traj.begin <= r < traj.end]
+        if not todo:
+            continue
+        last = max(todo)
+        for r, lv in _views.replay(traj):
+            if r in want:
+                keys = torch.tensor(list(lv), dtype=torch.long)
+                for hi, h in enumerate(heads):
+                    kk = k[keys, h // G].to(dtype)
+                    vv = v[keys, h // G].to(dtype)
+                    s = (kk @ q[r, h].to(dtype)) * scale
+                    p = torch.softmax(s, 0)
+                    do = dout[r, h].to(dtype)
+                    dp = vv @ do
+                    Di = torch.dot(p @ vv, do)
+                    g = scale * ((p * (dp - Di)) @ kk)
+                    for i in want[r]:
+                        dQ[i, hi] = g
+            if r == last:
+                break
+    return dQ

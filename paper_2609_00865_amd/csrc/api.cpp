@@ -1,0 +1,228 @@
+// C ABI of libmv: argument validation, workspace sizing and kernel dispatch.
+// Validation is complete before anything is enqueued, so a failing call
+// launches nothing.
+#include <cmath>
+#include <cstring>
+#include <sstream>
+
+#include "mv_internal.h"
+
+namespace mv {
+
+thread_local std::string g_last_error;
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+
+hipError_t launch_attn_fwd(const mv_view_mask& m, int Hq, int Hkv, int D, float scale,
+                           const void* q, const void* k, const void* v, void* o, float* lse,
+                           hipStream_t stream);
+hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float scale,
+                           const void* q, const void* k, const void* v, const void* o,
+                           const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                           void* ws, hipStream_t stream);
+size_t attn_bwd_ws_bytes(const mv_view_mask& m, int Hq, int Hkv, int D);
+hipError_t launch_materialize(const mv_view_mask& m, int row_begin, int row_end, uint32_t* bits,
+                              hipStream_t stream);
+hipError_t launch_ppo_clip(int n, const float* ratio, const float* adv, float eps_lo,
+                           float eps_hi, float scale, float* out, hipStream_t stream);
+size_t logprob_fwd_ws_bytes(int T, int H, int V);
+size_t logprob_bwd_ws_bytes(int T, int H, int V);
+hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, const void* hidden,
+                              const void* weight, const int32_t* target, const float* logp_old,
+                              float* logp, float* ratio, float* clipped, float* lse, void* ws,
+                              hipStream_t stream);
+hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const void* weight,
+                              const int32_t* target, const float* lse, const float* dlogp,
+                              void* dhidden, void* ws, hipStream_t stream);
+
+}  // namespace mv
+
+namespace {
+
+mv_status fail(mv_status s, const std::string& msg) {
+  mv::set_error(msg);
+  return s;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+mv_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return MV_OK;
+  return fail(MV_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+mv_status check_attn(const mv_view_mask* m, const mv_attn_shape* s) {
+  if (m == nullptr || s == nullptr) return fail(MV_ERR_INVALID_ARG, "null mask or shape");
+  if (s->total_tokens != m->T) {
+    std::ostringstream os;
+    os << "shape.total_tokens " << s->total_tokens << " != mask total_tokens " << m->T;
+    return fail(MV_ERR_SHAPE, os.str());
+  }
+  if (s->n_heads_q <= 0 || s->n_heads_kv <= 0 || s->n_heads_q % s->n_heads_kv != 0)
+    return fail(MV_ERR_SHAPE, "n_heads_q must be a positive multiple of n_heads_kv");
+  if (s->head_dim != 64 && s->head_dim != 128)
+    return fail(MV_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (!std::isfinite(s->softmax_scale)) return fail(MV_ERR_INVALID_ARG, "softmax_scale not finite");
+  return MV_OK;
+}
+
+mv_status check_uploaded(const mv_view_mask* m) {
+  if (m->dev == nullptr) return fail(MV_ERR_STATE, "mask has not been uploaded");
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(MV_ERR_HIP, "hipGetDevice failed");
+  if (dev != m->device) return fail(MV_ERR_STATE, "mask was uploaded to another device");
+  return MV_OK;
+}
+
+float attn_scale(const mv_attn_shape* s) {
+  return s->softmax_scale > 0.f ? s->softmax_scale : 1.f / std::sqrt(float(s->head_dim));
+}
+
+mv_status check_ptrs(std::initializer_list<const void*> ps) {
+  for (const void* p : ps) {
+    if (p == nullptr) return fail(MV_ERR_INVALID_ARG, "null device pointer");
+    if (!aligned16(p)) return fail(MV_ERR_INVALID_ARG, "device pointer not 16-byte aligned");
+  }
+  return MV_OK;
+}
+
+mv_status check_logprob(const mv_logprob_shape* s) {
+  if (s == nullptr) return fail(MV_ERR_INVALID_ARG, "null shape");
+  if (s->n_tokens < 0 || s->hidden <= 0 || s->vocab <= 0)
+    return fail(MV_ERR_SHAPE, "n_tokens >= 0, hidden > 0, vocab > 0 required");
+  if (s->hidden % 64 != 0) return fail(MV_ERR_UNSUPPORTED, "hidden must be a multiple of 64");
+  if (int64_t(s->n_tokens) * s->hidden >= (int64_t(1) << 31) ||
+      int64_t(s->vocab) * s->hidden >= (int64_t(1) << 31))
+    return fail(MV_ERR_UNSUPPORTED, "hidden/weight larger than 2^31 elements");
+  if (!(s->eps_low >= 0.f && s->eps_low < 1.f && s->eps_high >= 0.f && std::isfinite(s->eps_high)))
+    return fail(MV_ERR_INVALID_ARG, "clip range must satisfy 0 <= eps_low < 1, 0 <= eps_high");
+  return MV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mv_status_string(mv_status s) {
+  switch (s) {
+    case MV_OK: return "MV_OK";
+    case MV_ERR_INVALID_ARG: return "MV_ERR_INVALID_ARG";
+    case MV_ERR_BAD_RECORD: return "MV_ERR_BAD_RECORD";
+    case MV_ERR_SHAPE: return "MV_ERR_SHAPE";
+    case MV_ERR_UNSUPPORTED: return "MV_ERR_UNSUPPORTED";
+    case MV_ERR_WORKSPACE: return "MV_ERR_WORKSPACE";
+    case MV_ERR_HIP: return "MV_ERR_HIP";
+    case MV_ERR_STATE: return "MV_ERR_STATE";
+  }
+  return "MV_ERR_UNKNOWN";
+}
+
+const char* mv_last_error(void) { return mv::g_last_error.c_str(); }
+
+int32_t mv_version(void) { return (1 << 16) | 0; }
+
+mv_status mv_view_mask_materialize(const mv_view_mask* m, int32_t row_begin, int32_t row_end,
+                                   uint32_t* dev_bits, hipStream_t stream) {
+  if (m == nullptr || dev_bits == nullptr) return fail(MV_ERR_INVALID_ARG, "null argument");
+  if (row_begin < 0 || row_end > m->T || row_begin > row_end)
+    return fail(MV_ERR_INVALID_ARG, "row range outside [0, total_tokens]");
+  if (mv_status s = check_uploaded(m); s != MV_OK) return s;
+  return hip_status(mv::launch_materialize(*m, row_begin, row_end, dev_bits, stream),
+                    "materialize launch");
+}
+
+mv_status mv_attn_fwd(const mv_view_mask* m, const mv_attn_shape* s, const void* q, const void* k,
+                      const void* v, void* o, float* lse, hipStream_t stream) {
+  if (mv_status st = check_attn(m, s); st != MV_OK) return st;
+  if (mv_status st = check_ptrs({q, k, v, o, lse}); st != MV_OK) return st;
+  if (mv_status st = check_uploaded(m); st != MV_OK) return st;
+  return hip_status(mv::launch_attn_fwd(*m, s->n_heads_q, s->n_heads_kv, s->head_dim,
+                                        attn_scale(s), q, k, v, o, lse, stream),
+                    "attention forward launch");
+}
+
+size_t mv_attn_bwd_workspace_bytes(const mv_view_mask* m, const mv_attn_shape* s) {
+  if (m == nullptr || s == nullptr || check_attn(m, s) != MV_OK) return 0;
+  return mv::attn_bwd_ws_bytes(*m, s->n_heads_q, s->n_heads_kv, s->head_dim);
+}
+
+mv_status mv_attn_bwd(const mv_view_mask* m, const mv_attn_shape* s, const void* q, const void* k,
+                      const void* v, const void* o, const void* dout, const float* lse, void* dq,
+                      void* dk, void* dv, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (mv_status st = check_attn(m, s); st != MV_OK) return st;
+  if (mv_status st = check_ptrs({q, k, v, o, dout, lse, dq, dk, dv, ws}); st != MV_OK) return st;
+  const size_t need = mv::attn_bwd_ws_bytes(*m, s->n_heads_q, s->n_heads_kv, s->head_dim);
+  if (ws_bytes < need) {
+    std::ostringstream os;
+    os << "attention backward workspace has " << ws_bytes << " bytes, needs " << need;
+    return fail(MV_ERR_WORKSPACE, os.str());
+  }
+  if (mv_status st = check_uploaded(m); st != MV_OK) return st;
+  return hip_status(mv::launch_attn_bwd(*m, s->n_heads_q, s->n_heads_kv, s->head_dim,
+                                        attn_scale(s), q, k, v, o, dout, lse, dq, dk, dv, ws,
+                                        stream),
+                    "attention backward launch");
+}
+
+size_t mv_token_logprob_workspace_bytes(const mv_logprob_shape* s) {
+  if (check_logprob(s) != MV_OK) return 0;
+  return mv::logprob_fwd_ws_bytes(s->n_tokens, s->hidden, s->vocab);
+}
+
+mv_status mv_token_logprob(const mv_logprob_shape* s, const void* hidden, const void* weight,
+                           const int32_t* target, const float* logp_old, float* logp, float* ratio,
+                           float* clipped, float* lse, void* ws, size_t ws_bytes,
+                           hipStream_t stream) {
+  if (mv_status st = check_logprob(s); st != MV_OK) return st;
+  if (s->n_tokens == 0) return MV_OK;
+  if (mv_status st = check_ptrs({hidden, weight, ws}); st != MV_OK) return st;
+  if (target == nullptr || logp == nullptr || lse == nullptr)
+    return fail(MV_ERR_INVALID_ARG, "target, logp and lse are required");
+  if ((logp_old == nullptr) != (ratio == nullptr) || (ratio == nullptr) != (clipped == nullptr))
+    return fail(MV_ERR_INVALID_ARG, "logp_old, ratio and clipped must be all set or all null");
+  const size_t need = mv::logprob_fwd_ws_bytes(s->n_tokens, s->hidden, s->vocab);
+  if (ws_bytes < need) {
+    std::ostringstream os;
+    os << "log-prob workspace has " << ws_bytes << " bytes, needs " << need;
+    return fail(MV_ERR_WORKSPACE, os.str());
+  }
+  return hip_status(mv::launch_logprob_fwd(s->n_tokens, s->hidden, s->vocab, s->eps_low,
+                                           s->eps_high, hidden, weight, target, logp_old, logp,
+                                           ratio, clipped, lse, ws, stream),
+                    "log-prob forward launch");
+}
+
+size_t mv_token_logprob_bwd_workspace_bytes(const mv_logprob_shape* s) {
+  if (check_logprob(s) != MV_OK) return 0;
+  return mv::logprob_bwd_ws_bytes(s->n_tokens, s->hidden, s->vocab);
+}
+
+mv_status mv_token_logprob_bwd(const mv_logprob_shape* s, const void* hidden, const void* weight,
+                               const int32_t* target, const float* lse, const float* dlogp,
+                               void* dhidden, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (mv_status st = check_logprob(s); st != MV_OK) return st;
+  if (s->n_tokens == 0) return MV_OK;
+  if (mv_status st = check_ptrs({hidden, weight, dhidden, ws}); st != MV_OK) return st;
+  if (target == nullptr || lse == nullptr || dlogp == nullptr)
+    return fail(MV_ERR_INVALID_ARG, "target, lse and dlogp are required");
+  const size_t need = mv::logprob_bwd_ws_bytes(s->n_tokens, s->hidden, s->vocab);
+  if (ws_bytes < need) {
+    std::ostringstream os;
+    os << "log-prob backward workspace has " << ws_bytes << " bytes, needs " << need;
+    return fail(MV_ERR_WORKSPACE, os.str());
+  }
+  return hip_status(mv::launch_logprob_bwd(s->n_tokens, s->hidden, s->vocab, hidden, weight,
+                                           target, lse, dlogp, dhidden, ws, stream),
+                    "log-prob backward launch");
+}
+
+mv_status mv_ppo_clip_dlogp(int32_t n, const float* ratio, const float* adv, float eps_low,
+                            float eps_high, float scale, float* dlogp, hipStream_t stream) {
+  if (n < 0) return fail(MV_ERR_INVALID_ARG, "n must be >= 0");
+  if (n > 0 && (ratio == nullptr || adv == nullptr || dlogp == nullptr))
+    return fail(MV_ERR_INVALID_ARG, "null pointer");
+  return hip_status(mv::launch_ppo_clip(n, ratio, adv, eps_low, eps_high, scale, dlogp, stream),
+                    "ppo clip launch");
+}
+
+}  // extern "C"

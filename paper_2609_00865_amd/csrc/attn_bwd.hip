@@ -1,0 +1,529 @@
+// View-masked attention backward on gfx950: one backward for the packed
+// trajectory instead of one per branch (Section 4.3, "Cost and deployment
+// splits").  Three passes, all recomputing P from the forward's LSE:
+//
+//  1. D_i = <dO_i, O_i> per row and head (HBM-bound, tiny).
+//  2. dQ: per 128-row query tile and head, over the forward's tile list:
+//     S^T = K Q^T, dP^T = V dO^T, dS^T = P^T o (dP^T - D), dQ^T += K^T dS^T.
+//  3. dK/dV: per 128-key tile and KV head, over the contiguous row range that
+//     sees some key of the tile, for every query head of the GQA group:
+//     S = Q K^T, dV^T += dO^T P, dP = dO V^T, dK^T += Q^T dS.
+//     Long ranges are cut into items that write fp32 partial tiles; a reduce
+//     pass sums them in a fixed order (deterministic, no atomics).
+// All stores write whole 16-byte or 8-byte runs of a row.
+#include "mv_device.h"
+#include "mv_predicate.h"
+
+namespace mv {
+
+namespace {
+constexpr float kLog2e = 1.4426950408889634f;
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+}  // namespace
+
+struct BwdArgs {
+  const u16* q;
+  const u16* k;
+  const u16* v;
+  const u16* o;
+  const u16* dout;
+  const float* lse;
+  u16* dq;
+  u16* dk;
+  u16* dv;
+  float* Dd;       // [Hq, T]
+  float* partial;  // [n_slots, Hkv, 2, 128, D]
+  mv_mask_dev mask;
+  int T, Hq, Hkv, n_qt, n_items;
+  float scale, scale_log2;
+};
+
+// ---------------------------------------------------------------------------
+// 1. D = rowsum(dO * O)
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
+  const int64_t gid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (gid >= int64_t(a.T) * a.Hq) return;
+  const int i = int(gid / a.Hq), h = int(gid % a.Hq);
+  const u16* op = a.o + size_t(gid) * D;
+  const u16* dp = a.dout + size_t(gid) * D;
+  float acc = 0.f;
+#pragma unroll
+  for (int c = 0; c < D / 8; ++c) {
+    const uint4 x = ld16(op + c * 8), y = ld16(dp + c * 8);
+    const uint32_t xs[4] = {x.x, x.y, x.z, x.w}, ys[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      acc += bf16_to_f32(xs[w] & 0xffff) * bf16_to_f32(ys[w] & 0xffff);
+      acc += bf16_to_f32(xs[w] >> 16) * bf16_to_f32(ys[w] >> 16);
+    }
+  }
+  a.Dd[size_t(h) * a.T + i] = acc;
+}
+
+// Transposed 16-bit pair store: rows (r0, r0+1) x 8 columns from two 16-byte
+// row chunks into a [col][row] LDS tile whose row positions are permuted by
+// perm_col (so that MFMA operand reads are single 16-byte loads).
+template <int PAD>
+__device__ __forceinline__ void store_pair_t(u16* dst, int r0, int c0, const uint4& lo4,
+                                             const uint4& hi4) {
+  const int col = perm_col(r0);
+  const uint32_t lo[4] = {lo4.x, lo4.y, lo4.z, lo4.w}, hi[4] = {hi4.x, hi4.y, hi4.z, hi4.w};
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const uint32_t even = (lo[w] & 0xffffu) | (hi[w] << 16);
+    const uint32_t odd = (lo[w] >> 16) | (hi[w] & 0xffff0000u);
+    *reinterpret_cast<uint32_t*>(&dst[(c0 + 2 * w) * PAD + col]) = even;
+    *reinterpret_cast<uint32_t*>(&dst[(c0 + 2 * w + 1) * PAD + col]) = odd;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 2. dQ
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
+  constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
+  constexpr int KS = D / 16, DB = D / 32;
+  constexpr int RPAD = D + 8, TPAD = BK + 8;
+  constexpr int RLD = BK * D / 8 / 256;          // row-major V loads per thread
+  constexpr int PLD = (BK / 2) * (D / 8) / 256;  // K pair loads per thread
+
+  __shared__ __align__(16) u16 sK[BK * RPAD];
+  __shared__ __align__(16) u16 sV[BK * RPAD];
+  __shared__ __align__(16) u16 sKt[D * TPAD];
+  __shared__ __align__(16) int sOm[BK];
+
+  int xcd, local;
+  xcd_split(xcd, local);
+  const int qrank = (local / a.Hq) * kNumXcd + xcd;
+  const int h = local % a.Hq;
+  if (qrank >= a.n_qt) return;
+  const int qt = a.mask.qt_order[qrank];
+  const int hk = h / (a.Hq / a.Hkv);
+  const int T = a.T;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int c = lane & 31, g = lane >> 5;
+  const int qrow = qt * BQ + wave * 32 + c;
+  const bool qok = qrow < T;
+
+  bf16x8 qf[KS], df[KS];
+  {
+    const size_t off = (size_t(qok ? qrow : 0) * a.Hq + h) * D + g * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      qf[ks] = as_bf16x8(qok ? ld16(a.q + off + ks * 16) : make_uint4(0, 0, 0, 0));
+      df[ks] = as_bf16x8(qok ? ld16(a.dout + off + ks * 16) : make_uint4(0, 0, 0, 0));
+    }
+  }
+  const float lse2 = qok ? a.lse[size_t(h) * T + qrow] * kLog2e : 0.f;
+  const float Di = qok ? a.Dd[size_t(h) * T + qrow] : 0.f;
+
+  f32x16 acc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
+
+  const size_t kv_row = size_t(a.Hkv) * D;
+  const u16* kbase = a.k + size_t(hk) * D;
+  const u16* vbase = a.v + size_t(hk) * D;
+  uint4 vreg[RLD], kreg[PLD][2];
+  int omreg = 0;
+  auto load_tile = [&](int kt) {
+    const int j0 = kt * BK;
+#pragma unroll
+    for (int r = 0; r < RLD; ++r) {
+      const int idx = tid + r * 256;
+      const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
+      const int j = j0 + row;
+      vreg[r] = j < T ? ld16(vbase + size_t(j) * kv_row + col) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int r = 0; r < PLD; ++r) {
+      const int idx = tid + r * 256;
+      const int pp = idx % (BK / 2), cc = idx / (BK / 2);
+      const int j = j0 + 2 * pp;
+      kreg[r][0] = j < T ? ld16(kbase + size_t(j) * kv_row + cc * 8) : make_uint4(0, 0, 0, 0);
+      kreg[r][1] = j + 1 < T ? ld16(kbase + size_t(j + 1) * kv_row + cc * 8) : make_uint4(0, 0, 0, 0);
+    }
+    if (tid < BK) omreg = (j0 + tid < T) ? a.mask.omega[j0 + tid] : 0;
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int r = 0; r < RLD; ++r) {
+      const int idx = tid + r * 256;
+      const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
+      st16(&sV[row * RPAD + col], vreg[r]);
+    }
+#pragma unroll
+    for (int r = 0; r < PLD; ++r) {
+      const int idx = tid + r * 256;
+      const int pp = idx % (BK / 2), cc = idx / (BK / 2);
+      st16(&sK[(2 * pp) * RPAD + cc * 8], kreg[r][0]);
+      st16(&sK[(2 * pp + 1) * RPAD + cc * 8], kreg[r][1]);
+      store_pair_t<TPAD>(sKt, 2 * pp, cc * 8, kreg[r][0], kreg[r][1]);
+    }
+    if (tid < BK) sOm[tid] = omreg;
+  };
+
+  const int e0 = a.mask.q_ptr[qt], e1 = a.mask.q_ptr[qt + 1];
+  int ent = a.mask.k_list[e0];
+  load_tile(ent >> 1);
+  for (int e = e0; e < e1; ++e) {
+    const int kt = ent >> 1;
+    const bool full = ent & 1;
+    __syncthreads();
+    store_tile();
+    __syncthreads();
+    if (e + 1 < e1) {
+      ent = a.mask.k_list[e + 1];
+      load_tile(ent >> 1);
+    }
+    const int j0 = kt * BK;
+
+    f32x16 s[2], dp[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[kb][r] = 0.f;
+        dp[kb][r] = 0.f;
+      }
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int off = (kb * 32 + c) * RPAD + ks * 16 + g * 8;
+        s[kb] = mfma32(as_bf16x8(ld16(&sK[off])), qf[ks], s[kb]);
+        dp[kb] = mfma32(as_bf16x8(ld16(&sV[off])), df[ks], dp[kb]);
+      }
+    }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        int4 om = make_int4(0, 0, 0, 0);
+        if (!full) om = *reinterpret_cast<const int4*>(&sOm[kb * 32 + q4 * 8 + g * 4]);
+        const int omv[4] = {om.x, om.y, om.z, om.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int r = q4 * 4 + u;
+          float p = fast_exp2(s[kb][r] * a.scale_log2 - lse2);
+          if (!full) {
+            const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
+            if (!mv_visible(qrow, key, omv[u])) p = 0.f;
+          }
+          s[kb][r] = p * (dp[kb][r] - Di);
+        }
+      }
+    }
+    bf16x8 dsf[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) dsf[ks] = to_operand(s[ks >> 1], (ks & 1) * 8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const bf16x8 kf = as_bf16x8(ld16(&sKt[(db * 32 + c) * TPAD + ks * 16 + g * 8]));
+        acc[db] = mfma32(kf, dsf[ks], acc[db]);
+      }
+  }
+
+  if (!qok) return;
+  u16* out = a.dq + (size_t(qrow) * a.Hq + h) * D;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int d0 = db * 32 + q4 * 8 + g * 4;
+      uint2 w;
+      w.x = pack2(acc[db][q4 * 4 + 0] * a.scale, acc[db][q4 * 4 + 1] * a.scale);
+      w.y = pack2(acc[db][q4 * 4 + 2] * a.scale, acc[db][q4 * 4 + 3] * a.scale);
+      *reinterpret_cast<uint2*>(out + d0) = w;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// 3. dK / dV
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
+  constexpr int BK = kBwdTileK, BQ = kBwdBlockQ;
+  constexpr int KS = D / 16, DB = D / 32;
+  constexpr int RPAD = D + 8, TPAD = BQ + 8;
+  constexpr int PLD = (BQ / 2) * (D / 8) / 256;  // row-pair loads per thread per tensor
+
+  __shared__ __align__(16) u16 sQ[BQ * RPAD];
+  __shared__ __align__(16) u16 sdO[BQ * RPAD];
+  __shared__ __align__(16) u16 sQt[D * TPAD];
+  __shared__ __align__(16) u16 sdOt[D * TPAD];
+  __shared__ __align__(16) float sL[BQ];
+  __shared__ __align__(16) float sD[BQ];
+
+  int xcd, local;
+  xcd_split(xcd, local);
+  const int w = (local / a.Hkv) * kNumXcd + xcd;
+  const int hk = local % a.Hkv;
+  if (w >= a.n_items) return;
+  const int kt = a.mask.bwd_items[4 * w + 0];
+  const int qb0 = a.mask.bwd_items[4 * w + 1];
+  const int qb1 = a.mask.bwd_items[4 * w + 2];
+  const int slot = a.mask.bwd_items[4 * w + 3];
+  const int om_min = a.mask.bwd_tiles[4 * kt + 0];
+  const int T = a.T, G = a.Hq / a.Hkv;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int c = lane & 31, g = lane >> 5;
+  const int j0 = kt * BK, j1 = min(T, j0 + BK);
+  const int key = j0 + wave * 32 + c;
+  const bool kok = key < T;
+  const int om = kok ? a.mask.omega[key] : 0;
+
+  bf16x8 kf[KS], vf[KS];
+  {
+    const size_t off = (size_t(kok ? key : 0) * a.Hkv + hk) * D + g * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      kf[ks] = as_bf16x8(kok ? ld16(a.k + off + ks * 16) : make_uint4(0, 0, 0, 0));
+      vf[ks] = as_bf16x8(kok ? ld16(a.v + off + ks * 16) : make_uint4(0, 0, 0, 0));
+    }
+  }
+  f32x16 dk[DB], dv[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      dk[db][r] = 0.f;
+      dv[db][r] = 0.f;
+    }
+
+  const size_t q_row = size_t(a.Hq) * D;
+  uint4 qreg[PLD][2], dreg[PLD][2];
+  float lreg = 0.f, dreg1 = 0.f;
+  auto load_block = [&](int hh, int qb) {
+    const int i0 = qb * BQ;
+    const u16* qb_ = a.q + size_t(hh) * D;
+    const u16* db_ = a.dout + size_t(hh) * D;
+#pragma unroll
+    for (int r = 0; r < PLD; ++r) {
+      const int idx = tid + r * 256;
+      const int pp = idx % (BQ / 2), cc = idx / (BQ / 2);
+      const int i = i0 + 2 * pp;
+      const uint4 z = make_uint4(0, 0, 0, 0);
+      qreg[r][0] = i < T ? ld16(qb_ + size_t(i) * q_row + cc * 8) : z;
+      qreg[r][1] = i + 1 < T ? ld16(qb_ + size_t(i + 1) * q_row + cc * 8) : z;
+      dreg[r][0] = i < T ? ld16(db_ + size_t(i) * q_row + cc * 8) : z;
+      dreg[r][1] = i + 1 < T ? ld16(db_ + size_t(i + 1) * q_row + cc * 8) : z;
+    }
+    if (tid < BQ) {
+      const int i = i0 + tid;
+      lreg = i < T ? a.lse[size_t(hh) * T + i] * kLog2e : 0.f;
+      dreg1 = i < T ? a.Dd[size_t(hh) * T + i] : 0.f;
+    }
+  };
+  auto store_block = [&]() {
+#pragma unroll
+    for (int r = 0; r < PLD; ++r) {
+      const int idx = tid + r * 256;
+      const int pp = idx % (BQ / 2), cc = idx / (BQ / 2);
+      st16(&sQ[(2 * pp) * RPAD + cc * 8], qreg[r][0]);
+      st16(&sQ[(2 * pp + 1) * RPAD + cc * 8], qreg[r][1]);
+      st16(&sdO[(2 * pp) * RPAD + cc * 8], dreg[r][0]);
+      st16(&sdO[(2 * pp + 1) * RPAD + cc * 8], dreg[r][1]);
+      store_pair_t<TPAD>(sQt, 2 * pp, cc * 8, qreg[r][0], qreg[r][1]);
+      store_pair_t<TPAD>(sdOt, 2 * pp, cc * 8, dreg[r][0], dreg[r][1]);
+    }
+    if (tid < BQ) {
+      sL[tid] = lreg;
+      sD[tid] = dreg1;
+    }
+  };
+
+  const int nqb = qb1 - qb0;
+  const int steps = nqb * G;
+  const int h0 = hk * G;
+  load_block(h0, qb0);
+  for (int st = 0; st < steps; ++st) {
+    const int hh = h0 + st / nqb;
+    const int qb = qb0 + st % nqb;
+    (void)hh;
+    __syncthreads();
+    store_block();
+    __syncthreads();
+    if (st + 1 < steps) load_block(h0 + (st + 1) / nqb, qb0 + (st + 1) % nqb);
+    const int i0 = qb * BQ;
+    const bool full = (i0 >= j1 - 1) && (i0 + BQ <= om_min);
+
+    f32x16 s[2], dp[2];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[mb][r] = 0.f;
+        dp[mb][r] = 0.f;
+      }
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int off = (mb * 32 + c) * RPAD + ks * 16 + g * 8;
+        s[mb] = mfma32(as_bf16x8(ld16(&sQ[off])), kf[ks], s[mb]);
+        dp[mb] = mfma32(as_bf16x8(ld16(&sdO[off])), vf[ks], dp[mb]);
+      }
+    }
+    // P and dS in place; rows of s/dp are queries mb*32 + q4*8 + g*4 + u
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int qo = mb * 32 + q4 * 8 + g * 4;
+        const float4 l4 = *reinterpret_cast<const float4*>(&sL[qo]);
+        const float4 d4 = *reinterpret_cast<const float4*>(&sD[qo]);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dd[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int r = q4 * 4 + u;
+          float p = fast_exp2(s[mb][r] * a.scale_log2 - lv[u]);
+          if (!full && !mv_visible(i0 + qo + u, key, om)) p = 0.f;
+          s[mb][r] = p;
+          dp[mb][r] = p * (dp[mb][r] - dd[u]);
+        }
+      }
+    }
+    bf16x8 pf[4], dsf[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      pf[ks] = to_operand(s[ks >> 1], (ks & 1) * 8);
+      dsf[ks] = to_operand(dp[ks >> 1], (ks & 1) * 8);
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int off = (db * 32 + c) * TPAD + ks * 16 + g * 8;
+        dv[db] = mfma32(as_bf16x8(ld16(&sdOt[off])), pf[ks], dv[db]);
+        dk[db] = mfma32(as_bf16x8(ld16(&sQt[off])), dsf[ks], dk[db]);
+      }
+  }
+
+  if (!kok) return;
+  if (slot < 0) {
+    u16* pk = a.dk + (size_t(key) * a.Hkv + hk) * D;
+    u16* pv = a.dv + (size_t(key) * a.Hkv + hk) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d0 = db * 32 + q4 * 8 + g * 4;
+        uint2 wk, wv;
+        wk.x = pack2(dk[db][q4 * 4 + 0] * a.scale, dk[db][q4 * 4 + 1] * a.scale);
+        wk.y = pack2(dk[db][q4 * 4 + 2] * a.scale, dk[db][q4 * 4 + 3] * a.scale);
+        wv.x = pack2(dv[db][q4 * 4 + 0], dv[db][q4 * 4 + 1]);
+        wv.y = pack2(dv[db][q4 * 4 + 2], dv[db][q4 * 4 + 3]);
+        *reinterpret_cast<uint2*>(pk + d0) = wk;
+        *reinterpret_cast<uint2*>(pv + d0) = wv;
+      }
+  } else {
+    float* base = a.partial + (size_t(slot) * a.Hkv + hk) * 2 * BK * D;
+    float* pk = base + size_t(wave * 32 + c) * D;
+    float* pv = base + size_t(BK) * D + size_t(wave * 32 + c) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d0 = db * 32 + q4 * 8 + g * 4;
+        *reinterpret_cast<float4*>(pk + d0) =
+            make_float4(dk[db][q4 * 4 + 0] * a.scale, dk[db][q4 * 4 + 1] * a.scale,
+                        dk[db][q4 * 4 + 2] * a.scale, dk[db][q4 * 4 + 3] * a.scale);
+        *reinterpret_cast<float4*>(pv + d0) =
+            make_float4(dv[db][q4 * 4 + 0], dv[db][q4 * 4 + 1], dv[db][q4 * 4 + 2],
+                        dv[db][q4 * 4 + 3]);
+      }
+  }
+}
+
+// Sum the fp32 partial tiles of every split key tile in slot order.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(BwdArgs a, int n_red) {
+  constexpr int BK = kBwdTileK;
+  const int r = blockIdx.x / a.Hkv, hk = blockIdx.x % a.Hkv;
+  if (r >= n_red) return;
+  const int kt = a.mask.bwd_red[r];
+  const int first = a.mask.bwd_tiles[4 * kt + 2], n = a.mask.bwd_tiles[4 * kt + 3];
+  for (int e = threadIdx.x; e < 2 * BK * D / 4; e += blockDim.x) {
+    const int which = e / (BK * D / 4);
+    const int rem = e % (BK * D / 4);
+    const int kk = rem / (D / 4), d0 = (rem % (D / 4)) * 4;
+    const int key = kt * BK + kk;
+    if (key >= a.T) continue;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = 0; i < n; ++i) {
+      const float* p = a.partial + ((size_t(first + i) * a.Hkv + hk) * 2 + which) * BK * D +
+                       size_t(kk) * D + d0;
+      const float4 x = *reinterpret_cast<const float4*>(p);
+      s.x += x.x;
+      s.y += x.y;
+      s.z += x.z;
+      s.w += x.w;
+    }
+    u16* out = (which == 0 ? a.dk : a.dv) + (size_t(key) * a.Hkv + hk) * D + d0;
+    uint2 wv;
+    wv.x = pack2(s.x, s.y);
+    wv.y = pack2(s.z, s.w);
+    *reinterpret_cast<uint2*>(out) = wv;
+  }
+}
+
+size_t attn_bwd_ws_bytes(const mv_view_mask& m, int Hq, int Hkv, int D) {
+  return align256(size_t(Hq) * m.T * sizeof(float)) +
+         align256(size_t(m.n_slots) * Hkv * 2 * kBwdTileK * D * sizeof(float)) + 256;
+}
+
+hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float scale,
+                           const void* q, const void* k, const void* v, const void* o,
+                           const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                           void* ws, hipStream_t stream) {
+  BwdArgs a;
+  a.q = static_cast<const u16*>(q);
+  a.k = static_cast<const u16*>(k);
+  a.v = static_cast<const u16*>(v);
+  a.o = static_cast<const u16*>(o);
+  a.dout = static_cast<const u16*>(dout);
+  a.lse = lse;
+  a.dq = static_cast<u16*>(dq);
+  a.dk = static_cast<u16*>(dk);
+  a.dv = static_cast<u16*>(dv);
+  char* base = static_cast<char*>(ws);
+  base = reinterpret_cast<char*>((reinterpret_cast<uintptr_t>(base) + 255) & ~uintptr_t(255));
+  a.Dd = reinterpret_cast<float*>(base);
+  a.partial = reinterpret_cast<float*>(base + align256(size_t(Hq) * m.T * sizeof(float)));
+  a.mask = m.d;
+  a.T = m.T;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.n_qt = m.n_qt;
+  a.n_items = m.stats.bwd_items;
+  a.scale = scale;
+  a.scale_log2 = scale * kLog2e;
+
+  const int64_t rows = int64_t(m.T) * Hq;
+  const dim3 b256(256);
+  const dim3 g_pre(unsigned((rows + 255) / 256));
+  const int per_xcd_q = (m.n_qt + kNumXcd - 1) / kNumXcd;
+  const dim3 g_dq(per_xcd_q * Hq * kNumXcd);
+  const int per_xcd_kv = (a.n_items + kNumXcd - 1) / kNumXcd;
+  const dim3 g_kv(per_xcd_kv * Hkv * kNumXcd);
+  const int n_red = int(m.bwd_red.size());
+  const dim3 g_red(unsigned(std::max(1, n_red * Hkv)));
+  if (D == 128) {
+    hipLaunchKernelGGL(bwd_pre_kernel<128>, g_pre, b256, 0, stream, a);
+    hipLaunchKernelGGL(bwd_dkdv_kernel<128>, g_kv, b256, 0, stream, a);
+    if (n_red) hipLaunchKernelGGL(bwd_reduce_kernel<128>, g_red, b256, 0, stream, a, n_red);
+    hipLaunchKernelGGL(bwd_dq_kernel<128>, g_dq, b256, 0, stream, a);
+  } else {
+    hipLaunchKernelGGL(bwd_pre_kernel<64>, g_pre, b256, 0, stream, a);
+    hipLaunchKernelGGL(bwd_dkdv_kernel<64>, g_kv, b256, 0, stream, a);
+    if (n_red) hipLaunchKernelGGL(bwd_reduce_kernel<64>, g_red, b256, 0, stream, a, n_red);
+    hipLaunchKernelGGL(bwd_dq_kernel<64>, g_dq, b256, 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mv

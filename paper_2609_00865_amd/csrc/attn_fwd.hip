@@ -1,0 +1,247 @@
+// View-masked attention forward on gfx950.
+//
+// One workgroup = one 128-row query tile x one query head, 4 waves of 32 rows.
+// For each 64-key tile the schedule lists (Section 4.2's mask, block-sparse as
+// Appendix B.3 asks for), the block computes S^T = K Q^T with bf16 MFMA (keys
+// on the accumulator rows, one query per lane, so the softmax statistics of a
+// row stay inside a lane pair), applies the shared visibility predicate on
+// partial tiles only, updates the online softmax in base 2, and accumulates
+// O^T += V^T P^T with a second MFMA.  K is staged row-major and V transposed in
+// LDS; the next tile's global loads are in flight during the current tile's
+// math.  Query tiles are visited heaviest first and the heads of one query
+// tile are kept on one XCD so that GQA heads share K/V in that XCD's L2.
+#include "mv_device.h"
+#include "mv_predicate.h"
+
+namespace mv {
+
+struct FwdArgs {
+  const u16* q;
+  const u16* k;
+  const u16* v;
+  u16* o;
+  float* lse;
+  mv_mask_dev mask;
+  int T, Hq, Hkv, n_qt;
+  float scale_log2;
+};
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
+  constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
+  constexpr int KS = D / 16;          // MFMA k-steps over the head dimension
+  constexpr int DB = D / 32;          // 32-row blocks of O^T
+  constexpr int KPAD = D + 8;         // row stride of K in LDS (bf16)
+  constexpr int VPAD = BK + 8;        // row stride of V^T in LDS (bf16)
+  constexpr int KLD = BK * D / 8 / 256;        // 16-byte K loads per thread
+  constexpr int VLD = (BK / 2) * (D / 8) / 256;  // key pairs x 8-d chunks per thread
+  static_assert(KLD >= 1 && VLD >= 1, "tile too small for 256 threads");
+
+  __shared__ __align__(16) u16 sK[BK * KPAD];
+  __shared__ __align__(16) u16 sVt[D * VPAD];
+  __shared__ __align__(16) int sOm[BK];
+
+  int xcd, local;
+  xcd_split(xcd, local);
+  const int qrank = (local / a.Hq) * kNumXcd + xcd;
+  const int h = local % a.Hq;
+  if (qrank >= a.n_qt) return;
+  const int qt = a.mask.qt_order[qrank];
+  const int hk = h / (a.Hq / a.Hkv);
+  const int T = a.T;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int c = lane & 31, g = lane >> 5;
+  const int qrow = qt * BQ + wave * 32 + c;
+  const bool qok = qrow < T;
+
+  // Q^T as the B operand: lane holds query qrow, d = ks*16 + g*8 .. +8
+  bf16x8 qf[KS];
+  {
+    const u16* qp = a.q + (size_t(qok ? qrow : 0) * a.Hq + h) * D + g * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qf[ks] = as_bf16x8(qok ? ld16(qp + ks * 16) : make_uint4(0, 0, 0, 0));
+  }
+
+  f32x16 oacc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const size_t kv_row = size_t(a.Hkv) * D;
+  const u16* kbase = a.k + size_t(hk) * D;
+  const u16* vbase = a.v + size_t(hk) * D;
+
+  uint4 kreg[KLD], vreg[VLD][2];
+  int omreg = 0;
+  auto load_tile = [&](int kt) {
+    const int j0 = kt * BK;
+#pragma unroll
+    for (int r = 0; r < KLD; ++r) {
+      const int idx = tid + r * 256;
+      const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
+      const int j = j0 + row;
+      kreg[r] = j < T ? ld16(kbase + size_t(j) * kv_row + col) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int r = 0; r < VLD; ++r) {
+      const int idx = tid + r * 256;
+      const int pp = idx % (BK / 2), cc = idx / (BK / 2);
+      const int j = j0 + 2 * pp;
+      vreg[r][0] = j < T ? ld16(vbase + size_t(j) * kv_row + cc * 8) : make_uint4(0, 0, 0, 0);
+      vreg[r][1] = j + 1 < T ? ld16(vbase + size_t(j + 1) * kv_row + cc * 8) : make_uint4(0, 0, 0, 0);
+    }
+    if (tid < BK) omreg = (j0 + tid < T) ? a.mask.omega[j0 + tid] : 0;
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int r = 0; r < KLD; ++r) {
+      const int idx = tid + r * 256;
+      const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
+      st16(&sK[row * KPAD + col], kreg[r]);
+    }
+#pragma unroll
+    for (int r = 0; r < VLD; ++r) {
+      const int idx = tid + r * 256;
+      const int pp = idx % (BK / 2), cc = idx / (BK / 2);
+      const int col = perm_col(2 * pp);
+      const uint32_t* lo = reinterpret_cast<const uint32_t*>(&vreg[r][0]);
+      const uint32_t* hi = reinterpret_cast<const uint32_t*>(&vreg[r][1]);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        // d = cc*8 + 2w and cc*8 + 2w + 1; pair (key 2pp, key 2pp+1)
+        const uint32_t a0 = lo[w], a1 = hi[w];
+        const uint32_t even = (a0 & 0xffffu) | (a1 << 16);
+        const uint32_t odd = (a0 >> 16) | (a1 & 0xffff0000u);
+        *reinterpret_cast<uint32_t*>(&sVt[(cc * 8 + 2 * w) * VPAD + col]) = even;
+        *reinterpret_cast<uint32_t*>(&sVt[(cc * 8 + 2 * w + 1) * VPAD + col]) = odd;
+      }
+    }
+    if (tid < BK) sOm[tid] = omreg;
+  };
+
+  const int e0 = a.mask.q_ptr[qt], e1 = a.mask.q_ptr[qt + 1];
+  int ent = a.mask.k_list[e0];
+  load_tile(ent >> 1);
+  for (int e = e0; e < e1; ++e) {
+    const int kt = ent >> 1;
+    const bool full = ent & 1;
+    __syncthreads();
+    store_tile();
+    __syncthreads();
+    if (e + 1 < e1) {
+      ent = a.mask.k_list[e + 1];
+      load_tile(ent >> 1);
+    }
+    const int j0 = kt * BK;
+
+    // S^T for keys [kb*32, kb*32+32) of the tile
+    f32x16 s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 kf = as_bf16x8(ld16(&sK[(kb * 32 + c) * KPAD + ks * 16 + g * 8]));
+        s[kb] = mfma32(kf, qf[ks], s[kb]);
+      }
+    }
+
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        int4 om = make_int4(0, 0, 0, 0);
+        if (!full) om = *reinterpret_cast<const int4*>(&sOm[kb * 32 + q4 * 8 + g * 4]);
+        const int omv[4] = {om.x, om.y, om.z, om.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int r = q4 * 4 + u;
+          float x = s[kb][r] * a.scale_log2;
+          if (!full) {
+            const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
+            if (!mv_visible(qrow, key, omv[u])) x = -INFINITY;
+          }
+          s[kb][r] = x;
+          mx = fmaxf(mx, x);
+        }
+      }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = fast_exp2(m_run - m_use);
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(s[kb][r] - m_use);
+        s[kb][r] = p;
+        psum += p;
+      }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+
+    bf16x8 pf[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) pf[ks] = to_operand(s[ks >> 1], (ks & 1) * 8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const bf16x8 vf = as_bf16x8(ld16(&sVt[(db * 32 + c) * VPAD + ks * 16 + g * 8]));
+        oacc[db] = mfma32(vf, pf[ks], oacc[db]);
+      }
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (!qok) return;
+  const float inv = 1.f / l_tot;
+  u16* op = a.o + (size_t(qrow) * a.Hq + h) * D;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int d0 = db * 32 + q4 * 8 + g * 4;
+      uint2 w;
+      w.x = pack2(oacc[db][q4 * 4 + 0] * inv, oacc[db][q4 * 4 + 1] * inv);
+      w.y = pack2(oacc[db][q4 * 4 + 2] * inv, oacc[db][q4 * 4 + 3] * inv);
+      *reinterpret_cast<uint2*>(op + d0) = w;
+    }
+  if (g == 0) a.lse[size_t(h) * T + qrow] = (m_run + __log2f(l_tot)) * 0.69314718055994531f;
+}
+
+hipError_t launch_attn_fwd(const mv_view_mask& m, int Hq, int Hkv, int D, float scale,
+                           const void* q, const void* k, const void* v, void* o, float* lse,
+                           hipStream_t stream) {
+  FwdArgs a;
+  a.q = static_cast<const u16*>(q);
+  a.k = static_cast<const u16*>(k);
+  a.v = static_cast<const u16*>(v);
+  a.o = static_cast<u16*>(o);
+  a.lse = lse;
+  a.mask = m.d;
+  a.T = m.T;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.n_qt = m.n_qt;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  const int per_xcd = (m.n_qt + kNumXcd - 1) / kNumXcd;
+  const dim3 grid(per_xcd * Hq * kNumXcd), block(256);
+  if (D == 128)
+    hipLaunchKernelGGL(attn_fwd_kernel<128>, grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL(attn_fwd_kernel<64>, grid, block, 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace mv

@@ -1,0 +1,344 @@
+// Fused LM-head token log-prob, ratio and clip on gfx950.
+//
+// Forward: z = W h is produced 256 vocab rows x 256 tokens at a time by a bf16
+// MFMA tile engine and reduced in registers to a per-token (max, sum of
+// exp) over each wave's 128 vocab rows; the target logit is captured by the
+// one lane that owns it.  The full logits are never stored.  A combine pass
+// merges the partials into logsumexp and writes logp, ratio and the clipped
+// ratio (the GRPO ratio of Appendix C, "Pitfall A, RL view").
+//
+// Backward: the logits tile is recomputed and turned into
+// G_tv = g_t (onehot(y_t)_v - softmax(z_t)_v), stored once in bf16, and a
+// second pass of the same engine computes dH = G W (contraction over the
+// vocabulary).
+//
+// Tile engine: 256 threads, 4 waves in a 2 x 2 grid, each wave 128 rows of
+// the "A" side (vocab, or hidden for dH) x 128 tokens, MFMA 32x32x16 with
+// tokens on lanes.  The next 64-wide k slice is loaded into registers while
+// the current one is multiplied from LDS.
+#include "mv_device.h"
+
+namespace mv {
+
+namespace {
+constexpr int BA = 256, BT = 256, BKK = 64;
+constexpr int PAD = BKK + 8;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994531f;
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+int vocab_pad(int V) { return (V + BA - 1) / BA * BA; }
+}  // namespace
+
+enum { kModeLogits = 0, kModeGrad = 1, kModeDh = 2 };
+
+struct LmArgs {
+  const u16* h;       // [T, H]
+  const u16* w;       // [V, H]
+  const int32_t* tgt; // [T]
+  const float* lse;   // [T] (grad mode)
+  const float* g;     // [T] upstream dlogp (grad mode)
+  const u16* G;       // [T, Vp] (dH mode)
+  u16* Gout;          // [T, Vp] (grad mode)
+  u16* dh;            // [T, H] (dH mode)
+  float2* part;       // [T, n_chunks] (logits mode)
+  float* tlogit;      // [T] (logits mode)
+  int T, H, V, Vp, n_chunks;
+  int nA, nT;         // tiles along the A side and along tokens
+};
+
+template <int MODE>
+__global__ __launch_bounds__(256, 1) void lm_gemm_kernel(LmArgs a) {
+  __shared__ __align__(16) u16 sA[BA * PAD];
+  __shared__ __align__(16) u16 sB[BT * PAD];
+
+  // tile order: groups of 16 token tiles sweep the A side, so concurrently
+  // running blocks share both operands' k slices in L2 / MALL
+  const int L = blockIdx.x;
+  constexpr int GT = 16;
+  const int per_group = GT * a.nA;
+  const int grp = L / per_group;
+  const int rem = L % per_group;
+  const int t_in = min(GT, a.nT - grp * GT);
+  const int tt = grp * GT + rem % t_in;
+  const int at = rem / t_in;
+  if (tt >= a.nT || at >= a.nA) return;
+  const int a0 = at * BA, t0 = tt * BT;
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int c = lane & 31, g = lane >> 5;
+  const int wa = wave >> 1, wt = wave & 1;
+
+  const int K = (MODE == kModeDh) ? a.Vp : a.H;
+  // "A" operand source rows / "B" operand source rows
+  const int a_rows = (MODE == kModeDh) ? a.H : a.V;
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  uint4 ra[8], rb[8];
+  auto load = [&](int k0) {
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    if (MODE == kModeDh) {
+      // A = W^T: rows are hidden units, k = vocab; read vocab-row pairs
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int idx = tid + r * 256;
+        const int pp = idx % (BKK / 2), cc = idx / (BKK / 2);
+        const int v = k0 + 2 * pp;
+        const bool hok = a0 + cc * 8 < a.H;
+        const u16* p = a.w + size_t(v) * a.H + a0 + cc * 8;
+        ra[2 * r] = (hok && v < a.V) ? ld16(p) : z;
+        ra[2 * r + 1] = (hok && v + 1 < a.V) ? ld16(p + a.H) : z;
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const int idx = tid + r * 256;
+        const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
+        const int v = a0 + row;
+        ra[r] = v < a_rows ? ld16(a.w + size_t(v) * a.H + k0 + cc) : z;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int idx = tid + r * 256;
+      const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
+      const int t = t0 + row;
+      if (MODE == kModeDh)
+        rb[r] = t < a.T ? ld16(a.G + size_t(t) * a.Vp + k0 + cc) : z;
+      else
+        rb[r] = t < a.T ? ld16(a.h + size_t(t) * a.H + k0 + cc) : z;
+    }
+  };
+  auto store = [&]() {
+    if (MODE == kModeDh) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int idx = tid + r * 256;
+        const int pp = idx % (BKK / 2), cc = idx / (BKK / 2);
+        const uint32_t lo[4] = {ra[2 * r].x, ra[2 * r].y, ra[2 * r].z, ra[2 * r].w};
+        const uint32_t hi[4] = {ra[2 * r + 1].x, ra[2 * r + 1].y, ra[2 * r + 1].z, ra[2 * r + 1].w};
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t even = (lo[w] & 0xffffu) | (hi[w] << 16);
+          const uint32_t odd = (lo[w] >> 16) | (hi[w] & 0xffff0000u);
+          *reinterpret_cast<uint32_t*>(&sA[(cc * 8 + 2 * w) * PAD + 2 * pp]) = even;
+          *reinterpret_cast<uint32_t*>(&sA[(cc * 8 + 2 * w + 1) * PAD + 2 * pp]) = odd;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const int idx = tid + r * 256;
+        const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
+        st16(&sA[row * PAD + cc], ra[r]);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int idx = tid + r * 256;
+      const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
+      st16(&sB[row * PAD + cc], rb[r]);
+    }
+  };
+
+  load(0);
+  for (int k0 = 0; k0 < K; k0 += BKK) {
+    __syncthreads();
+    store();
+    __syncthreads();
+    if (k0 + BKK < K) load(k0 + BKK);
+#pragma unroll
+    for (int ks = 0; ks < BKK / 16; ++ks) {
+      bf16x8 af[4], bf[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[i] = as_bf16x8(ld16(&sA[(wa * 128 + i * 32 + c) * PAD + ks * 16 + g * 8]));
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        bf[j] = as_bf16x8(ld16(&sB[(wt * 128 + j * 32 + c) * PAD + ks * 16 + g * 8]));
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
+    }
+  }
+
+  // acc[i][j][r]: A-row a0 + wa*128 + i*32 + (r/4)*8 + g*4 + r%4,
+  //               token t0 + wt*128 + j*32 + c
+  const int arow0 = a0 + wa * 128;
+  if (MODE == kModeLogits) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = t0 + wt * 128 + j * 32 + c;
+      const int y = t < a.T ? a.tgt[t] : -1;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = arow0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+          float z = acc[i][j][r];
+          if (v == y) a.tlogit[t] = z;
+          z = v < a.V ? z * kLog2e : -INFINITY;
+          acc[i][j][r] = z;
+          mx = fmaxf(mx, z);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mu = mx == -INFINITY ? 0.f : mx;  // a chunk of vocabulary padding only
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s += fast_exp2(acc[i][j][r] - mu);
+      s += __shfl_xor(s, 32);
+      if (g == 0 && t < a.T) a.part[size_t(t) * a.n_chunks + arow0 / 128] = make_float2(mx, s);
+    }
+  } else if (MODE == kModeGrad) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = t0 + wt * 128 + j * 32 + c;
+      if (t >= a.T) continue;
+      const int y = a.tgt[t];
+      const float gt = y >= 0 ? a.g[t] : 0.f;
+      const float l2 = a.lse[t] * kLog2e;
+      u16* out = a.Gout + size_t(t) * a.Vp;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          float vals[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int v = arow0 + i * 32 + q4 * 8 + g * 4 + u;
+            const float p = fast_exp2(acc[i][j][q4 * 4 + u] * kLog2e - l2);
+            vals[u] = v < a.V ? gt * ((v == y ? 1.f : 0.f) - p) : 0.f;
+          }
+          uint2 wv;
+          wv.x = pack2(vals[0], vals[1]);
+          wv.y = pack2(vals[2], vals[3]);
+          *reinterpret_cast<uint2*>(out + arow0 + i * 32 + q4 * 8 + g * 4) = wv;
+        }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = t0 + wt * 128 + j * 32 + c;
+      if (t >= a.T) continue;
+      u16* out = a.dh + size_t(t) * a.H;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int hcol = arow0 + i * 32 + q4 * 8 + g * 4;
+          if (hcol >= a.H) continue;
+          uint2 wv;
+          wv.x = pack2(acc[i][j][q4 * 4 + 0], acc[i][j][q4 * 4 + 1]);
+          wv.y = pack2(acc[i][j][q4 * 4 + 2], acc[i][j][q4 * 4 + 3]);
+          *reinterpret_cast<uint2*>(out + hcol) = wv;
+        }
+    }
+  }
+}
+
+// Merge the per-chunk (max, sum) pairs of one token and finish the epilogue.
+__global__ __launch_bounds__(256) void lm_combine_kernel(LmArgs a, const float* logp_old,
+                                                         float* logp, float* ratio,
+                                                         float* clipped, float* lse, float eps_lo,
+                                                         float eps_hi) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= a.T) return;
+  const float2* p = a.part + size_t(t) * a.n_chunks;
+  float m = -INFINITY;
+  for (int i = lane; i < a.n_chunks; i += 64) m = fmaxf(m, p[i].x);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  float s = 0.f;
+  for (int i = lane; i < a.n_chunks; i += 64) s += p[i].y * fast_exp2(p[i].x - m);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+  if (lane != 0) return;
+  const float l = (m + __log2f(s)) * kLn2;
+  lse[t] = l;
+  const int y = a.tgt[t];
+  const float lp = y >= 0 ? a.tlogit[t] - l : 0.f;
+  logp[t] = lp;
+  if (logp_old != nullptr) {
+    const float r = y >= 0 ? expf(lp - logp_old[t]) : 1.f;
+    ratio[t] = r;
+    clipped[t] = fminf(fmaxf(r, 1.f - eps_lo), 1.f + eps_hi);
+  }
+}
+
+size_t logprob_fwd_ws_bytes(int T, int H, int V) {
+  (void)H;
+  const int n_chunks = vocab_pad(V) / 128;
+  return align256(size_t(T) * n_chunks * sizeof(float2)) + align256(size_t(T) * sizeof(float)) +
+         256;
+}
+
+size_t logprob_bwd_ws_bytes(int T, int H, int V) {
+  (void)H;
+  return align256(size_t(T) * vocab_pad(V) * sizeof(u16)) + 256;
+}
+
+static char* align_ptr(void* p) {
+  return reinterpret_cast<char*>((reinterpret_cast<uintptr_t>(p) + 255) & ~uintptr_t(255));
+}
+
+hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, const void* hidden,
+                              const void* weight, const int32_t* target, const float* logp_old,
+                              float* logp, float* ratio, float* clipped, float* lse, void* ws,
+                              hipStream_t stream) {
+  LmArgs a{};
+  a.h = static_cast<const u16*>(hidden);
+  a.w = static_cast<const u16*>(weight);
+  a.tgt = target;
+  a.T = T;
+  a.H = H;
+  a.V = V;
+  a.Vp = vocab_pad(V);
+  a.n_chunks = a.Vp / 128;
+  char* base = align_ptr(ws);
+  a.part = reinterpret_cast<float2*>(base);
+  a.tlogit = reinterpret_cast<float*>(base + align256(size_t(T) * a.n_chunks * sizeof(float2)));
+  a.nA = a.Vp / BA;
+  a.nT = (T + BT - 1) / BT;
+  hipLaunchKernelGGL(lm_gemm_kernel<kModeLogits>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(lm_combine_kernel, dim3((T + 3) / 4), dim3(256), 0, stream, a, logp_old,
+                     logp, ratio, clipped, lse, eps_lo, eps_hi);
+  return hipGetLastError();
+}
+
+hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const void* weight,
+                              const int32_t* target, const float* lse, const float* dlogp,
+                              void* dhidden, void* ws, hipStream_t stream) {
+  LmArgs a{};
+  a.h = static_cast<const u16*>(hidden);
+  a.w = static_cast<const u16*>(weight);
+  a.tgt = target;
+  a.lse = lse;
+  a.g = dlogp;
+  a.T = T;
+  a.H = H;
+  a.V = V;
+  a.Vp = vocab_pad(V);
+  u16* G = reinterpret_cast<u16*>(align_ptr(ws));
+  a.Gout = G;
+  a.G = G;
+  a.dh = static_cast<u16*>(dhidden);
+  a.nA = a.Vp / BA;
+  a.nT = (T + BT - 1) / BT;
+  hipLaunchKernelGGL(lm_gemm_kernel<kModeGrad>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
+  a.nA = (H + BA - 1) / BA;
+  hipLaunchKernelGGL(lm_gemm_kernel<kModeDh>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace mv

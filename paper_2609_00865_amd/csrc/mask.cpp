@@ -1,0 +1,307 @@
+// Host construction of the view mask: eviction records -> key lifetimes
+// omega(j) (Eq. "4d-mask-def", Section 4.2) -> block-sparse tile schedules.
+//
+// The paper notes that a dense per-query mask is costly (Section 4.3, "Cost
+// and deployment splits") and that a real FLOP saving needs a block-sparse
+// kernel (Appendix B.3).  Here the mask is never materialised: each key keeps
+// one integer, and the passes visit only tiles holding a visible pair.
+#include <algorithm>
+#include <cstring>
+#include <numeric>
+#include <sstream>
+
+#include "mv_internal.h"
+#include "mv_predicate.h"
+
+namespace {
+
+mv_status bad(mv_status s, const std::string& msg) {
+  mv::set_error(msg);
+  return s;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+mv_status validate_and_fill_omega(const mv_trajectory* trajs, int32_t n_traj, int32_t T,
+                                  std::vector<int32_t>& omega) {
+  omega.assign(T, 0);
+  int32_t pos = 0;
+  for (int32_t t = 0; t < n_traj; ++t) {
+    const mv_trajectory& tr = trajs[t];
+    if (tr.begin != pos || tr.end <= tr.begin || tr.end > T) {
+      std::ostringstream os;
+      os << "trajectory " << t << " [" << tr.begin << ", " << tr.end
+         << ") does not continue the packing at " << pos;
+      return bad(MV_ERR_BAD_RECORD, os.str());
+    }
+    for (int32_t j = tr.begin; j < tr.end; ++j) omega[j] = tr.end;
+    if (tr.n_edits < 0 || (tr.n_edits > 0 && tr.edits == nullptr))
+      return bad(MV_ERR_INVALID_ARG, "trajectory edits: null pointer or negative count");
+    int32_t last_j = tr.begin;
+    for (int32_t k = 0; k < tr.n_edits; ++k) {
+      const mv_edit& e = tr.edits[k];
+      if (e.junction <= last_j || e.junction >= tr.end) {
+        std::ostringstream os;
+        os << "trajectory " << t << " edit " << k << ": junction " << e.junction
+           << " must be in (" << last_j << ", " << tr.end << ") and increasing";
+        return bad(MV_ERR_BAD_RECORD, os.str());
+      }
+      last_j = e.junction;
+      if (e.n_evict < 0 || (e.n_evict > 0 && e.evict == nullptr))
+        return bad(MV_ERR_INVALID_ARG, "edit evict: null pointer or negative count");
+      int32_t prev_end = tr.begin;
+      for (int32_t s = 0; s < e.n_evict; ++s) {
+        const mv_span sp = e.evict[s];
+        if (sp.begin < prev_end || sp.end <= sp.begin || sp.end > e.junction) {
+          std::ostringstream os;
+          os << "trajectory " << t << " edit " << k << " span " << s << " [" << sp.begin
+             << ", " << sp.end << ") must be non-empty, sorted, disjoint and inside ["
+             << tr.begin << ", " << e.junction << ")";
+          return bad(MV_ERR_BAD_RECORD, os.str());
+        }
+        prev_end = sp.end;
+        for (int32_t j = sp.begin; j < sp.end; ++j) {
+          if (omega[j] != tr.end) {
+            std::ostringstream os;
+            os << "token " << j << " is evicted at row " << e.junction
+               << " but already left the view at row " << omega[j];
+            return bad(MV_ERR_BAD_RECORD, os.str());
+          }
+          omega[j] = e.junction;
+        }
+        if (e.summary.begin < e.summary.end &&
+            std::max(sp.begin, e.summary.begin) < std::min(sp.end, e.summary.end))
+          return bad(MV_ERR_BAD_RECORD, "summary block intersects its own eviction set");
+      }
+      if (e.summary.begin != e.summary.end &&
+          (e.summary.begin > e.summary.end || e.summary.begin < tr.begin || e.summary.end > tr.end))
+        return bad(MV_ERR_BAD_RECORD, "summary block outside its trajectory");
+    }
+    pos = tr.end;
+  }
+  if (pos != T) return bad(MV_ERR_BAD_RECORD, "trajectories do not cover [0, total_tokens)");
+  return MV_OK;
+}
+
+void build_stats(mv_view_mask& m) {
+  const int32_t T = m.T;
+  int64_t pairs = 0;
+  std::vector<int32_t> diff(T + 1, 0);
+  int32_t segs = 0;
+  for (int32_t j = 0; j < T; ++j) {
+    pairs += m.omega[j] - j;
+    diff[j] += 1;
+    diff[m.omega[j]] -= 1;
+    if (j == 0 || m.omega[j] != m.omega[j - 1]) ++segs;
+  }
+  int32_t run = 0, mx = 0;
+  for (int32_t i = 0; i < T; ++i) {
+    run += diff[i];
+    mx = std::max(mx, run);
+  }
+  m.stats.visible_pairs = pairs;
+  m.stats.total_tokens = T;
+  m.stats.max_view = mx;
+  m.stats.n_segments = segs;
+}
+
+void build_fwd_schedule(mv_view_mask& m) {
+  const int32_t T = m.T, BQ = mv::kFwdTileQ, BK = mv::kFwdTileK;
+  m.n_kt64 = (T + BK - 1) / BK;
+  m.n_qt = (T + BQ - 1) / BQ;
+  m.kt_minmax.resize(2 * size_t(m.n_kt64));
+  for (int32_t kt = 0; kt < m.n_kt64; ++kt) {
+    int32_t lo = INT32_MAX, hi = 0;
+    for (int32_t j = kt * BK; j < std::min(T, (kt + 1) * BK); ++j) {
+      lo = std::min(lo, m.omega[j]);
+      hi = std::max(hi, m.omega[j]);
+    }
+    m.kt_minmax[2 * kt] = lo;
+    m.kt_minmax[2 * kt + 1] = hi;
+  }
+  m.q_ptr.assign(m.n_qt + 1, 0);
+  m.k_list.clear();
+  int64_t full = 0, partial = 0, skipped = 0;
+  for (int32_t qt = 0; qt < m.n_qt; ++qt) {
+    const int32_t i0 = qt * BQ, i1 = std::min(T, i0 + BQ);
+    const int32_t kt_end = (i1 - 1) / BK + 1;
+    for (int32_t kt = 0; kt < kt_end; ++kt) {
+      const int32_t j0 = kt * BK, j1 = std::min(T, j0 + BK);
+      const int32_t lo = m.kt_minmax[2 * kt], hi = m.kt_minmax[2 * kt + 1];
+      if (j1 - 1 <= i0) {
+        // every key precedes every row: visible pairs exist iff some key is
+        // still alive at the tile's first row
+        if (hi <= i0) {
+          ++skipped;
+          continue;
+        }
+        const bool is_full = lo >= i1;
+        m.k_list.push_back((kt << 1) | (is_full ? 1 : 0));
+        (is_full ? full : partial) += 1;
+      } else {
+        // the tile meets the diagonal: row r = max(j0, i0) sees key r
+        m.k_list.push_back(kt << 1);
+        ++partial;
+      }
+    }
+    m.q_ptr[qt + 1] = int32_t(m.k_list.size());
+  }
+  m.qt_order.resize(m.n_qt);
+  std::iota(m.qt_order.begin(), m.qt_order.end(), 0);
+  std::stable_sort(m.qt_order.begin(), m.qt_order.end(), [&](int32_t a, int32_t b) {
+    return (m.q_ptr[a + 1] - m.q_ptr[a]) > (m.q_ptr[b + 1] - m.q_ptr[b]);
+  });
+  m.stats.tiles_full = int32_t(full);
+  m.stats.tiles_partial = int32_t(partial);
+  m.stats.tiles_skipped = int32_t(skipped);
+}
+
+void build_bwd_schedule(mv_view_mask& m) {
+  const int32_t T = m.T, BK = mv::kBwdTileK, BQ = mv::kBwdBlockQ, CH = mv::kBwdChunk;
+  m.n_kt128 = (T + BK - 1) / BK;
+  m.bwd_tiles.assign(4 * size_t(m.n_kt128), 0);
+  m.bwd_items.clear();
+  m.bwd_red.clear();
+  int32_t slot = 0;
+  std::vector<std::array<int32_t, 4>> items;
+  for (int32_t kt = 0; kt < m.n_kt128; ++kt) {
+    const int32_t j0 = kt * BK, j1 = std::min(T, j0 + BK);
+    int32_t lo = INT32_MAX, hi = 0;
+    for (int32_t j = j0; j < j1; ++j) {
+      lo = std::min(lo, m.omega[j]);
+      hi = std::max(hi, m.omega[j]);
+    }
+    // rows seeing some key of the tile form the contiguous range [j0, hi)
+    const int32_t qb0 = j0 / BQ, qb1 = (hi + BQ - 1) / BQ;
+    const int32_t n = qb1 - qb0, chunks = (n + CH - 1) / CH;
+    m.bwd_tiles[4 * kt + 0] = lo;
+    m.bwd_tiles[4 * kt + 1] = hi;
+    if (chunks == 1) {
+      items.push_back({kt, qb0, qb1, -1});
+      m.bwd_tiles[4 * kt + 2] = -1;
+      m.bwd_tiles[4 * kt + 3] = 0;
+    } else {
+      m.bwd_tiles[4 * kt + 2] = slot;
+      m.bwd_tiles[4 * kt + 3] = chunks;
+      for (int32_t c = 0; c < chunks; ++c)
+        items.push_back({kt, qb0 + c * CH, std::min(qb1, qb0 + (c + 1) * CH), slot + c});
+      slot += chunks;
+      m.bwd_red.push_back(kt);
+    }
+  }
+  std::stable_sort(items.begin(), items.end(), [](const auto& a, const auto& b) {
+    return (a[2] - a[1]) > (b[2] - b[1]);
+  });
+  m.bwd_items.reserve(items.size() * 4);
+  for (const auto& it : items) m.bwd_items.insert(m.bwd_items.end(), it.begin(), it.end());
+  m.n_slots = slot;
+  m.stats.bwd_items = int32_t(items.size());
+  m.stats.bwd_partial_slots = slot;
+}
+
+void layout_device(mv_view_mask& m) {
+  const std::vector<int32_t>* arrs[8] = {&m.omega,  &m.kt_minmax, &m.q_ptr,     &m.k_list,
+                                         &m.qt_order, &m.bwd_items, &m.bwd_tiles, &m.bwd_red};
+  size_t off = 0;
+  for (int i = 0; i < 8; ++i) {
+    m.off[i] = off;
+    off = align256(off + std::max<size_t>(1, arrs[i]->size()) * sizeof(int32_t));
+  }
+  m.bytes = off;
+}
+
+}  // namespace
+
+extern "C" {
+
+mv_status mv_build_view_mask(const mv_trajectory* trajs, int32_t n_traj, int32_t total_tokens,
+                             mv_view_mask** out) {
+  if (out == nullptr) return bad(MV_ERR_INVALID_ARG, "out is null");
+  *out = nullptr;
+  if (trajs == nullptr || n_traj <= 0) return bad(MV_ERR_INVALID_ARG, "no trajectories");
+  if (total_tokens <= 0 || total_tokens > (1 << 30))
+    return bad(MV_ERR_INVALID_ARG, "total_tokens must be in [1, 2^30]");
+  try {
+    auto* m = new mv_view_mask();
+    m->T = total_tokens;
+    mv_status s = validate_and_fill_omega(trajs, n_traj, total_tokens, m->omega);
+    if (s != MV_OK) {
+      delete m;
+      return s;
+    }
+    build_stats(*m);
+    build_fwd_schedule(*m);
+    build_bwd_schedule(*m);
+    layout_device(*m);
+    *out = m;
+    return MV_OK;
+  } catch (const std::exception& e) {
+    return bad(MV_ERR_INVALID_ARG, std::string("host allocation failed: ") + e.what());
+  }
+}
+
+size_t mv_view_mask_device_bytes(const mv_view_mask* m) { return m ? m->bytes : 0; }
+
+mv_status mv_view_mask_upload(mv_view_mask* m, void* dev_buf, size_t bytes, hipStream_t stream) {
+  if (m == nullptr || dev_buf == nullptr) return bad(MV_ERR_INVALID_ARG, "null mask or buffer");
+  if ((reinterpret_cast<uintptr_t>(dev_buf) & 255) != 0)
+    return bad(MV_ERR_INVALID_ARG, "mask buffer must be 256-byte aligned");
+  if (bytes < m->bytes) {
+    std::ostringstream os;
+    os << "mask buffer has " << bytes << " bytes, needs " << m->bytes;
+    return bad(MV_ERR_WORKSPACE, os.str());
+  }
+  const std::vector<int32_t>* arrs[8] = {&m->omega,    &m->kt_minmax, &m->q_ptr,
+                                         &m->k_list,   &m->qt_order,  &m->bwd_items,
+                                         &m->bwd_tiles, &m->bwd_red};
+  char* base = static_cast<char*>(dev_buf);
+  for (int i = 0; i < 8; ++i) {
+    if (arrs[i]->empty()) continue;
+    hipError_t e = hipMemcpyAsync(base + m->off[i], arrs[i]->data(),
+                                  arrs[i]->size() * sizeof(int32_t), hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return bad(MV_ERR_HIP, std::string("mask upload: ") + hipGetErrorString(e));
+  }
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return bad(MV_ERR_HIP, "hipGetDevice failed");
+  m->dev = dev_buf;
+  m->device = dev;
+  auto at = [&](int i) { return reinterpret_cast<const int32_t*>(base + m->off[i]); };
+  m->d = mv_mask_dev{at(0), at(1), at(2), at(3), at(4), at(5), at(6), at(7)};
+  return MV_OK;
+}
+
+mv_status mv_view_mask_stats(const mv_view_mask* m, mv_mask_stats* out) {
+  if (m == nullptr || out == nullptr) return bad(MV_ERR_INVALID_ARG, "null argument");
+  *out = m->stats;
+  return MV_OK;
+}
+
+mv_status mv_view_mask_death(const mv_view_mask* m, int32_t* host_out) {
+  if (m == nullptr || host_out == nullptr) return bad(MV_ERR_INVALID_ARG, "null argument");
+  std::memcpy(host_out, m->omega.data(), m->omega.size() * sizeof(int32_t));
+  return MV_OK;
+}
+
+mv_status mv_view_mask_materialize_host(const mv_view_mask* m, int32_t row_begin, int32_t row_end,
+                                        uint32_t* host_bits) {
+  if (m == nullptr || host_bits == nullptr) return bad(MV_ERR_INVALID_ARG, "null argument");
+  if (row_begin < 0 || row_end > m->T || row_begin > row_end)
+    return bad(MV_ERR_INVALID_ARG, "row range outside [0, total_tokens]");
+  const int32_t T = m->T, words = (T + 31) / 32;
+  std::memset(host_bits, 0, size_t(row_end - row_begin) * words * sizeof(uint32_t));
+  for (int32_t i = row_begin; i < row_end; ++i) {
+    uint32_t* row = host_bits + size_t(i - row_begin) * words;
+    const int32_t qt = i / mv::kFwdTileQ;
+    for (int32_t e = m->q_ptr[qt]; e < m->q_ptr[qt + 1]; ++e) {
+      const int32_t kt = m->k_list[e] >> 1;
+      const bool full = m->k_list[e] & 1;
+      for (int32_t j = kt * mv::kFwdTileK; j < std::min(T, (kt + 1) * mv::kFwdTileK); ++j)
+        if (full || mv_visible(i, j, m->omega[j])) row[j >> 5] |= 1u << (j & 31);
+    }
+  }
+  return MV_OK;
+}
+
+void mv_view_mask_free(mv_view_mask* m) { delete m; }
+
+}  // extern "C"

@@ -1,0 +1,72 @@
+// Device helpers for gfx950 (CDNA4): MFMA operand types, bf16 packing, and
+// the block -> work mapping that keeps related blocks on one XCD.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "mv_internal.h"
+
+namespace mv {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16;
+
+// D = A * B + C on a 32x32 tile with K = 16 (bf16 in, fp32 accumulate).
+// Lane l supplies row (l % 32) of A and column (l % 32) of B, each as 8
+// consecutive k values of group (l / 32); any permutation of k applied to both
+// operands leaves D unchanged.  D element r of lane l is row
+// (r / 4) * 8 + (l / 32) * 4 + r % 4, column l % 32.
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+__device__ __forceinline__ void st16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
+
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(f)));
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __builtin_bit_cast(float, static_cast<uint32_t>(b) << 16);
+}
+
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  return bf16_bits(lo) | (bf16_bits(hi) << 16);
+}
+
+// Eight consecutive fp32 accumulator values as one bf16 MFMA operand.
+__device__ __forceinline__ bf16x8 to_operand(const f32x16& acc, int base) {
+  uint4 u;
+  u.x = pack2(acc[base + 0], acc[base + 1]);
+  u.y = pack2(acc[base + 2], acc[base + 3]);
+  u.z = pack2(acc[base + 4], acc[base + 5]);
+  u.w = pack2(acc[base + 6], acc[base + 7]);
+  return as_bf16x8(u);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Column of key offset kk (0..63) inside a transposed LDS tile: the 16-key
+// groups are permuted so that one 16-byte read gives a lane the 8 keys its
+// accumulator rows hold (see mfma32: rows g*4..g*4+3 and 8+g*4..8+g*4+3).
+__device__ __forceinline__ int perm_col(int kk) {
+  const int r = kk & 15;
+  return (kk & ~15) + ((r >> 2) & 1) * 8 + (r >> 3) * 4 + (r & 3);
+}
+
+// The dispatcher deals consecutive block ids to the 8 XCDs round-robin.
+// Returns (xcd, index of the block among those of its XCD).
+__device__ __forceinline__ void xcd_split(int& xcd, int& local) {
+  xcd = blockIdx.x % kNumXcd;
+  local = blockIdx.x / kNumXcd;
+}
+
+}  // namespace mv

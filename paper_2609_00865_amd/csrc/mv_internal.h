@@ -1,0 +1,56 @@
+// Internal declarations of libmv: the view-mask object, tile constants and
+// kernel launchers.  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/mv.h"
+
+namespace mv {
+
+// Forward / dQ schedule: 128-row query tiles x 64-key key tiles.
+constexpr int kFwdTileQ = 128;
+constexpr int kFwdTileK = 64;
+// dK/dV schedule: 128-key key tiles visited by 64-row query blocks; a key
+// tile's row range is cut into work items of at most kBwdChunk query blocks.
+constexpr int kBwdTileK = 128;
+constexpr int kBwdBlockQ = 64;
+constexpr int kBwdChunk = 32;
+// Blocks are dealt to the 8 XCDs round-robin by the dispatcher.
+constexpr int kNumXcd = 8;
+
+void set_error(const std::string& msg);
+
+}  // namespace mv
+
+// Device-side view of an uploaded mask (all int32 arrays).
+struct mv_mask_dev {
+  const int32_t* omega;      // [T] death row of each key
+  const int32_t* kt_minmax;  // [n_kt64 * 2] min/max omega per 64-key tile
+  const int32_t* q_ptr;      // [n_qt + 1] CSR row pointers per 128-row tile
+  const int32_t* k_list;     // [nnz] (kt64 << 1) | full_flag, ascending kt
+  const int32_t* qt_order;   // [n_qt] query tiles, heaviest first
+  const int32_t* bwd_items;  // [n_items * 4] (kt128, qb_begin, qb_end, slot)
+  const int32_t* bwd_tiles;  // [n_kt128 * 4] (min omega, max omega, first slot, n slots)
+  const int32_t* bwd_red;    // [n_red] key tiles whose partials are reduced
+};
+
+struct mv_view_mask {
+  int32_t T = 0;
+  int32_t n_qt = 0, n_kt64 = 0, n_kt128 = 0;
+  std::vector<int32_t> omega, kt_minmax, q_ptr, k_list, qt_order;
+  std::vector<int32_t> bwd_items, bwd_tiles, bwd_red;
+  int32_t n_slots = 0;
+  mv_mask_stats stats{};
+  // device copy
+  size_t off[8] = {0};
+  size_t bytes = 0;
+  void* dev = nullptr;
+  int device = -1;
+  mv_mask_dev d{};
+};

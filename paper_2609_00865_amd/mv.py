@@ -1,0 +1,321 @@
+"""Python binding of libmv: argument marshalling only.
+
+Every computation runs in libmv (the HIP kernels and the C++ mask builder);
+this module turns trajectories and torch tensors into the C ABI's plain
+pointers and sizes, allocates outputs and workspaces with torch, and raises
+``MVError`` on any non-OK status.  If libmv.so has not been built the import
+fails loudly: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmv.so")
+
+
+class MVError(RuntimeError):
+    def __init__(self, status: int, name: str, message: str):
+        super().__init__(f"{name}: {message}")
+        self.status = status
+        self.name = name
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"libmv.so not found at {_LIB_PATH}; run "
+                          "`python -m paper_2609_00865_amd.build` (or __graft_entry__.build())")
+    return ctypes.CDLL(_LIB_PATH)
+
+
+_lib = _load()
+
+
+class Span(ctypes.Structure):
+    _fields_ = [("begin", ctypes.c_int32), ("end", ctypes.c_int32)]
+
+
+class EditC(ctypes.Structure):
+    _fields_ = [("junction", ctypes.c_int32), ("n_evict", ctypes.c_int32),
+                ("evict", ctypes.POINTER(Span)), ("summary", Span)]
+
+
+class TrajectoryC(ctypes.Structure):
+    _fields_ = [("begin", ctypes.c_int32), ("end", ctypes.c_int32),
+                ("n_edits", ctypes.c_int32), ("edits", ctypes.POINTER(EditC))]
+
+
+class MaskStats(ctypes.Structure):
+    _fields_ = [("visible_pairs", ctypes.c_int64), ("total_tokens", ctypes.c_int32),
+                ("max_view", ctypes.c_int32), ("n_segments", ctypes.c_int32),
+                ("tiles_full", ctypes.c_int32), ("tiles_partial", ctypes.c_int32),
+                ("tiles_skipped", ctypes.c_int32), ("bwd_items", ctypes.c_int32),
+                ("bwd_partial_slots", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+class AttnShape(ctypes.Structure):
+    _fields_ = [("total_tokens", ctypes.c_int32), ("n_heads_q", ctypes.c_int32),
+                ("n_heads_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float)]
+
+
+class LogprobShape(ctypes.Structure):
+    _fields_ = [("n_tokens", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("eps_low", ctypes.c_float),
+                ("eps_high", ctypes.c_float)]
+
+
+_vp, _sz, _i32, _f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_float
+_P = ctypes.POINTER
+
+
+def _sig(name, res, *args):
+    fn = getattr(_lib, name)
+    fn.restype = res
+    fn.argtypes = list(args)
+    return fn
+
+
+mv_status_string = _sig("mv_status_string", ctypes.c_char_p, ctypes.c_int)
+mv_last_error = _sig("mv_last_error", ctypes.c_char_p)
+mv_version = _sig("mv_version", _i32)
+mv_build_view_mask = _sig("mv_build_view_mask", ctypes.c_int, _P(TrajectoryC), _i32, _i32,
+                          _P(_vp))
+mv_view_mask_device_bytes = _sig("mv_view_mask_device_bytes", _sz, _vp)
+mv_view_mask_upload = _sig("mv_view_mask_upload", ctypes.c_int, _vp, _vp, _sz, _vp)
+mv_view_mask_stats = _sig("mv_view_mask_stats", ctypes.c_int, _vp, _P(MaskStats))
+mv_view_mask_death = _sig("mv_view_mask_death", ctypes.c_int, _vp, _vp)
+mv_view_mask_materialize = _sig("mv_view_mask_materialize", ctypes.c_int, _vp, _i32, _i32, _vp,
+                                _vp)
+mv_view_mask_materialize_host = _sig("mv_view_mask_materialize_host", ctypes.c_int, _vp, _i32,
+                                     _i32, _vp)
+mv_view_mask_free = _sig("mv_view_mask_free", None, _vp)
+mv_attn_fwd = _sig("mv_attn_fwd", ctypes.c_int, _vp, _P(AttnShape), _vp, _vp, _vp, _vp, _vp,
+                   _vp)
+mv_attn_bwd_workspace_bytes = _sig("mv_attn_bwd_workspace_bytes", _sz, _vp, _P(AttnShape))
+mv_attn_bwd = _sig("mv_attn_bwd", ctypes.c_int, _vp, _P(AttnShape), _vp, _vp, _vp, _vp, _vp,
+                   _vp, _vp, _vp, _vp, _vp, _sz, _vp)
+mv_token_logprob_workspace_bytes = _sig("mv_token_logprob_workspace_bytes", _sz,
+                                        _P(LogprobShape))
+mv_token_logprob = _sig("mv_token_logprob", ctypes.c_int, _P(LogprobShape), _vp, _vp, _vp, _vp,
+                        _vp, _vp, _vp, _vp, _vp, _sz, _vp)
+mv_token_logprob_bwd_workspace_bytes = _sig("mv_token_logprob_bwd_workspace_bytes", _sz,
+                                            _P(LogprobShape))
+mv_token_logprob_bwd = _sig("mv_token_logprob_bwd", ctypes.c_int, _P(LogprobShape), _vp, _vp,
+                            _vp, _vp, _vp, _vp, _vp, _sz, _vp)
+mv_ppo_clip_dlogp = _sig("mv_ppo_clip_dlogp", ctypes.c_int, _i32, _vp, _vp, _f32, _f32, _f32,
+                         _vp, _vp)
+
+EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_mask",
+            "mv_view_mask_device_bytes", "mv_view_mask_upload", "mv_view_mask_stats",
+            "mv_view_mask_death", "mv_view_mask_materialize", "mv_view_mask_materialize_host",
+            "mv_view_mask_free", "mv_attn_fwd", "mv_attn_bwd_workspace_bytes", "mv_attn_bwd",
+            "mv_token_logprob_workspace_bytes", "mv_token_logprob",
+            "mv_token_logprob_bwd_workspace_bytes", "mv_token_logprob_bwd", "mv_ppo_clip_dlogp"]
+
+
+def check(status: int) -> None:
+    if status != 0:
+        raise MVError(status, mv_status_string(status).decode(), mv_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _aligned_buffer(nbytes: int, device) -> tuple:
+    """A uint8 device tensor and the first 256-byte aligned address inside it."""
+    buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    addr = (buf.data_ptr() + 255) & ~255
+    return buf, addr
+
+
+# ---------------------------------------------------------------------------
+# view mask
+# ---------------------------------------------------------------------------
+class ViewMask:
+    """Owns a libmv mask object built from trajectories (host), optionally uploaded."""
+
+    def __init__(self, trajectories: Sequence, total_tokens: Optional[int] = None):
+        keep = []
+        trajs = (TrajectoryC * len(trajectories))()
+        for ti, t in enumerate(trajectories):
+            edits = (EditC * max(1, len(t.edits)))()
+            for ei, e in enumerate(t.edits):
+                spans = (Span * max(1, len(e.evict)))()
+                for si, (b, x) in enumerate(e.evict):
+                    spans[si] = Span(int(b), int(x))
+                keep.append(spans)
+                summ = getattr(e, "summary", (0, 0))
+                edits[ei] = EditC(int(e.junction), len(e.evict), spans,
+                                  Span(int(summ[0]), int(summ[1])))
+            keep.append(edits)
+            trajs[ti] = TrajectoryC(int(t.begin), int(t.end), len(t.edits), edits)
+        T = total_tokens if total_tokens is not None else int(trajectories[-1].end)
+        handle = ctypes.c_void_p()
+        check(mv_build_view_mask(trajs, len(trajectories), T, ctypes.byref(handle)))
+        self._h = handle
+        self.total_tokens = T
+        self._dev = None
+
+    def __del__(self, _free=mv_view_mask_free):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            _free(h)
+            self._h = None
+
+    @property
+    def handle(self):
+        return self._h
+
+    def stats(self) -> dict:
+        s = MaskStats()
+        check(mv_view_mask_stats(self._h, ctypes.byref(s)))
+        return s.as_dict()
+
+    def death(self) -> torch.Tensor:
+        out = torch.empty(self.total_tokens, dtype=torch.int32)
+        check(mv_view_mask_death(self._h, _ptr(out)))
+        return out
+
+    def device_bytes(self) -> int:
+        return int(mv_view_mask_device_bytes(self._h))
+
+    def upload(self, device="cuda", stream=None) -> "ViewMask":
+        buf, addr = _aligned_buffer(self.device_bytes(), device)
+        check(mv_view_mask_upload(self._h, ctypes.c_void_p(addr), self.device_bytes(),
+                                  _stream(stream)))
+        self._dev = buf
+        return self
+
+    def materialize(self, row_begin: int, row_end: int, stream=None) -> torch.Tensor:
+        words = (self.total_tokens + 31) // 32
+        out = torch.empty((row_end - row_begin) * words, dtype=torch.int32, device="cuda")
+        check(mv_view_mask_materialize(self._h, row_begin, row_end, _ptr(out), _stream(stream)))
+        return out.view(row_end - row_begin, words)
+
+    def materialize_host(self, row_begin: int, row_end: int) -> torch.Tensor:
+        words = (self.total_tokens + 31) // 32
+        out = torch.empty((row_end - row_begin) * words, dtype=torch.int32)
+        check(mv_view_mask_materialize_host(self._h, row_begin, row_end, _ptr(out)))
+        return out.view(row_end - row_begin, words)
+
+
+def unpack_bits(words: torch.Tensor, total_tokens: int) -> torch.Tensor:
+    """[rows, ceil(T/32)] int32 words -> [rows, T] bool (bit j%32 of word j//32)."""
+    w = words.to(torch.int64) & 0xFFFFFFFF
+    shifts = torch.arange(32, dtype=torch.int64, device=w.device)
+    bits = (w[..., None] >> shifts) & 1
+    return bits.reshape(words.shape[0], -1)[:, :total_tokens].bool()
+
+
+# ---------------------------------------------------------------------------
+# attention
+# ---------------------------------------------------------------------------
+def _attn_shape(mask: ViewMask, q, k, scale):
+    T, hq, d = q.shape
+    return AttnShape(T, hq, k.shape[1], d, float(scale) if scale else 0.0)
+
+
+def _need_bf16_cuda(*ts):
+    for t in ts:
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError("expected contiguous bf16 CUDA tensors")
+
+
+def attn_fwd(mask: ViewMask, q, k, v, scale: Optional[float] = None, stream=None):
+    _need_bf16_cuda(q, k, v)
+    shape = _attn_shape(mask, q, k, scale)
+    o = torch.empty_like(q)
+    lse = torch.empty((q.shape[1], q.shape[0]), dtype=torch.float32, device=q.device)
+    check(mv_attn_fwd(mask.handle, ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                      _ptr(lse), _stream(stream)))
+    return o, lse
+
+
+def attn_bwd_workspace(mask: ViewMask, q, k, scale=None) -> torch.Tensor:
+    shape = _attn_shape(mask, q, k, scale)
+    n = int(mv_attn_bwd_workspace_bytes(mask.handle, ctypes.byref(shape)))
+    return torch.empty(n, dtype=torch.uint8, device=q.device)
+
+
+def attn_bwd(mask: ViewMask, q, k, v, o, dout, lse, scale: Optional[float] = None,
+             workspace: Optional[torch.Tensor] = None, stream=None):
+    _need_bf16_cuda(q, k, v, o, dout)
+    shape = _attn_shape(mask, q, k, scale)
+    ws = workspace if workspace is not None else attn_bwd_workspace(mask, q, k, scale)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    check(mv_attn_bwd(mask.handle, ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                      _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws),
+                      ws.numel(), _stream(stream)))
+    return dq, dk, dv
+
+
+# ---------------------------------------------------------------------------
+# token log-prob
+# ---------------------------------------------------------------------------
+def _lp_shape(hidden, weight, eps_low, eps_high):
+    return LogprobShape(hidden.shape[0], hidden.shape[1], weight.shape[0], float(eps_low),
+                        float(eps_high))
+
+
+def token_logprob_workspace(hidden, weight) -> torch.Tensor:
+    s = _lp_shape(hidden, weight, 0.2, 0.2)
+    n = int(mv_token_logprob_workspace_bytes(ctypes.byref(s)))
+    return torch.empty(n, dtype=torch.uint8, device=hidden.device)
+
+
+def token_logprob(hidden, weight, target, logp_old=None, eps_low=0.2, eps_high=0.2,
+                  workspace=None, stream=None):
+    _need_bf16_cuda(hidden, weight)
+    s = _lp_shape(hidden, weight, eps_low, eps_high)
+    T = hidden.shape[0]
+    dev = hidden.device
+    logp = torch.empty(T, dtype=torch.float32, device=dev)
+    lse = torch.empty(T, dtype=torch.float32, device=dev)
+    ratio = clipped = None
+    if logp_old is not None:
+        ratio = torch.empty(T, dtype=torch.float32, device=dev)
+        clipped = torch.empty(T, dtype=torch.float32, device=dev)
+    ws = workspace if workspace is not None else token_logprob_workspace(hidden, weight)
+    check(mv_token_logprob(ctypes.byref(s), _ptr(hidden), _ptr(weight), _ptr(target),
+                           _ptr(logp_old), _ptr(logp), _ptr(ratio), _ptr(clipped), _ptr(lse),
+                           _ptr(ws), ws.numel(), _stream(stream)))
+    return logp, ratio, clipped, lse
+
+
+def token_logprob_bwd_workspace(hidden, weight) -> torch.Tensor:
+    s = _lp_shape(hidden, weight, 0.2, 0.2)
+    n = int(mv_token_logprob_bwd_workspace_bytes(ctypes.byref(s)))
+    return torch.empty(n, dtype=torch.uint8, device=hidden.device)
+
+
+def token_logprob_bwd(hidden, weight, target, lse, dlogp, workspace=None, stream=None):
+    _need_bf16_cuda(hidden, weight)
+    s = _lp_shape(hidden, weight, 0.2, 0.2)
+    dh = torch.empty_like(hidden)
+    ws = workspace if workspace is not None else token_logprob_bwd_workspace(hidden, weight)
+    check(mv_token_logprob_bwd(ctypes.byref(s), _ptr(hidden), _ptr(weight), _ptr(target),
+                               _ptr(lse), _ptr(dlogp), _ptr(dh), _ptr(ws), ws.numel(),
+                               _stream(stream)))
+    return dh
+
+
+def ppo_clip_dlogp(ratio, adv, eps_low=0.2, eps_high=0.2, scale=1.0, stream=None):
+    out = torch.empty_like(ratio)
+    check(mv_ppo_clip_dlogp(ratio.numel(), _ptr(ratio), _ptr(adv), eps_low, eps_high, scale,
+                            _ptr(out), _stream(stream)))
+    return out

@@ -1,0 +1,42 @@
+"""Comparison helpers for GPU-vs-oracle parity.
+
+Floating-point gates (bf16 outputs and gradients):
+  * max |gpu - ref| <= 2e-2 (absolute), and
+  * ||gpu - ref||_F <= 1e-2 * ||ref||_F (relative Frobenius), which stays
+    meaningful where the absolute gate is loose (long rows have small |O|).
+Both sides read the same bf16 input values; the oracle runs in fp64 (fp32 for
+the largest samples).
+"""
+import torch
+
+ATOL_BF16 = 2e-2
+REL_FRO = 1e-2
+LOGP_REL = 1e-4
+
+
+def errors(gpu, ref):
+    g = gpu.detach().to("cpu", torch.float64)
+    r = ref.detach().to("cpu", torch.float64)
+    diff = g - r
+    max_abs = float(diff.abs().max()) if diff.numel() else 0.0
+    den = float(r.norm())
+    rel = float(diff.norm()) / den if den > 0 else float(diff.norm())
+    return max_abs, rel, float(r.abs().max()) if r.numel() else 0.0
+
+
+def assert_bf16_close(gpu, ref, what, atol=ATOL_BF16, rel_fro=REL_FRO):
+    max_abs, rel, ref_max = errors(gpu, ref)
+    msg = f"{what}: max_abs={max_abs:.3e} rel_fro={rel:.3e} max|ref|={ref_max:.3e}"
+    print(msg, flush=True)
+    assert max_abs <= atol and rel <= rel_fro, msg
+    return max_abs, rel
+
+
+def assert_rel_close(gpu, ref, what, rel=LOGP_REL, floor=1e-6):
+    g = gpu.detach().to("cpu", torch.float64)
+    r = ref.detach().to("cpu", torch.float64)
+    err = float(((g - r).abs() / r.abs().clamp(min=floor)).max()) if r.numel() else 0.0
+    msg = f"{what}: max_rel={err:.3e}"
+    print(msg, flush=True)
+    assert err <= rel, msg
+    return err

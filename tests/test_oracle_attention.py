@@ -199,3 +199,19 @@ def test_planted_mistake_in_layers_is_caught(monkeypatch):
     monkeypatch.setattr(V, "branch_layers", leaky)
     O, _ = A.logittree(trajs, q, k, v)
     assert (O - Ob).abs().max() > 1e-3
+
+
+def test_row_grads_and_row_range_match_full_backward():
+    trajs = _random_trajs(21, [40, 33], max_edits=4, max_span=9)
+    T = trajs[-1].end
+    q, k, v, do = _rand(T, 4, 2, 8, 4)
+    _, _, dq, dk, dv = A.logittree(trajs, q, k, v, dout=do)
+    rows = [0, 7, 39, 40, 55, T - 1]
+    g = A.row_grads(trajs, q, k, v, do, rows)
+    assert torch.allclose(g, dq[rows], atol=1e-12, rtol=0)
+    # restricting the loss to the rows that see key j reproduces dK_j, dV_j
+    death = [x for t in trajs for x in V.death_rows(t)]
+    for j in (3, 12, 41, 60):
+        _, _, _, dkj, dvj = A.logittree(trajs, q, k, v, dout=do, row_range=(j, death[j]))
+        assert torch.allclose(dkj[j], dk[j], atol=1e-12, rtol=0)
+        assert torch.allclose(dvj[j], dv[j], atol=1e-12, rtol=0)
