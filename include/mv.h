@@ -247,6 +247,20 @@ mv_status mv_ppo_clip_dlogp(int32_t n, const float* ratio, const float* adv,
                             float eps_low, float eps_high, float scale,
                             float* dlogp, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Kernel timing (measurement support, not part of the method).
+ *
+ * While enabled, every kernel the library enqueues is bracketed by a pair of
+ * HIP events recorded on the launch stream.  mv_profile_enable(1) clears the
+ * previous records; mv_profile_read waits for the recorded events and returns
+ * the summed duration (ms) and launch count of the kernels named `kernel`
+ * (one of "attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce",
+ * "attn_bwd_dq", "lm_logits", "lm_combine", "lm_grad", "lm_dh",
+ * "materialize", "ppo_clip").  Not for use under stream capture.
+ * ------------------------------------------------------------------------ */
+mv_status mv_profile_enable(int32_t on);
+mv_status mv_profile_read(const char* kernel, double* total_ms, int32_t* count);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,8 +1,10 @@
 // C ABI of libmv: argument validation, workspace sizing and kernel dispatch.
 // Validation is complete before anything is enqueued, so a failing call
 // launches nothing.
+#include <atomic>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <sstream>
 
 #include "mv_internal.h"
@@ -12,6 +14,45 @@ namespace mv {
 thread_local std::string g_last_error;
 
 void set_error(const std::string& msg) { g_last_error = msg; }
+
+namespace {
+struct ProfRecord {
+  std::string name;
+  hipEvent_t start, stop;
+};
+std::atomic<bool> g_prof_on{false};
+std::mutex g_prof_mu;
+std::vector<ProfRecord> g_prof;
+
+void prof_clear_locked() {
+  for (auto& r : g_prof) {
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  g_prof.clear();
+}
+}  // namespace
+
+ProfScope::ProfScope(const char* name, hipStream_t stream) : name_(name), stream_(stream) {
+  if (!g_prof_on.load(std::memory_order_relaxed)) return;
+  if (hipEventCreate(&start_) != hipSuccess) {
+    start_ = nullptr;
+    return;
+  }
+  (void)hipEventRecord(start_, stream_);
+}
+
+ProfScope::~ProfScope() {
+  if (start_ == nullptr) return;
+  hipEvent_t stop = nullptr;
+  if (hipEventCreate(&stop) != hipSuccess) {
+    (void)hipEventDestroy(start_);
+    return;
+  }
+  (void)hipEventRecord(stop, stream_);
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof.push_back({name_, start_, stop});
+}
 
 hipError_t launch_attn_fwd(const mv_view_mask& m, int Hq, int Hkv, int D, float scale,
                            const void* q, const void* k, const void* v, void* o, float* lse,
@@ -214,6 +255,33 @@ mv_status mv_token_logprob_bwd(const mv_logprob_shape* s, const void* hidden, co
   return hip_status(mv::launch_logprob_bwd(s->n_tokens, s->hidden, s->vocab, hidden, weight,
                                            target, lse, dlogp, dhidden, ws, stream),
                     "log-prob backward launch");
+}
+
+mv_status mv_profile_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(mv::g_prof_mu);
+  mv::prof_clear_locked();
+  mv::g_prof_on.store(on != 0);
+  return MV_OK;
+}
+
+mv_status mv_profile_read(const char* kernel, double* total_ms, int32_t* count) {
+  if (kernel == nullptr || total_ms == nullptr || count == nullptr)
+    return fail(MV_ERR_INVALID_ARG, "null argument");
+  std::lock_guard<std::mutex> lk(mv::g_prof_mu);
+  double tot = 0.0;
+  int32_t n = 0;
+  for (auto& r : mv::g_prof) {
+    if (r.name != kernel) continue;
+    if (hipEventSynchronize(r.stop) != hipSuccess) return fail(MV_ERR_HIP, "event wait failed");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess)
+      return fail(MV_ERR_HIP, "event timing failed");
+    tot += ms;
+    ++n;
+  }
+  *total_ms = tot;
+  *count = n;
+  return MV_OK;
 }
 
 mv_status mv_ppo_clip_dlogp(int32_t n, const float* ratio, const float* adv, float eps_low,

@@ -513,15 +513,27 @@ hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float 
   const int n_red = int(m.bwd_red.size());
   const dim3 g_red(unsigned(std::max(1, n_red * Hkv)));
   if (D == 128) {
-    hipLaunchKernelGGL(bwd_pre_kernel<128>, g_pre, b256, 0, stream, a);
-    hipLaunchKernelGGL(bwd_dkdv_kernel<128>, g_kv, b256, 0, stream, a);
-    if (n_red) hipLaunchKernelGGL(bwd_reduce_kernel<128>, g_red, b256, 0, stream, a, n_red);
-    hipLaunchKernelGGL(bwd_dq_kernel<128>, g_dq, b256, 0, stream, a);
+    { ProfScope p("attn_bwd_pre", stream);
+      hipLaunchKernelGGL(bwd_pre_kernel<128>, g_pre, b256, 0, stream, a); }
+    { ProfScope p("attn_bwd_dkdv", stream);
+      hipLaunchKernelGGL(bwd_dkdv_kernel<128>, g_kv, b256, 0, stream, a); }
+    if (n_red) {
+      ProfScope p("attn_bwd_reduce", stream);
+      hipLaunchKernelGGL(bwd_reduce_kernel<128>, g_red, b256, 0, stream, a, n_red);
+    }
+    { ProfScope p("attn_bwd_dq", stream);
+      hipLaunchKernelGGL(bwd_dq_kernel<128>, g_dq, b256, 0, stream, a); }
   } else {
-    hipLaunchKernelGGL(bwd_pre_kernel<64>, g_pre, b256, 0, stream, a);
-    hipLaunchKernelGGL(bwd_dkdv_kernel<64>, g_kv, b256, 0, stream, a);
-    if (n_red) hipLaunchKernelGGL(bwd_reduce_kernel<64>, g_red, b256, 0, stream, a, n_red);
-    hipLaunchKernelGGL(bwd_dq_kernel<64>, g_dq, b256, 0, stream, a);
+    { ProfScope p("attn_bwd_pre", stream);
+      hipLaunchKernelGGL(bwd_pre_kernel<64>, g_pre, b256, 0, stream, a); }
+    { ProfScope p("attn_bwd_dkdv", stream);
+      hipLaunchKernelGGL(bwd_dkdv_kernel<64>, g_kv, b256, 0, stream, a); }
+    if (n_red) {
+      ProfScope p("attn_bwd_reduce", stream);
+      hipLaunchKernelGGL(bwd_reduce_kernel<64>, g_red, b256, 0, stream, a, n_red);
+    }
+    { ProfScope p("attn_bwd_dq", stream);
+      hipLaunchKernelGGL(bwd_dq_kernel<64>, g_dq, b256, 0, stream, a); }
   }
   return hipGetLastError();
 }

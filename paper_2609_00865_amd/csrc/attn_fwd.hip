@@ -237,6 +237,7 @@ hipError_t launch_attn_fwd(const mv_view_mask& m, int Hq, int Hkv, int D, float 
   a.scale_log2 = scale * 1.4426950408889634f;
   const int per_xcd = (m.n_qt + kNumXcd - 1) / kNumXcd;
   const dim3 grid(per_xcd * Hq * kNumXcd), block(256);
+  ProfScope prof("attn_fwd", stream);
   if (D == 128)
     hipLaunchKernelGGL(attn_fwd_kernel<128>, grid, block, 0, stream, a);
   else

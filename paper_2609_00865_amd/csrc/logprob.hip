@@ -310,9 +310,15 @@ hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, c
   a.tlogit = reinterpret_cast<float*>(base + align256(size_t(T) * a.n_chunks * sizeof(float2)));
   a.nA = a.Vp / BA;
   a.nT = (T + BT - 1) / BT;
-  hipLaunchKernelGGL(lm_gemm_kernel<kModeLogits>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(lm_combine_kernel, dim3((T + 3) / 4), dim3(256), 0, stream, a, logp_old,
-                     logp, ratio, clipped, lse, eps_lo, eps_hi);
+  {
+    ProfScope p("lm_logits", stream);
+    hipLaunchKernelGGL(lm_gemm_kernel<kModeLogits>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
+  }
+  {
+    ProfScope p("lm_combine", stream);
+    hipLaunchKernelGGL(lm_combine_kernel, dim3((T + 3) / 4), dim3(256), 0, stream, a, logp_old,
+                       logp, ratio, clipped, lse, eps_lo, eps_hi);
+  }
   return hipGetLastError();
 }
 
@@ -335,9 +341,15 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
   a.dh = static_cast<u16*>(dhidden);
   a.nA = a.Vp / BA;
   a.nT = (T + BT - 1) / BT;
-  hipLaunchKernelGGL(lm_gemm_kernel<kModeGrad>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
+  {
+    ProfScope p("lm_grad", stream);
+    hipLaunchKernelGGL(lm_gemm_kernel<kModeGrad>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
+  }
   a.nA = (H + BA - 1) / BA;
-  hipLaunchKernelGGL(lm_gemm_kernel<kModeDh>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
+  {
+    ProfScope p("lm_dh", stream);
+    hipLaunchKernelGGL(lm_gemm_kernel<kModeDh>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

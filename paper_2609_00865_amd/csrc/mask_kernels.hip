@@ -47,6 +47,7 @@ hipError_t launch_materialize(const mv_view_mask& m, int row_begin, int row_end,
   const int64_t total = int64_t(row_end - row_begin) * words;
   if (total == 0) return hipSuccess;
   const int64_t blocks = (total + 255) / 256;
+  ProfScope p("materialize", stream);
   hipLaunchKernelGGL(materialize_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, m.d, m.T,
                      row_begin, row_end, words, bits);
   return hipGetLastError();
@@ -65,6 +66,7 @@ __global__ void ppo_clip_kernel(int n, const float* ratio, const float* adv, flo
 hipError_t launch_ppo_clip(int n, const float* ratio, const float* adv, float eps_lo,
                            float eps_hi, float scale, float* out, hipStream_t stream) {
   if (n == 0) return hipSuccess;
+  ProfScope p("ppo_clip", stream);
   hipLaunchKernelGGL(ppo_clip_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, n, ratio, adv,
                      eps_lo, eps_hi, scale, out);
   return hipGetLastError();

@@ -26,6 +26,20 @@ constexpr int kNumXcd = 8;
 
 void set_error(const std::string& msg);
 
+// Brackets one kernel launch with HIP events when profiling is enabled.
+class ProfScope {
+ public:
+  ProfScope(const char* name, hipStream_t stream);
+  ~ProfScope();
+  ProfScope(const ProfScope&) = delete;
+  ProfScope& operator=(const ProfScope&) = delete;
+
+ private:
+  const char* name_;
+  hipStream_t stream_;
+  hipEvent_t start_ = nullptr;
+};
+
 }  // namespace mv
 
 // Device-side view of an uploaded mask (all int32 arrays).

@@ -113,12 +113,17 @@ mv_token_logprob_bwd = _sig("mv_token_logprob_bwd", ctypes.c_int, _P(LogprobShap
 mv_ppo_clip_dlogp = _sig("mv_ppo_clip_dlogp", ctypes.c_int, _i32, _vp, _vp, _f32, _f32, _f32,
                          _vp, _vp)
 
+mv_profile_enable = _sig("mv_profile_enable", ctypes.c_int, _i32)
+mv_profile_read = _sig("mv_profile_read", ctypes.c_int, ctypes.c_char_p, _P(ctypes.c_double),
+                       _P(_i32))
+
 EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_mask",
             "mv_view_mask_device_bytes", "mv_view_mask_upload", "mv_view_mask_stats",
             "mv_view_mask_death", "mv_view_mask_materialize", "mv_view_mask_materialize_host",
             "mv_view_mask_free", "mv_attn_fwd", "mv_attn_bwd_workspace_bytes", "mv_attn_bwd",
             "mv_token_logprob_workspace_bytes", "mv_token_logprob",
-            "mv_token_logprob_bwd_workspace_bytes", "mv_token_logprob_bwd", "mv_ppo_clip_dlogp"]
+            "mv_token_logprob_bwd_workspace_bytes", "mv_token_logprob_bwd", "mv_ppo_clip_dlogp",
+            "mv_profile_enable", "mv_profile_read"]
 
 
 def check(status: int) -> None:
@@ -319,3 +324,22 @@ def ppo_clip_dlogp(ratio, adv, eps_low=0.2, eps_high=0.2, scale=1.0, stream=None
     check(mv_ppo_clip_dlogp(ratio.numel(), _ptr(ratio), _ptr(adv), eps_low, eps_high, scale,
                             _ptr(out), _stream(stream)))
     return out
+
+
+# ---------------------------------------------------------------------------
+# kernel timing
+# ---------------------------------------------------------------------------
+KERNELS = ["attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq",
+           "lm_logits", "lm_combine", "lm_grad", "lm_dh", "materialize", "ppo_clip"]
+
+
+def profile_enable(on: bool = True) -> None:
+    check(mv_profile_enable(1 if on else 0))
+
+
+def profile_read(kernel: str):
+    """(total ms, launches) of the named kernel since profiling was enabled."""
+    ms = ctypes.c_double()
+    n = ctypes.c_int32()
+    check(mv_profile_read(kernel.encode(), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
