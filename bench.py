@@ -1,0 +1,259 @@
+"""Benchmark of the view-masked scoring hot path on one MI355X.
+
+One step = the whole path over one batch of synthetic input:
+  * view-masked attention forward + backward over 4 packed trajectories of
+    32768 tokens (28 query / 4 KV heads, head_dim 128, bf16; 16 compression
+    events per trajectory, 2048-token protected prompt), and
+  * the fused LM-head token log-prob / ratio / clip forward + backward over
+    32768 tokens (hidden 3584, vocab 152064, bf16).
+The eviction records are turned into the mask on the host before the timed
+region (the mask is an input, like the tensors); its build time is reported.
+
+Printed JSON (one line): useful TFLOP/s of the whole step (attention useful
+FLOPs 14 d P Hq with P the visible (row, key) pairs, plus LM-head 6 T H V),
+per-part breakdowns, the roofline of the dominant kernel measured with HIP
+events on the launch stream, and the CPU oracle's rate on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "view-masked attn fwd+bwd useful TFLOP/s + % MFMA peak; trajectory tokens/s"
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 flop/clk)
+PEAK_HBM_GBS = 8000.0
+ATTN_WORKLOAD = "b4x32k"
+LM_WORKLOAD = "lmhead"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run one plain 1 GiB device copy (PMC byte-counter calibration)")
+    ap.add_argument("--seed", type=int, default=0)
+    return ap.parse_args()
+
+
+def kernel_flops(P, d, hq, T_lm, H, V):
+    """Algorithmic FLOPs of one launch of each kernel."""
+    return {
+        "attn_fwd": 4.0 * d * P * hq,         # S = Q K^T and O = P V over visible pairs
+        "attn_bwd_dkdv": 8.0 * d * P * hq,    # S, dP recomputed; dV = P^T dO, dK = dS^T Q
+        "attn_bwd_dq": 6.0 * d * P * hq,      # S, dP recomputed; dQ = dS K
+        "lm_logits": 2.0 * T_lm * H * V,
+        "lm_grad": 2.0 * T_lm * H * V,
+        "lm_dh": 2.0 * T_lm * H * V,
+    }
+
+
+def cpu_baseline(trajs, wl, lmw, attn_flops_step, lm_flops_step):
+    """The oracle, untouched, on a bounded sample of the same workload."""
+    import torch
+    from oracle import attention as OA
+    from oracle import logprob as OL
+    from oracle import views as V
+    from paper_2609_00865_amd import synth
+
+    cores = torch.get_num_threads()
+    # attention: first trajectory, KV group 0, rows [0, R), fp32 forward + backward
+    R = 6144
+    G = wl.n_heads_q // wl.n_heads_kv
+    heads = list(range(G))
+    t0 = trajs[0]
+    sub = [synth.Trajectory(t0.begin, t0.begin + R,
+                            tuple(e for e in t0.edits if e.junction < t0.begin + R))]
+    gen = torch.Generator().manual_seed(99)
+    q = torch.randn(R, wl.n_heads_q, wl.head_dim, generator=gen).to(torch.bfloat16)
+    k = torch.randn(R, wl.n_heads_kv, wl.head_dim, generator=gen).to(torch.bfloat16)
+    v = torch.randn(R, wl.n_heads_kv, wl.head_dim, generator=gen).to(torch.bfloat16)
+    do = torch.randn(R, wl.n_heads_q, wl.head_dim, generator=gen).to(torch.bfloat16)
+    pairs = sum(V.view_sizes(sub[0]))
+    a0 = time.perf_counter()
+    OA.logittree(sub, q, k, v, dout=do, heads=heads, dtype=torch.float32, row_chunk=2048)
+    a_s = time.perf_counter() - a0
+    attn_rate = 14.0 * wl.head_dim * pairs * len(heads) / a_s
+    log(f"cpu oracle attention sample: {a_s:.2f}s, {attn_rate / 1e9:.1f} GFLOP/s")
+    # LM head: 128 tokens, fp32 forward + backward
+    n = 128
+    h, w, y, old, g = synth.make_logprob_inputs(n, lmw.hidden, lmw.vocab, 0)
+    l0 = time.perf_counter()
+    OL.token_logprob(h, w, y, old, dtype=torch.float32)
+    OL.token_logprob_bwd(h, w, y, g, dtype=torch.float32)
+    l_s = time.perf_counter() - l0
+    lm_rate = 6.0 * n * lmw.hidden * lmw.vocab / l_s
+    log(f"cpu oracle lm-head sample: {l_s:.2f}s, {lm_rate / 1e9:.1f} GFLOP/s")
+    step_s = attn_flops_step / attn_rate + lm_flops_step / lm_rate
+    return {
+        "value": (attn_flops_step + lm_flops_step) / step_s / 1e12,
+        "unit": "TFLOP/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": (f"attention: trajectory 0 rows [0,{R}) x KV group 0 ({len(heads)} heads), "
+                   f"fp32 LogitTree fwd+bwd, {a_s:.2f}s; lm-head: {n} tokens x full vocab, "
+                   f"fp32 fwd+bwd, {l_s:.2f}s; scaled to one step by useful FLOPs "
+                   f"(oracle step = {step_s:.0f}s)"),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see DESIGN.md, 'How the path would shard').", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_00865_amd import mv, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = synth.ATTN_WORKLOADS[ATTN_WORKLOAD]
+    lmw = synth.LOGPROB_WORKLOADS[LM_WORKLOAD]
+
+    # ---- inputs (resident in HBM before timing) ----
+    trajs = synth.make_trajectories(ATTN_WORKLOAD, args.seed)
+    b0 = time.perf_counter()
+    mask = mv.ViewMask(trajs)
+    build_ms = (time.perf_counter() - b0) * 1e3
+    mask.upload(dev)
+    st = mask.stats()
+    P = st["visible_pairs"]
+    log(f"mask built in {build_ms:.1f} ms: {st}")
+    q, k, v, do = synth.make_attn_tensors(ATTN_WORKLOAD, args.seed, device="cuda")
+    h, w, y, old, g = synth.make_logprob_inputs(lmw.n_tokens, lmw.hidden, lmw.vocab, args.seed,
+                                                device="cuda")
+    attn_ws = mv.attn_bwd_workspace(mask, q, k)
+    lp_ws = mv.token_logprob_workspace(h, w)
+    lpb_ws = mv.token_logprob_bwd_workspace(h, w)
+    torch.cuda.synchronize()
+    log("inputs resident")
+
+    def step():
+        o, lse = mv.attn_fwd(mask, q, k, v)
+        mv.attn_bwd(mask, q, k, v, o, do, lse, workspace=attn_ws)
+        logp, ratio, clipped, lse_lm = mv.token_logprob(h, w, y, old, lmw.eps_low, lmw.eps_high,
+                                                        workspace=lp_ws)
+        mv.token_logprob_bwd(h, w, y, lse_lm, g, workspace=lpb_ws)
+
+    for i in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    if args.calib_copy:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("calibration copy of 1 GiB done")
+
+    mv.profile_enable(True)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for i in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    kt = {}
+    for name in mv.KERNELS:
+        tot, n = mv.profile_read(name)
+        if n:
+            kt[name] = {"ms_per_launch": tot / n, "launches": n}
+    mv.profile_enable(False)
+    log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step (host wall {wall_ms:.2f})")
+
+    d, hq = wl.head_dim, wl.n_heads_q
+    T_lm, H, V = lmw.n_tokens, lmw.hidden, lmw.vocab
+    attn_useful = 14.0 * d * P * hq
+    lm_useful = 6.0 * T_lm * H * V
+    step_flops = attn_useful + lm_useful
+    per_launch = kernel_flops(P, d, hq, T_lm, H, V)
+    attn_ms = sum(kt[n]["ms_per_launch"] for n in kt if n.startswith("attn"))
+    lm_ms = sum(kt[n]["ms_per_launch"] for n in kt if n.startswith("lm"))
+    dom = max((n for n in kt if n in per_launch), key=lambda n: kt[n]["ms_per_launch"])
+    dom_tflops = per_launch[dom] / (kt[dom]["ms_per_launch"] * 1e-3) / 1e12
+    value = step_flops / (ms_per_step * 1e-3) / 1e12
+    tokens = wl.total_tokens
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{ATTN_WORKLOAD}: {wl.n_traj} x {wl.traj_len}-token packed trajectories, "
+                         f"{wl.n_heads_q}/{wl.n_heads_kv} heads, d={d}, 16 edits/trajectory, "
+                         f"attention fwd+bwd; {LM_WORKLOAD}: {T_lm} tokens x {H} hidden x {V} "
+                         f"vocab log-prob/ratio/clip fwd+bwd"),
+            "global_batch": wl.n_traj,
+            "seq_len": wl.traj_len,
+            "parallelism": "single GPU",
+            "visible_pairs": P,
+            "useful_tflop_per_step": round(step_flops / 1e12, 3),
+        },
+        "frac_peak": round(value / PEAK_BF16_TFLOPS, 4),
+        "tokens_per_s": round(tokens / (ms_per_step * 1e-3), 1),
+        "attn": {
+            "ms": round(attn_ms, 3),
+            "useful_tflops": round(attn_useful / (attn_ms * 1e-3) / 1e12, 2),
+            "frac_peak": round(attn_useful / (attn_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "trajectory_tokens_per_s": round(tokens / (attn_ms * 1e-3), 1),
+            "useful_tflop": round(attn_useful / 1e12, 3),
+        },
+        "lmhead": {
+            "ms": round(lm_ms, 3),
+            "useful_tflops": round(lm_useful / (lm_ms * 1e-3) / 1e12, 2),
+            "frac_peak": round(lm_useful / (lm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "tokens_per_s": round(T_lm / (lm_ms * 1e-3), 1),
+        },
+        "kernels_ms": {n: round(x["ms_per_launch"], 3) for n, x in kt.items()},
+        "mask_build_ms": round(build_ms, 2),
+        "roofline": {
+            "bound": "mfma",
+            "kernel": dom,
+            "achieved": round(dom_tflops, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(trajs, wl, lmw, attn_useful, lm_useful)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

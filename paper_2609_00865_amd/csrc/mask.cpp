@@ -135,7 +135,8 @@ void build_fwd_schedule(mv_view_mask& m) {
           ++skipped;
           continue;
         }
-        const bool is_full = lo >= i1;
+        // full tiles skip the predicate, so they must hold no padding keys
+        const bool is_full = lo >= i1 && j0 + BK <= T;
         m.k_list.push_back((kt << 1) | (is_full ? 1 : 0));
         (is_full ? full : partial) += 1;
       } else {

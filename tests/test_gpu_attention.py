@@ -75,6 +75,8 @@ def test_tiny_negative_controls():
     (64, 6, 3, [129, 64, 700], 4),
     (128, 2, 1, [1], 5),
     (128, 3, 1, [65], 6),
+    (128, 2, 2, [129], 7),
+    (64, 4, 2, [200, 57], 8),
 ])
 def test_ragged_packed(d, hq, hkv, lens, seed):
     """Several trajectories, lengths off the tile grid, GQA, both head sizes."""

@@ -139,3 +139,19 @@ def test_schedule_statistics_are_consistent():
     causal = sum((min(8192, (q + 1) * 128) - 1) // 64 + 1 for q in range(nq))
     assert st["tiles_full"] + st["tiles_partial"] + st["tiles_skipped"] == causal
     assert st["tiles_skipped"] > 0.3 * causal
+
+
+@pytest.mark.parametrize("T", [1, 63, 64, 65, 129, 257, 300])
+def test_ragged_tail_tiles_are_never_full(T):
+    """A key tile that runs past the last token is always partial: full tiles
+    skip the predicate and would otherwise admit padding keys."""
+    m = mv.ViewMask([synth.Trajectory(0, T, ())])
+    st = m.stats()
+    n_qt = (T + 127) // 128
+    causal = sum((min(T, (q + 1) * 128) - 1) // 64 + 1 for q in range(n_qt))
+    # with no edits a tile is full iff it is complete and lies below the diagonal
+    full = sum(1 for q in range(n_qt) for kt in range((min(T, (q + 1) * 128) - 1) // 64 + 1)
+               if kt * 64 + 64 <= T and kt * 64 + 63 <= q * 128)
+    assert st["tiles_full"] == full
+    assert st["tiles_full"] + st["tiles_partial"] == causal
+    assert _bits_ok(m, [synth.Trajectory(0, T, ())])
