@@ -61,6 +61,29 @@ def kernel_flops(P, d, hq, T_lm, H, V):
     }
 
 
+def measured_traffic(kernel):
+    """HBM bytes per launch recorded by the counter runs under profiles/, or None
+    when the kernel's sources have changed since (or were never measured)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "roofline_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        if line.startswith("#") or not line.strip():
+            continue
+        kv = dict(x.split("=", 1) for x in line.split())
+        if kv.get("kernel") != kernel:
+            continue
+        m = hashlib.sha256()
+        for n in kv["sources"].split(","):
+            with open(os.path.join(ROOT, "paper_2609_00865_amd", "csrc", n), "rb") as f:
+                m.update(f.read())
+        if m.hexdigest()[:16] != kv["sha256_16"]:
+            return None
+        return float(kv["fetch_bytes"]) + float(kv["write_bytes"])
+    return None
+
+
 def cpu_baseline(trajs, wl, lmw, attn_flops_step, lm_flops_step):
     """The oracle, untouched, on a bounded sample of the same workload."""
     import torch
@@ -71,7 +94,7 @@ def cpu_baseline(trajs, wl, lmw, attn_flops_step, lm_flops_step):
 
     cores = torch.get_num_threads()
     # attention: first trajectory, KV group 0, rows [0, R), fp32 forward + backward
-    R = 6144
+    R = 24576
     G = wl.n_heads_q // wl.n_heads_kv
     heads = list(range(G))
     t0 = trajs[0]
@@ -88,8 +111,8 @@ def cpu_baseline(trajs, wl, lmw, attn_flops_step, lm_flops_step):
     a_s = time.perf_counter() - a0
     attn_rate = 14.0 * wl.head_dim * pairs * len(heads) / a_s
     log(f"cpu oracle attention sample: {a_s:.2f}s, {attn_rate / 1e9:.1f} GFLOP/s")
-    # LM head: 128 tokens, fp32 forward + backward
-    n = 128
+    # LM head: 1024 tokens, fp32 forward + backward
+    n = 1024
     h, w, y, old, g = synth.make_logprob_inputs(n, lmw.hidden, lmw.vocab, 0)
     l0 = time.perf_counter()
     OL.token_logprob(h, w, y, old, dtype=torch.float32)
@@ -246,7 +269,8 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(dom),
+            "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated)",
         },
     }
     if not args.no_cpu_baseline:
