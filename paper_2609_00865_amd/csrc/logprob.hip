@@ -12,17 +12,24 @@
 // second pass of the same engine computes dH = G W (contraction over the
 // vocabulary).
 //
-// Tile engine: 256 threads, 4 waves in a 2 x 2 grid, each wave 128 rows of
-// the "A" side (vocab, or hidden for dH) x 128 tokens, MFMA 32x32x16 with
-// tokens on lanes.  The next 64-wide k slice is loaded into registers while
-// the current one is multiplied from LDS.
+// Tile engine: 512 threads = 8 waves (two per SIMD) in a 2 x 4 grid over a
+// 256 A-row x 256 token tile; each wave owns 128 A-rows x 64 tokens (tokens on
+// lanes), MFMA 32x32x16.  The 64-wide k slices are double-buffered in LDS with
+// one barrier per slice: while a slice is multiplied, the next one is written
+// from registers into the other buffer and the one after is loaded from HBM.
+// Tiles are ordered so that the blocks resident on one XCD at a time form a
+// compact 2-D patch (a few token tiles x several A tiles) and share operand
+// slices in that XCD's L2.
 #include "mv_device.h"
 
 namespace mv {
 
 namespace {
 constexpr int BA = 256, BT = 256, BKK = 64;
-constexpr int PAD = BKK + 8;
+constexpr int PAD = BKK + 8;               // LDS row stride (bf16), conflict-free operand reads
+constexpr int STAGE = (BA + BT) * PAD;     // one k slice of both operands
+constexpr int NTHR = 512;
+constexpr int GROUP_T = 4;                 // token tiles per raster group
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -47,47 +54,48 @@ struct LmArgs {
 };
 
 template <int MODE>
-__global__ __launch_bounds__(256, 1) void lm_gemm_kernel(LmArgs a) {
-  __shared__ __align__(16) u16 sA[BA * PAD];
-  __shared__ __align__(16) u16 sB[BT * PAD];
+__global__ __launch_bounds__(NTHR, 1) void lm_gemm_kernel(LmArgs a) {
+  __shared__ __align__(16) u16 smem[2 * STAGE];
 
-  // tile order: groups of 16 token tiles sweep the A side, so concurrently
-  // running blocks share both operands' k slices in L2 / MALL
-  const int L = blockIdx.x;
-  constexpr int GT = 16;
-  const int per_group = GT * a.nA;
-  const int grp = L / per_group;
-  const int rem = L % per_group;
-  const int t_in = min(GT, a.nT - grp * GT);
-  const int tt = grp * GT + rem % t_in;
+  // Blocks are dealt to XCDs round-robin; give each XCD a contiguous range of
+  // the rasterised tile order (groups of GROUP_T token tiles x all A tiles).
+  const int n_tiles = a.nA * a.nT;
+  const int per_xcd = (n_tiles + kNumXcd - 1) / kNumXcd;
+  int xcd, local;
+  xcd_split(xcd, local);
+  const int L = xcd * per_xcd + local;
+  if (local >= per_xcd || L >= n_tiles) return;
+  const int grp = L / (GROUP_T * a.nA);
+  const int rem = L % (GROUP_T * a.nA);
+  const int t_in = min(GROUP_T, a.nT - grp * GROUP_T);
+  const int tt = grp * GROUP_T + rem % t_in;
   const int at = rem / t_in;
-  if (tt >= a.nT || at >= a.nA) return;
   const int a0 = at * BA, t0 = tt * BT;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int c = lane & 31, g = lane >> 5;
-  const int wa = wave >> 1, wt = wave & 1;
+  const int wa = wave >> 2, wt = wave & 3;
 
   const int K = (MODE == kModeDh) ? a.Vp : a.H;
-  // "A" operand source rows / "B" operand source rows
   const int a_rows = (MODE == kModeDh) ? a.H : a.V;
+  const int nk = K / BKK;
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  uint4 ra[8], rb[8];
+  uint4 ra[4], rb[4];
   auto load = [&](int k0) {
     const uint4 z = make_uint4(0, 0, 0, 0);
     if (MODE == kModeDh) {
       // A = W^T: rows are hidden units, k = vocab; read vocab-row pairs
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int idx = tid + r * 256;
+      for (int r = 0; r < 2; ++r) {
+        const int idx = tid + r * NTHR;
         const int pp = idx % (BKK / 2), cc = idx / (BKK / 2);
         const int v = k0 + 2 * pp;
         const bool hok = a0 + cc * 8 < a.H;
@@ -97,16 +105,16 @@ __global__ __launch_bounds__(256, 1) void lm_gemm_kernel(LmArgs a) {
       }
     } else {
 #pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const int idx = tid + r * 256;
+      for (int r = 0; r < 4; ++r) {
+        const int idx = tid + r * NTHR;
         const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
         const int v = a0 + row;
         ra[r] = v < a_rows ? ld16(a.w + size_t(v) * a.H + k0 + cc) : z;
       }
     }
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int idx = tid + r * 256;
+    for (int r = 0; r < 4; ++r) {
+      const int idx = tid + r * NTHR;
       const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
       const int t = t0 + row;
       if (MODE == kModeDh)
@@ -115,14 +123,16 @@ __global__ __launch_bounds__(256, 1) void lm_gemm_kernel(LmArgs a) {
         rb[r] = t < a.T ? ld16(a.h + size_t(t) * a.H + k0 + cc) : z;
     }
   };
-  auto store = [&]() {
+  auto store = [&](u16* sA) {
+    u16* sB = sA + BA * PAD;
     if (MODE == kModeDh) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int idx = tid + r * 256;
+      for (int r = 0; r < 2; ++r) {
+        const int idx = tid + r * NTHR;
         const int pp = idx % (BKK / 2), cc = idx / (BKK / 2);
         const uint32_t lo[4] = {ra[2 * r].x, ra[2 * r].y, ra[2 * r].z, ra[2 * r].w};
-        const uint32_t hi[4] = {ra[2 * r + 1].x, ra[2 * r + 1].y, ra[2 * r + 1].z, ra[2 * r + 1].w};
+        const uint32_t hi[4] = {ra[2 * r + 1].x, ra[2 * r + 1].y, ra[2 * r + 1].z,
+                                ra[2 * r + 1].w};
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
           const uint32_t even = (lo[w] & 0xffffu) | (hi[w] << 16);
@@ -133,49 +143,55 @@ __global__ __launch_bounds__(256, 1) void lm_gemm_kernel(LmArgs a) {
       }
     } else {
 #pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const int idx = tid + r * 256;
+      for (int r = 0; r < 4; ++r) {
+        const int idx = tid + r * NTHR;
         const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
         st16(&sA[row * PAD + cc], ra[r]);
       }
     }
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int idx = tid + r * 256;
+    for (int r = 0; r < 4; ++r) {
+      const int idx = tid + r * NTHR;
       const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
       st16(&sB[row * PAD + cc], rb[r]);
     }
   };
 
   load(0);
-  for (int k0 = 0; k0 < K; k0 += BKK) {
-    __syncthreads();
-    store();
-    __syncthreads();
-    if (k0 + BKK < K) load(k0 + BKK);
+  store(smem);
+  if (nk > 1) load(BKK);
+  __syncthreads();
+  for (int kk = 0; kk < nk; ++kk) {
+    const u16* sA = smem + (kk & 1) * STAGE;
+    const u16* sB = sA + BA * PAD;
 #pragma unroll
     for (int ks = 0; ks < BKK / 16; ++ks) {
-      bf16x8 af[4], bf[4];
+      bf16x8 af[4], bf[2];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         af[i] = as_bf16x8(ld16(&sA[(wa * 128 + i * 32 + c) * PAD + ks * 16 + g * 8]));
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        bf[j] = as_bf16x8(ld16(&sB[(wt * 128 + j * 32 + c) * PAD + ks * 16 + g * 8]));
+      for (int j = 0; j < 2; ++j)
+        bf[j] = as_bf16x8(ld16(&sB[(wt * 64 + j * 32 + c) * PAD + ks * 16 + g * 8]));
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
     }
+    if (kk + 1 < nk) {
+      store(smem + ((kk + 1) & 1) * STAGE);
+      if (kk + 2 < nk) load((kk + 2) * BKK);
+    }
+    __syncthreads();
   }
 
   // acc[i][j][r]: A-row a0 + wa*128 + i*32 + (r/4)*8 + g*4 + r%4,
-  //               token t0 + wt*128 + j*32 + c
+  //               token t0 + wt*64 + j*32 + c
   const int arow0 = a0 + wa * 128;
   if (MODE == kModeLogits) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int t = t0 + wt * 128 + j * 32 + c;
+    for (int j = 0; j < 2; ++j) {
+      const int t = t0 + wt * 64 + j * 32 + c;
       const int y = t < a.T ? a.tgt[t] : -1;
       float mx = -INFINITY;
 #pragma unroll
@@ -201,8 +217,8 @@ __global__ __launch_bounds__(256, 1) void lm_gemm_kernel(LmArgs a) {
     }
   } else if (MODE == kModeGrad) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int t = t0 + wt * 128 + j * 32 + c;
+    for (int j = 0; j < 2; ++j) {
+      const int t = t0 + wt * 64 + j * 32 + c;
       if (t >= a.T) continue;
       const int y = a.tgt[t];
       const float gt = y >= 0 ? a.g[t] : 0.f;
@@ -227,8 +243,8 @@ __global__ __launch_bounds__(256, 1) void lm_gemm_kernel(LmArgs a) {
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int t = t0 + wt * 128 + j * 32 + c;
+    for (int j = 0; j < 2; ++j) {
+      const int t = t0 + wt * 64 + j * 32 + c;
       if (t >= a.T) continue;
       u16* out = a.dh + size_t(t) * a.H;
 #pragma unroll
@@ -292,6 +308,11 @@ static char* align_ptr(void* p) {
   return reinterpret_cast<char*>((reinterpret_cast<uintptr_t>(p) + 255) & ~uintptr_t(255));
 }
 
+static dim3 gemm_grid(const LmArgs& a) {
+  const int per_xcd = (a.nA * a.nT + kNumXcd - 1) / kNumXcd;
+  return dim3(per_xcd * kNumXcd);
+}
+
 hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, const void* hidden,
                               const void* weight, const int32_t* target, const float* logp_old,
                               float* logp, float* ratio, float* clipped, float* lse, void* ws,
@@ -312,7 +333,7 @@ hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, c
   a.nT = (T + BT - 1) / BT;
   {
     ProfScope p("lm_logits", stream);
-    hipLaunchKernelGGL(lm_gemm_kernel<kModeLogits>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(lm_gemm_kernel<kModeLogits>, gemm_grid(a), dim3(NTHR), 0, stream, a);
   }
   {
     ProfScope p("lm_combine", stream);
@@ -343,12 +364,12 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
   a.nT = (T + BT - 1) / BT;
   {
     ProfScope p("lm_grad", stream);
-    hipLaunchKernelGGL(lm_gemm_kernel<kModeGrad>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(lm_gemm_kernel<kModeGrad>, gemm_grid(a), dim3(NTHR), 0, stream, a);
   }
   a.nA = (H + BA - 1) / BA;
   {
     ProfScope p("lm_dh", stream);
-    hipLaunchKernelGGL(lm_gemm_kernel<kModeDh>, dim3(a.nA * a.nT), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(lm_gemm_kernel<kModeDh>, gemm_grid(a), dim3(NTHR), 0, stream, a);
   }
   return hipGetLastError();
 }
