@@ -76,7 +76,10 @@ def measured_traffic(kernel):
             continue
         m = hashlib.sha256()
         for n in kv["sources"].split(","):
-            with open(os.path.join(ROOT, "paper_2609_00865_amd", "csrc", n), "rb") as f:
+            src = os.path.join(ROOT, "paper_2609_00865_amd", "csrc", n)
+            if not os.path.exists(src):
+                return None
+            with open(src, "rb") as f:
                 m.update(f.read())
         if m.hexdigest()[:16] != kv["sha256_16"]:
             return None

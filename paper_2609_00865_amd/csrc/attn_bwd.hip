@@ -250,13 +250,13 @@ template <int D>
 __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   constexpr int BK = kBwdTileK, BQ = kBwdBlockQ;
   constexpr int KS = D / 16, DB = D / 32;
-  constexpr int RPAD = D + 8, TPAD = BQ + 8;
-  constexpr int PLD = (BQ / 2) * (D / 8) / 256;  // row-pair loads per thread per tensor
+  constexpr int RPAD = D + 8;
+  constexpr int RLD = BQ * (D / 8) / 256;  // 16-byte row loads per thread per tensor
 
+  // Q and dO blocks are staged row-major only; their transposed operands are
+  // read with the transposing LDS read (ld_operand_tr).
   __shared__ __align__(16) u16 sQ[BQ * RPAD];
   __shared__ __align__(16) u16 sdO[BQ * RPAD];
-  __shared__ __align__(16) u16 sQt[D * TPAD];
-  __shared__ __align__(16) u16 sdOt[D * TPAD];
   __shared__ __align__(16) float sL[BQ];
   __shared__ __align__(16) float sD[BQ];
 
@@ -297,22 +297,20 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     }
 
   const size_t q_row = size_t(a.Hq) * D;
-  uint4 qreg[PLD][2], dreg[PLD][2];
+  uint4 qreg[RLD], dreg[RLD];
   float lreg = 0.f, dreg1 = 0.f;
   auto load_block = [&](int hh, int qb) {
     const int i0 = qb * BQ;
     const u16* qb_ = a.q + size_t(hh) * D;
     const u16* db_ = a.dout + size_t(hh) * D;
 #pragma unroll
-    for (int r = 0; r < PLD; ++r) {
+    for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
-      const int pp = idx % (BQ / 2), cc = idx / (BQ / 2);
-      const int i = i0 + 2 * pp;
+      const int row = idx / (D / 8), cc = idx % (D / 8);
+      const int i = i0 + row;
       const uint4 z = make_uint4(0, 0, 0, 0);
-      qreg[r][0] = i < T ? ld16(qb_ + size_t(i) * q_row + cc * 8) : z;
-      qreg[r][1] = i + 1 < T ? ld16(qb_ + size_t(i + 1) * q_row + cc * 8) : z;
-      dreg[r][0] = i < T ? ld16(db_ + size_t(i) * q_row + cc * 8) : z;
-      dreg[r][1] = i + 1 < T ? ld16(db_ + size_t(i + 1) * q_row + cc * 8) : z;
+      qreg[r] = i < T ? ld16(qb_ + size_t(i) * q_row + cc * 8) : z;
+      dreg[r] = i < T ? ld16(db_ + size_t(i) * q_row + cc * 8) : z;
     }
     if (tid < BQ) {
       const int i = i0 + tid;
@@ -322,15 +320,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   };
   auto store_block = [&]() {
 #pragma unroll
-    for (int r = 0; r < PLD; ++r) {
+    for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
-      const int pp = idx % (BQ / 2), cc = idx / (BQ / 2);
-      st16(&sQ[(2 * pp) * RPAD + cc * 8], qreg[r][0]);
-      st16(&sQ[(2 * pp + 1) * RPAD + cc * 8], qreg[r][1]);
-      st16(&sdO[(2 * pp) * RPAD + cc * 8], dreg[r][0]);
-      st16(&sdO[(2 * pp + 1) * RPAD + cc * 8], dreg[r][1]);
-      store_pair_t<TPAD>(sQt, 2 * pp, cc * 8, qreg[r][0], qreg[r][1]);
-      store_pair_t<TPAD>(sdOt, 2 * pp, cc * 8, dreg[r][0], dreg[r][1]);
+      const int row = idx / (D / 8), cc = idx % (D / 8);
+      st16(&sQ[row * RPAD + cc * 8], qreg[r]);
+      st16(&sdO[row * RPAD + cc * 8], dreg[r]);
     }
     if (tid < BQ) {
       sL[tid] = lreg;
@@ -397,9 +391,9 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        const int off = (db * 32 + c) * TPAD + ks * 16 + g * 8;
-        dv[db] = mfma32(as_bf16x8(ld16(&sdOt[off])), pf[ks], dv[db]);
-        dk[db] = mfma32(as_bf16x8(ld16(&sQt[off])), dsf[ks], dk[db]);
+        // dO^T and Q^T operands: columns db*32.. of rows ks*16.. in accumulator order
+        dv[db] = mfma32(ld_operand_tr<RPAD>(sdO, ks * 16, db * 32), pf[ks], dv[db]);
+        dk[db] = mfma32(ld_operand_tr<RPAD>(sQ, ks * 16, db * 32), dsf[ks], dk[db]);
       }
   }
 
