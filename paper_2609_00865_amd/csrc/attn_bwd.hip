@@ -62,23 +62,6 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
   a.Dd[size_t(h) * a.T + i] = acc;
 }
 
-// Transposed 16-bit pair store: rows (r0, r0+1) x 8 columns from two 16-byte
-// row chunks into a [col][row] LDS tile whose row positions are permuted by
-// perm_col (so that MFMA operand reads are single 16-byte loads).
-template <int PAD>
-__device__ __forceinline__ void store_pair_t(u16* dst, int r0, int c0, const uint4& lo4,
-                                             const uint4& hi4) {
-  const int col = perm_col(r0);
-  const uint32_t lo[4] = {lo4.x, lo4.y, lo4.z, lo4.w}, hi[4] = {hi4.x, hi4.y, hi4.z, hi4.w};
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    const uint32_t even = (lo[w] & 0xffffu) | (hi[w] << 16);
-    const uint32_t odd = (lo[w] >> 16) | (hi[w] & 0xffff0000u);
-    *reinterpret_cast<uint32_t*>(&dst[(c0 + 2 * w) * PAD + col]) = even;
-    *reinterpret_cast<uint32_t*>(&dst[(c0 + 2 * w + 1) * PAD + col]) = odd;
-  }
-}
-
 // ---------------------------------------------------------------------------
 // 2. dQ
 // ---------------------------------------------------------------------------
@@ -86,13 +69,11 @@ template <int D>
 __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
   constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
   constexpr int KS = D / 16, DB = D / 32;
-  constexpr int RPAD = D + 8, TPAD = BK + 8;
-  constexpr int RLD = BK * D / 8 / 256;          // row-major V loads per thread
-  constexpr int PLD = (BK / 2) * (D / 8) / 256;  // K pair loads per thread
+  constexpr int RPAD = D + 8;
+  constexpr int RLD = BK * D / 8 / 256;          // row-major K and V loads per thread
 
   __shared__ __align__(16) u16 sK[BK * RPAD];
   __shared__ __align__(16) u16 sV[BK * RPAD];
-  __shared__ __align__(16) u16 sKt[D * TPAD];
   __shared__ __align__(16) int sOm[BK];
 
   int xcd, local;
@@ -129,7 +110,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
   const size_t kv_row = size_t(a.Hkv) * D;
   const u16* kbase = a.k + size_t(hk) * D;
   const u16* vbase = a.v + size_t(hk) * D;
-  uint4 vreg[RLD], kreg[PLD][2];
+  uint4 vreg[RLD], kreg[RLD];
   int omreg = 0;
   auto load_tile = [&](int kt) {
     const int j0 = kt * BK;
@@ -138,15 +119,9 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
       const int j = j0 + row;
-      vreg[r] = j < T ? ld16(vbase + size_t(j) * kv_row + col) : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int r = 0; r < PLD; ++r) {
-      const int idx = tid + r * 256;
-      const int pp = idx % (BK / 2), cc = idx / (BK / 2);
-      const int j = j0 + 2 * pp;
-      kreg[r][0] = j < T ? ld16(kbase + size_t(j) * kv_row + cc * 8) : make_uint4(0, 0, 0, 0);
-      kreg[r][1] = j + 1 < T ? ld16(kbase + size_t(j + 1) * kv_row + cc * 8) : make_uint4(0, 0, 0, 0);
+      const uint4 z = make_uint4(0, 0, 0, 0);
+      vreg[r] = j < T ? ld16(vbase + size_t(j) * kv_row + col) : z;
+      kreg[r] = j < T ? ld16(kbase + size_t(j) * kv_row + col) : z;
     }
     if (tid < BK) omreg = (j0 + tid < T) ? a.mask.omega[j0 + tid] : 0;
   };
@@ -156,14 +131,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
       st16(&sV[row * RPAD + col], vreg[r]);
-    }
-#pragma unroll
-    for (int r = 0; r < PLD; ++r) {
-      const int idx = tid + r * 256;
-      const int pp = idx % (BK / 2), cc = idx / (BK / 2);
-      st16(&sK[(2 * pp) * RPAD + cc * 8], kreg[r][0]);
-      st16(&sK[(2 * pp + 1) * RPAD + cc * 8], kreg[r][1]);
-      store_pair_t<TPAD>(sKt, 2 * pp, cc * 8, kreg[r][0], kreg[r][1]);
+      st16(&sK[row * RPAD + col], kreg[r]);
     }
     if (tid < BK) sOm[tid] = omreg;
   };
@@ -224,8 +192,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        const bf16x8 kf = as_bf16x8(ld16(&sKt[(db * 32 + c) * TPAD + ks * 16 + g * 8]));
-        acc[db] = mfma32(kf, dsf[ks], acc[db]);
+        // K^T operand: column block db of keys ks*16.. in accumulator order
+        acc[db] = mfma32(ld_operand_tr<RPAD>(sK, ks * 16, db * 32), dsf[ks], acc[db]);
       }
   }
 

@@ -6,9 +6,9 @@
 // on the accumulator rows, one query per lane, so the softmax statistics of a
 // row stay inside a lane pair), applies the shared visibility predicate on
 // partial tiles only, updates the online softmax in base 2, and accumulates
-// O^T += V^T P^T with a second MFMA.  K is staged row-major and V transposed in
-// LDS; the next tile's global loads are in flight during the current tile's
-// math.  Query tiles are visited heaviest first and the heads of one query
+// O^T += V^T P^T with a second MFMA.  K and V are staged row-major in LDS; the
+// V^T operand is read with the transposing LDS read.  The next tile's global
+// loads are in flight during the current tile's math.  Query tiles are visited heaviest first and the heads of one query
 // tile are kept on one XCD so that GQA heads share K/V in that XCD's L2.
 #include "mv_device.h"
 #include "mv_predicate.h"
@@ -31,14 +31,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
   constexpr int KS = D / 16;          // MFMA k-steps over the head dimension
   constexpr int DB = D / 32;          // 32-row blocks of O^T
-  constexpr int KPAD = D + 8;         // row stride of K in LDS (bf16)
-  constexpr int VPAD = BK + 8;        // row stride of V^T in LDS (bf16)
-  constexpr int KLD = BK * D / 8 / 256;        // 16-byte K loads per thread
-  constexpr int VLD = (BK / 2) * (D / 8) / 256;  // key pairs x 8-d chunks per thread
-  static_assert(KLD >= 1 && VLD >= 1, "tile too small for 256 threads");
+  constexpr int KPAD = D + 8;         // K row stride (bf16): row reads across 32 lanes hit distinct banks
+  constexpr int VPAD = D + 16;        // V row stride: the 4 rows of a transposing read hit distinct banks
+  constexpr int KLD = BK * D / 8 / 256;        // 16-byte K (and V) loads per thread
+  static_assert(KLD >= 1, "tile too small for 256 threads");
 
   __shared__ __align__(16) u16 sK[BK * KPAD];
-  __shared__ __align__(16) u16 sVt[D * VPAD];
+  __shared__ __align__(16) u16 sV[BK * VPAD];
   __shared__ __align__(16) int sOm[BK];
 
   int xcd, local;
@@ -74,7 +73,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   const u16* kbase = a.k + size_t(hk) * D;
   const u16* vbase = a.v + size_t(hk) * D;
 
-  uint4 kreg[KLD], vreg[VLD][2];
+  uint4 kreg[KLD], vreg[KLD];
   int omreg = 0;
   auto load_tile = [&](int kt) {
     const int j0 = kt * BK;
@@ -83,15 +82,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
       const int j = j0 + row;
-      kreg[r] = j < T ? ld16(kbase + size_t(j) * kv_row + col) : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int r = 0; r < VLD; ++r) {
-      const int idx = tid + r * 256;
-      const int pp = idx % (BK / 2), cc = idx / (BK / 2);
-      const int j = j0 + 2 * pp;
-      vreg[r][0] = j < T ? ld16(vbase + size_t(j) * kv_row + cc * 8) : make_uint4(0, 0, 0, 0);
-      vreg[r][1] = j + 1 < T ? ld16(vbase + size_t(j + 1) * kv_row + cc * 8) : make_uint4(0, 0, 0, 0);
+      const uint4 z = make_uint4(0, 0, 0, 0);
+      kreg[r] = j < T ? ld16(kbase + size_t(j) * kv_row + col) : z;
+      vreg[r] = j < T ? ld16(vbase + size_t(j) * kv_row + col) : z;
     }
     if (tid < BK) omreg = (j0 + tid < T) ? a.mask.omega[j0 + tid] : 0;
   };
@@ -101,23 +94,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
       st16(&sK[row * KPAD + col], kreg[r]);
-    }
-#pragma unroll
-    for (int r = 0; r < VLD; ++r) {
-      const int idx = tid + r * 256;
-      const int pp = idx % (BK / 2), cc = idx / (BK / 2);
-      const int col = perm_col(2 * pp);
-      const uint32_t* lo = reinterpret_cast<const uint32_t*>(&vreg[r][0]);
-      const uint32_t* hi = reinterpret_cast<const uint32_t*>(&vreg[r][1]);
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        // d = cc*8 + 2w and cc*8 + 2w + 1; pair (key 2pp, key 2pp+1)
-        const uint32_t a0 = lo[w], a1 = hi[w];
-        const uint32_t even = (a0 & 0xffffu) | (a1 << 16);
-        const uint32_t odd = (a0 >> 16) | (a1 & 0xffff0000u);
-        *reinterpret_cast<uint32_t*>(&sVt[(cc * 8 + 2 * w) * VPAD + col]) = even;
-        *reinterpret_cast<uint32_t*>(&sVt[(cc * 8 + 2 * w + 1) * VPAD + col]) = odd;
-      }
+      st16(&sV[row * VPAD + col], vreg[r]);
     }
     if (tid < BK) sOm[tid] = omreg;
   };
@@ -198,8 +175,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        const bf16x8 vf = as_bf16x8(ld16(&sVt[(db * 32 + c) * VPAD + ks * 16 + g * 8]));
-        oacc[db] = mfma32(vf, pf[ks], oacc[db]);
+        // V^T operand: column block db of keys ks*16.. in accumulator order
+        oacc[db] = mfma32(ld_operand_tr<VPAD>(sV, ks * 16, db * 32), pf[ks], oacc[db]);
       }
   }
 

@@ -14,7 +14,8 @@
 //
 // Tile engine: 512 threads = 8 waves (two per SIMD) in a 2 x 4 grid over a
 // 256 A-row x 256 token tile; each wave owns 128 A-rows x 64 tokens (tokens on
-// lanes), MFMA 32x32x16.  The 64-wide k slices are double-buffered in LDS with
+// lanes), MFMA 32x32x16 (the dH pass reads its W^T operand from a row-major W
+// slice with the transposing LDS read).  The 64-wide k slices are double-buffered in LDS with
 // one barrier per slice: while a slice is multiplied, the next one is written
 // from registers into the other buffer and the one after is loaded from HBM.
 // Tiles are ordered so that the blocks resident on one XCD at a time form a
@@ -27,7 +28,9 @@ namespace mv {
 namespace {
 constexpr int BA = 256, BT = 256, BKK = 64;
 constexpr int PAD = BKK + 8;               // LDS row stride (bf16), conflict-free operand reads
+constexpr int WPAD = BA + 16;              // row stride of the row-major W slice of the dH pass
 constexpr int STAGE = (BA + BT) * PAD;     // one k slice of both operands
+static_assert(BKK * WPAD <= BA * PAD, "dH pass W slice must fit the A region");
 constexpr int NTHR = 512;
 constexpr int GROUP_T = 4;                 // token tiles per raster group
 constexpr float kLog2e = 1.4426950408889634f;
@@ -92,16 +95,14 @@ __global__ __launch_bounds__(NTHR, 1) void lm_gemm_kernel(LmArgs a) {
   auto load = [&](int k0) {
     const uint4 z = make_uint4(0, 0, 0, 0);
     if (MODE == kModeDh) {
-      // A = W^T: rows are hidden units, k = vocab; read vocab-row pairs
+      // W slice [64 vocab rows][256 hidden], staged row-major; the A = W^T
+      // operand is read across its rows with the transposing LDS read
 #pragma unroll
-      for (int r = 0; r < 2; ++r) {
+      for (int r = 0; r < 4; ++r) {
         const int idx = tid + r * NTHR;
-        const int pp = idx % (BKK / 2), cc = idx / (BKK / 2);
-        const int v = k0 + 2 * pp;
-        const bool hok = a0 + cc * 8 < a.H;
-        const u16* p = a.w + size_t(v) * a.H + a0 + cc * 8;
-        ra[2 * r] = (hok && v < a.V) ? ld16(p) : z;
-        ra[2 * r + 1] = (hok && v + 1 < a.V) ? ld16(p + a.H) : z;
+        const int row = idx / (BA / 8), cc = (idx % (BA / 8)) * 8;
+        const int v = k0 + row;
+        ra[r] = (v < a.V && a0 + cc < a.H) ? ld16(a.w + size_t(v) * a.H + a0 + cc) : z;
       }
     } else {
 #pragma unroll
@@ -127,19 +128,10 @@ __global__ __launch_bounds__(NTHR, 1) void lm_gemm_kernel(LmArgs a) {
     u16* sB = sA + BA * PAD;
     if (MODE == kModeDh) {
 #pragma unroll
-      for (int r = 0; r < 2; ++r) {
+      for (int r = 0; r < 4; ++r) {
         const int idx = tid + r * NTHR;
-        const int pp = idx % (BKK / 2), cc = idx / (BKK / 2);
-        const uint32_t lo[4] = {ra[2 * r].x, ra[2 * r].y, ra[2 * r].z, ra[2 * r].w};
-        const uint32_t hi[4] = {ra[2 * r + 1].x, ra[2 * r + 1].y, ra[2 * r + 1].z,
-                                ra[2 * r + 1].w};
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const uint32_t even = (lo[w] & 0xffffu) | (hi[w] << 16);
-          const uint32_t odd = (lo[w] >> 16) | (hi[w] & 0xffff0000u);
-          *reinterpret_cast<uint32_t*>(&sA[(cc * 8 + 2 * w) * PAD + 2 * pp]) = even;
-          *reinterpret_cast<uint32_t*>(&sA[(cc * 8 + 2 * w + 1) * PAD + 2 * pp]) = odd;
-        }
+        const int row = idx / (BA / 8), cc = (idx % (BA / 8)) * 8;
+        st16(&sA[row * WPAD + cc], ra[r]);
       }
     } else {
 #pragma unroll
@@ -169,7 +161,9 @@ __global__ __launch_bounds__(NTHR, 1) void lm_gemm_kernel(LmArgs a) {
       bf16x8 af[4], bf[2];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        af[i] = as_bf16x8(ld16(&sA[(wa * 128 + i * 32 + c) * PAD + ks * 16 + g * 8]));
+        af[i] = (MODE == kModeDh)
+                    ? ld_operand_tr<WPAD, true>(sA, ks * 16, wa * 128 + i * 32)
+                    : as_bf16x8(ld16(&sA[(wa * 128 + i * 32 + c) * PAD + ks * 16 + g * 8]));
 #pragma unroll
       for (int j = 0; j < 2; ++j)
         bf[j] = as_bf16x8(ld16(&sB[(wt * 64 + j * 32 + c) * PAD + ks * 16 + g * 8]));

@@ -54,14 +54,6 @@ __device__ __forceinline__ bf16x8 to_operand(const f32x16& acc, int base) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Column of key offset kk (0..63) inside a transposed LDS tile: the 16-key
-// groups are permuted so that one 16-byte read gives a lane the 8 keys its
-// accumulator rows hold (see mfma32: rows g*4..g*4+3 and 8+g*4..8+g*4+3).
-__device__ __forceinline__ int perm_col(int kk) {
-  const int r = kk & 15;
-  return (kk & ~15) + ((r >> 2) & 1) * 8 + (r >> 3) * 4 + (r & 3);
-}
-
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
@@ -74,14 +66,16 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 // rbase + g*4 + {0,1,2,3} and rbase + 8 + g*4 + {0,1,2,3}: the k order of an
 // MFMA accumulator's rows (see mfma32), so the result pairs with an operand
 // taken straight from an accumulator.
-template <int PAD>
+// With NATURAL = true the 8 rows are rbase + g*8 + {0..7} instead, the k order
+// of an operand read from a row-major tile along its rows.
+template <int PAD, bool NATURAL = false>
 __device__ __forceinline__ bf16x8 ld_operand_tr(const u16* tile, int rbase, int col0) {
   const int lane = threadIdx.x & 63;
   const int l = lane & 15;
-  const int row = rbase + (lane >> 5) * 4 + (l >> 2);
+  const int row = rbase + (lane >> 5) * (NATURAL ? 8 : 4) + (l >> 2);
   const int col = col0 + ((lane >> 4) & 1) * 16 + 4 * (l & 3);
   const u16* p0 = tile + row * PAD + col;
-  const u16* p1 = p0 + 8 * PAD;
+  const u16* p1 = p0 + (NATURAL ? 4 : 8) * PAD;
   const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0));
   const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p1));
   typedef short i16x8 __attribute__((ext_vector_type(8)));
