@@ -31,7 +31,7 @@ constexpr int PAD = BKK + 8;               // LDS row stride (bf16), conflict-fr
 constexpr int WPAD = BA + 16;              // row stride of the row-major W slice of the dH pass
 constexpr int STAGE = (BA + BT) * PAD;     // one k slice of both operands
 static_assert(BKK * WPAD <= BA * PAD, "dH pass W slice must fit the A region");
-constexpr int NTHR = 512;
+constexpr int NWAVES = 8;                 // waves per tile (2 x NWAVES/2 grid)
 constexpr int GROUP_T = 4;                 // token tiles per raster group
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
@@ -56,8 +56,13 @@ struct LmArgs {
   int nA, nT;         // tiles along the A side and along tokens
 };
 
-template <int MODE>
-__global__ __launch_bounds__(NTHR, 1) void lm_gemm_kernel(LmArgs a) {
+template <int MODE, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
+  constexpr int NT = NW * 64;              // threads
+  constexpr int WTOK = 256 / (NW / 2);     // tokens per wave (2 waves along the A side)
+  constexpr int NJ = WTOK / 32;            // 32-token MFMA blocks per wave
+  constexpr int LDA = (BA * BKK / 8) / NT; // 16-byte loads per thread, A slice
+  constexpr int LDB = (BT * BKK / 8) / NT; // 16-byte loads per thread, token slice
   __shared__ __align__(16) u16 smem[2 * STAGE];
 
   // Blocks are dealt to XCDs round-robin; give each XCD a contiguous range of
@@ -77,73 +82,68 @@ __global__ __launch_bounds__(NTHR, 1) void lm_gemm_kernel(LmArgs a) {
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int c = lane & 31, g = lane >> 5;
-  const int wa = wave >> 2, wt = wave & 3;
+  const int wa = wave / (NW / 2), wt = wave % (NW / 2);
 
   const int K = (MODE == kModeDh) ? a.Vp : a.H;
   const int a_rows = (MODE == kModeDh) ? a.H : a.V;
   const int nk = K / BKK;
+  // tiles wholly inside the operands skip the per-load bounds checks
+  const bool interior = (t0 + BT <= a.T) && (MODE == kModeDh ? (a0 + BA <= a.H) : (a0 + BA <= a_rows));
 
-  f32x16 acc[4][2];
+  f32x16 acc[4][NJ];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  uint4 ra[4], rb[4];
+  uint4 ra[LDA], rb[LDB];
   auto load = [&](int k0) {
     const uint4 z = make_uint4(0, 0, 0, 0);
-    if (MODE == kModeDh) {
-      // W slice [64 vocab rows][256 hidden], staged row-major; the A = W^T
-      // operand is read across its rows with the transposing LDS read
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int idx = tid + r * NTHR;
+    for (int r = 0; r < LDA; ++r) {
+      const int idx = tid + r * NT;
+      if (MODE == kModeDh) {
+        // W slice [64 vocab rows][256 hidden], staged row-major; the A = W^T
+        // operand is read across its rows with the transposing LDS read
         const int row = idx / (BA / 8), cc = (idx % (BA / 8)) * 8;
         const int v = k0 + row;
-        ra[r] = (v < a.V && a0 + cc < a.H) ? ld16(a.w + size_t(v) * a.H + a0 + cc) : z;
-      }
-    } else {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int idx = tid + r * NTHR;
+        const u16* p = a.w + size_t(v) * a.H + a0 + cc;
+        ra[r] = (interior && v < a.V) || (v < a.V && a0 + cc < a.H) ? ld16(p) : z;
+      } else {
         const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
         const int v = a0 + row;
-        ra[r] = v < a_rows ? ld16(a.w + size_t(v) * a.H + k0 + cc) : z;
+        const u16* p = a.w + size_t(v) * a.H + k0 + cc;
+        ra[r] = (interior || v < a_rows) ? ld16(p) : z;
       }
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int idx = tid + r * NTHR;
+    for (int r = 0; r < LDB; ++r) {
+      const int idx = tid + r * NT;
       const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
       const int t = t0 + row;
-      if (MODE == kModeDh)
-        rb[r] = t < a.T ? ld16(a.G + size_t(t) * a.Vp + k0 + cc) : z;
-      else
-        rb[r] = t < a.T ? ld16(a.h + size_t(t) * a.H + k0 + cc) : z;
+      const u16* p = (MODE == kModeDh) ? a.G + size_t(t) * a.Vp + k0 + cc
+                                       : a.h + size_t(t) * a.H + k0 + cc;
+      rb[r] = (interior || t < a.T) ? ld16(p) : z;
     }
   };
   auto store = [&](u16* sA) {
     u16* sB = sA + BA * PAD;
-    if (MODE == kModeDh) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int idx = tid + r * NTHR;
+    for (int r = 0; r < LDA; ++r) {
+      const int idx = tid + r * NT;
+      if (MODE == kModeDh) {
         const int row = idx / (BA / 8), cc = (idx % (BA / 8)) * 8;
         st16(&sA[row * WPAD + cc], ra[r]);
-      }
-    } else {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int idx = tid + r * NTHR;
+      } else {
         const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
         st16(&sA[row * PAD + cc], ra[r]);
       }
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int idx = tid + r * NTHR;
+    for (int r = 0; r < LDB; ++r) {
+      const int idx = tid + r * NT;
       const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
       st16(&sB[row * PAD + cc], rb[r]);
     }
@@ -158,19 +158,19 @@ __global__ __launch_bounds__(NTHR, 1) void lm_gemm_kernel(LmArgs a) {
     const u16* sB = sA + BA * PAD;
 #pragma unroll
     for (int ks = 0; ks < BKK / 16; ++ks) {
-      bf16x8 af[4], bf[2];
+      bf16x8 af[4], bf[NJ];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         af[i] = (MODE == kModeDh)
                     ? ld_operand_tr<WPAD, true>(sA, ks * 16, wa * 128 + i * 32)
                     : as_bf16x8(ld16(&sA[(wa * 128 + i * 32 + c) * PAD + ks * 16 + g * 8]));
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        bf[j] = as_bf16x8(ld16(&sB[(wt * 64 + j * 32 + c) * PAD + ks * 16 + g * 8]));
+      for (int j = 0; j < NJ; ++j)
+        bf[j] = as_bf16x8(ld16(&sB[(wt * WTOK + j * 32 + c) * PAD + ks * 16 + g * 8]));
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
+        for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
     }
     if (kk + 1 < nk) {
       store(smem + ((kk + 1) & 1) * STAGE);
@@ -180,12 +180,12 @@ __global__ __launch_bounds__(NTHR, 1) void lm_gemm_kernel(LmArgs a) {
   }
 
   // acc[i][j][r]: A-row a0 + wa*128 + i*32 + (r/4)*8 + g*4 + r%4,
-  //               token t0 + wt*64 + j*32 + c
+  //               token t0 + wt*WTOK + j*32 + c
   const int arow0 = a0 + wa * 128;
   if (MODE == kModeLogits) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int t = t0 + wt * 64 + j * 32 + c;
+    for (int j = 0; j < NJ; ++j) {
+      const int t = t0 + wt * WTOK + j * 32 + c;
       const int y = t < a.T ? a.tgt[t] : -1;
       float mx = -INFINITY;
 #pragma unroll
@@ -211,8 +211,8 @@ __global__ __launch_bounds__(NTHR, 1) void lm_gemm_kernel(LmArgs a) {
     }
   } else if (MODE == kModeGrad) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int t = t0 + wt * 64 + j * 32 + c;
+    for (int j = 0; j < NJ; ++j) {
+      const int t = t0 + wt * WTOK + j * 32 + c;
       if (t >= a.T) continue;
       const int y = a.tgt[t];
       const float gt = y >= 0 ? a.g[t] : 0.f;
@@ -237,8 +237,8 @@ __global__ __launch_bounds__(NTHR, 1) void lm_gemm_kernel(LmArgs a) {
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int t = t0 + wt * 64 + j * 32 + c;
+    for (int j = 0; j < NJ; ++j) {
+      const int t = t0 + wt * WTOK + j * 32 + c;
       if (t >= a.T) continue;
       u16* out = a.dh + size_t(t) * a.H;
 #pragma unroll
@@ -327,7 +327,8 @@ hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, c
   a.nT = (T + BT - 1) / BT;
   {
     ProfScope p("lm_logits", stream);
-    hipLaunchKernelGGL(lm_gemm_kernel<kModeLogits>, gemm_grid(a), dim3(NTHR), 0, stream, a);
+    hipLaunchKernelGGL((lm_gemm_kernel<kModeLogits, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
+                       stream, a);
   }
   {
     ProfScope p("lm_combine", stream);
@@ -358,12 +359,14 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
   a.nT = (T + BT - 1) / BT;
   {
     ProfScope p("lm_grad", stream);
-    hipLaunchKernelGGL(lm_gemm_kernel<kModeGrad>, gemm_grid(a), dim3(NTHR), 0, stream, a);
+    hipLaunchKernelGGL((lm_gemm_kernel<kModeGrad, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
+                       stream, a);
   }
   a.nA = (H + BA - 1) / BA;
   {
     ProfScope p("lm_dh", stream);
-    hipLaunchKernelGGL(lm_gemm_kernel<kModeDh>, gemm_grid(a), dim3(NTHR), 0, stream, a);
+    hipLaunchKernelGGL((lm_gemm_kernel<kModeDh, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
+                       stream, a);
   }
   return hipGetLastError();
 }
