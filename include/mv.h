@@ -105,7 +105,17 @@ typedef struct {
   int32_t tiles_skipped;         /* causal tiles holding no visible pair              */
   int32_t bwd_items;             /* key-tile work items of the dK/dV pass             */
   int32_t bwd_partial_slots;     /* fp32 partial tiles the dK/dV pass reduces         */
+  int32_t n_leaves;              /* diverging leaves (see mv_view_mask_leaves)        */
 } mv_mask_stats;
+
+/* Which conditioning a mask encodes. */
+enum {
+  MV_VIEW_LIVE = 0,   /* the live view of every row (Eq. "live-view"): the exact walk */
+  MV_VIEW_FINAL = 1   /* the final compressed walk (Eq. "live-vs-final"): every edit
+                         applied to every row; an evicted key is seen by its own row
+                         only.  This is the student conditioning of SDCC (Section 5.1)
+                         and the Naive-Compressed baseline (Section 3.3, Pitfall A). */
+};
 
 /*
  * Build the key-lifetime array omega (Eq. "4d-mask-def") and the block-sparse
@@ -118,6 +128,25 @@ typedef struct {
  */
 mv_status mv_build_view_mask(const mv_trajectory* trajs, int32_t n_traj,
                              int32_t total_tokens, mv_view_mask** out);
+
+/* As mv_build_view_mask, for kind MV_VIEW_LIVE or MV_VIEW_FINAL. */
+mv_status mv_build_view_mask_kind(const mv_trajectory* trajs, int32_t n_traj,
+                                  int32_t total_tokens, int32_t kind, mv_view_mask** out);
+
+/*
+ * The diverging leaves of the record (Definition "trajectory tree", Appendix
+ * B.1; the set C of Section 5.1), in position order: tokens t that survive
+ * every edit and whose live view differs from their final-walk prefix, i.e.
+ * some key before t is evicted by an edit firing at row t or later.  For each:
+ * tokens[i] = t; teacher_rows[i] = t - 1 (the row that predicted t under its
+ * live view); student_rows[i] = the last surviving row before t (the row that
+ * predicts t on the final compressed walk).  For the running example of
+ * Section 3.2 these are y6, y7, y9, y10, y12 (Table "running-prefixes").
+ * Host arrays of `capacity` entries; *n_out receives the count.  Passing
+ * capacity 0 and null arrays only queries the count.
+ */
+mv_status mv_view_mask_leaves(const mv_view_mask* m, int32_t* tokens, int32_t* teacher_rows,
+                              int32_t* student_rows, int32_t capacity, int32_t* n_out);
 
 /* Bytes of device memory the uploaded mask needs. */
 size_t mv_view_mask_device_bytes(const mv_view_mask* m);
@@ -248,6 +277,59 @@ mv_status mv_ppo_clip_dlogp(int32_t n, const float* ratio, const float* adv,
                             float* dlogp, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * SDCC junction KL (Section 5.1, Eq. "soft_loss"; forward KL, teacher first).
+ *
+ * At each diverging leaf p the teacher distribution p = softmax(W h_T[p]) (the
+ * policy under the live prefix, stop-gradient) and the student distribution
+ * q = softmax(W h_S[p]) (under the final-walk prefix) give
+ *     KL_p = sum_v p_v (log p_v - log q_v),
+ * computed by streaming vocabulary tiles through the same MFMA engine as the
+ * log-prob, never storing logits.  Teacher and student hidden rows are read in
+ * place through row indices (e.g. teacher_rows / student_rows of
+ * mv_view_mask_leaves applied to the hidden states of a live-view and a
+ * final-walk pass).  Layouts: hidden_* bf16 [n_rows_*, hidden]; rows int32
+ * [n_leaves] (device); weight bf16 [vocab, hidden]; per-leaf fp32 [n_leaves].
+ * A row index outside [0, n_rows_*) is read as an all-zero hidden state (the
+ * kernels never read outside the matrices).  hidden % 64 == 0; n_leaves == 0
+ * is a no-op.  The workspace (device, >= *_workspace_bytes, caller-owned) holds
+ * per-leaf vocabulary-chunk partials (forward) or the bf16 rows dkl * (q - p)
+ * (backward).
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t n_leaves, hidden, vocab;
+  int32_t n_rows_teacher, n_rows_student;  /* rows of the two hidden matrices */
+} mv_kl_shape;
+
+size_t mv_sdcc_kl_workspace_bytes(const mv_kl_shape* shape);
+
+mv_status mv_sdcc_kl(const mv_kl_shape* shape, const void* hidden_teacher,
+                     const int32_t* teacher_rows, const void* hidden_student,
+                     const int32_t* student_rows, const void* weight, float* kl,
+                     float* lse_teacher, float* lse_student, void* workspace,
+                     size_t workspace_bytes, hipStream_t stream);
+
+size_t mv_sdcc_kl_bwd_workspace_bytes(const mv_kl_shape* shape);
+
+/*
+ * dh_student[p] = dkl[p] * (q - p)^T W  (bf16 [n_leaves, hidden]), the gradient
+ * of sum_p dkl[p] KL_p into the student hidden state of each leaf (the teacher
+ * is stop-gradient).  Logits are recomputed from the forward's LSEs.
+ */
+mv_status mv_sdcc_kl_bwd(const mv_kl_shape* shape, const void* hidden_teacher,
+                         const int32_t* teacher_rows, const void* hidden_student,
+                         const int32_t* student_rows, const void* weight,
+                         const float* lse_teacher, const float* lse_student, const float* dkl,
+                         void* dh_student, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream);
+
+/*
+ * The KL weight schedule of the training recipe (Appendix F): lambda ramps
+ * linearly from 0 to lambda_max over the first warmup_frac of total_steps and
+ * stays there.  Host only.
+ */
+float mv_sdcc_lambda(int32_t step, int32_t total_steps, float lambda_max, float warmup_frac);
+
+/* ---------------------------------------------------------------------------
  * Kernel timing (measurement support, not part of the method).
  *
  * While enabled, every kernel the library enqueues is bracketed by a pair of
@@ -255,8 +337,9 @@ mv_status mv_ppo_clip_dlogp(int32_t n, const float* ratio, const float* adv,
  * previous records; mv_profile_read waits for the recorded events and returns
  * the summed duration (ms) and launch count of the kernels named `kernel`
  * (one of "attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce",
- * "attn_bwd_dq", "lm_logits", "lm_combine", "lm_grad", "lm_dh",
- * "materialize", "ppo_clip").  Not for use under stream capture.
+ * "attn_bwd_dq", "lm_logits", "lm_combine", "lm_grad", "lm_dh", "kl_logits",
+ * "kl_combine", "kl_grad", "kl_dh", "materialize", "ppo_clip").  Not for use
+ * under stream capture.
  * ------------------------------------------------------------------------ */
 mv_status mv_profile_enable(int32_t on);
 mv_status mv_profile_read(const char* kernel, double* total_ms, int32_t* count);

@@ -75,6 +75,15 @@ hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, c
 hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const void* weight,
                               const int32_t* target, const float* lse, const float* dlogp,
                               void* dhidden, void* ws, hipStream_t stream);
+size_t kl_fwd_ws_bytes(int n, int H, int V);
+size_t kl_bwd_ws_bytes(int n, int H, int V);
+hipError_t launch_kl_fwd(int n, int H, int V, const void* hT, int nT, const int32_t* rowsT,
+                         const void* hS, int nS, const int32_t* rowsS, const void* weight,
+                         float* kl, float* lseT, float* lseS, void* ws, hipStream_t stream);
+hipError_t launch_kl_bwd(int n, int H, int V, const void* hT, int nT, const int32_t* rowsT,
+                         const void* hS, int nS, const int32_t* rowsS, const void* weight,
+                         const float* lseT, const float* lseS, const float* dkl, void* dh,
+                         void* ws, hipStream_t stream);
 
 }  // namespace mv
 
@@ -137,6 +146,17 @@ mv_status check_logprob(const mv_logprob_shape* s) {
     return fail(MV_ERR_UNSUPPORTED, "hidden/weight larger than 2^31 elements");
   if (!(s->eps_low >= 0.f && s->eps_low < 1.f && s->eps_high >= 0.f && std::isfinite(s->eps_high)))
     return fail(MV_ERR_INVALID_ARG, "clip range must satisfy 0 <= eps_low < 1, 0 <= eps_high");
+  return MV_OK;
+}
+
+mv_status check_kl(const mv_kl_shape* s) {
+  if (s == nullptr) return fail(MV_ERR_INVALID_ARG, "null shape");
+  if (s->n_leaves < 0 || s->hidden <= 0 || s->vocab <= 0 || s->n_rows_teacher < 0 ||
+      s->n_rows_student < 0)
+    return fail(MV_ERR_SHAPE, "n_leaves >= 0, hidden > 0, vocab > 0, row counts >= 0 required");
+  if (s->hidden % 64 != 0) return fail(MV_ERR_UNSUPPORTED, "hidden must be a multiple of 64");
+  if (int64_t(s->vocab) * s->hidden >= (int64_t(1) << 31) || s->n_leaves > (1 << 29))
+    return fail(MV_ERR_UNSUPPORTED, "operands larger than 2^31 elements");
   return MV_OK;
 }
 
@@ -255,6 +275,62 @@ mv_status mv_token_logprob_bwd(const mv_logprob_shape* s, const void* hidden, co
   return hip_status(mv::launch_logprob_bwd(s->n_tokens, s->hidden, s->vocab, hidden, weight,
                                            target, lse, dlogp, dhidden, ws, stream),
                     "log-prob backward launch");
+}
+
+size_t mv_sdcc_kl_workspace_bytes(const mv_kl_shape* s) {
+  if (check_kl(s) != MV_OK) return 0;
+  return mv::kl_fwd_ws_bytes(s->n_leaves, s->hidden, s->vocab);
+}
+
+size_t mv_sdcc_kl_bwd_workspace_bytes(const mv_kl_shape* s) {
+  if (check_kl(s) != MV_OK) return 0;
+  return mv::kl_bwd_ws_bytes(s->n_leaves, s->hidden, s->vocab);
+}
+
+mv_status mv_sdcc_kl(const mv_kl_shape* s, const void* hT, const int32_t* rowsT, const void* hS,
+                     const int32_t* rowsS, const void* weight, float* kl, float* lseT, float* lseS,
+                     void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (mv_status st = check_kl(s); st != MV_OK) return st;
+  if (s->n_leaves == 0) return MV_OK;
+  if (mv_status st = check_ptrs({hT, hS, weight, ws}); st != MV_OK) return st;
+  if (rowsT == nullptr || rowsS == nullptr || kl == nullptr || lseT == nullptr || lseS == nullptr)
+    return fail(MV_ERR_INVALID_ARG, "row indices and per-leaf outputs are required");
+  const size_t need = mv::kl_fwd_ws_bytes(s->n_leaves, s->hidden, s->vocab);
+  if (ws_bytes < need) {
+    std::ostringstream os;
+    os << "KL workspace has " << ws_bytes << " bytes, needs " << need;
+    return fail(MV_ERR_WORKSPACE, os.str());
+  }
+  return hip_status(mv::launch_kl_fwd(s->n_leaves, s->hidden, s->vocab, hT, s->n_rows_teacher,
+                                      rowsT, hS, s->n_rows_student, rowsS, weight, kl, lseT, lseS, ws, stream),
+                    "KL forward launch");
+}
+
+mv_status mv_sdcc_kl_bwd(const mv_kl_shape* s, const void* hT, const int32_t* rowsT,
+                         const void* hS, const int32_t* rowsS, const void* weight,
+                         const float* lseT, const float* lseS, const float* dkl, void* dh,
+                         void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (mv_status st = check_kl(s); st != MV_OK) return st;
+  if (s->n_leaves == 0) return MV_OK;
+  if (mv_status st = check_ptrs({hT, hS, weight, dh, ws}); st != MV_OK) return st;
+  if (rowsT == nullptr || rowsS == nullptr || lseT == nullptr || lseS == nullptr || dkl == nullptr)
+    return fail(MV_ERR_INVALID_ARG, "row indices, LSEs and dkl are required");
+  const size_t need = mv::kl_bwd_ws_bytes(s->n_leaves, s->hidden, s->vocab);
+  if (ws_bytes < need) {
+    std::ostringstream os;
+    os << "KL backward workspace has " << ws_bytes << " bytes, needs " << need;
+    return fail(MV_ERR_WORKSPACE, os.str());
+  }
+  return hip_status(mv::launch_kl_bwd(s->n_leaves, s->hidden, s->vocab, hT, s->n_rows_teacher,
+                                      rowsT, hS, s->n_rows_student, rowsS, weight, lseT, lseS, dkl, dh, ws, stream),
+                    "KL backward launch");
+}
+
+float mv_sdcc_lambda(int32_t step, int32_t total_steps, float lambda_max, float warmup_frac) {
+  const double warm = double(warmup_frac) * double(total_steps);
+  if (warm <= 0.0 || step >= warm) return lambda_max;
+  if (step <= 0) return 0.f;
+  return float(double(lambda_max) * double(step) / warm);
 }
 
 mv_status mv_profile_enable(int32_t on) {

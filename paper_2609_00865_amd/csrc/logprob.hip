@@ -39,7 +39,7 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int vocab_pad(int V) { return (V + BA - 1) / BA * BA; }
 }  // namespace
 
-enum { kModeLogits = 0, kModeGrad = 1, kModeDh = 2 };
+enum { kModeLogits = 0, kModeGrad = 1, kModeDh = 2, kModeKL = 3, kModeKLGrad = 4 };
 
 struct LmArgs {
   const u16* h;       // [T, H]
@@ -52,6 +52,17 @@ struct LmArgs {
   u16* dh;            // [T, H] (dH mode)
   float2* part;       // [T, n_chunks] (logits mode)
   float* tlogit;      // [T] (logits mode)
+  // KL modes: token row 2i is leaf i's teacher row, 2i + 1 its student row
+  const u16* hT;      // teacher hidden states [*, H]
+  const u16* hS;      // student hidden states [*, H]
+  const int32_t* rowsT;
+  const int32_t* rowsS;
+  float4* partT;      // [n, n_chunks] (max, sum, cross, -) of the teacher
+  float2* partS;      // [n, n_chunks] (max, sum) of the student
+  const float* lseT;  // [n] (KL grad mode)
+  const float* lseS;
+  const float* dkl;   // [n] upstream gradient of each leaf's KL
+  int n_leaves, n_rows_T, n_rows_S;
   int T, H, V, Vp, n_chunks;
   int nA, nT;         // tiles along the A side and along tokens
 };
@@ -98,6 +109,28 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // each thread's token rows are fixed across k slices: resolve them once
+  const u16* brow[LDB];
+  bool bok[LDB];
+#pragma unroll
+  for (int r = 0; r < LDB; ++r) {
+    const int t = t0 + (tid + r * NT) / (BKK / 8);
+    bok[r] = interior || t < a.T;
+    const int tc = bok[r] ? t : 0;
+    if (MODE == kModeDh) {
+      brow[r] = a.G + size_t(tc) * a.Vp;
+    } else if (MODE == kModeKL || MODE == kModeKLGrad) {
+      // a row index outside its matrix reads as a zero hidden state
+      const int row = (tc & 1) ? a.rowsS[tc >> 1] : a.rowsT[tc >> 1];
+      const int n_rows = (tc & 1) ? a.n_rows_S : a.n_rows_T;
+      const bool row_ok = row >= 0 && row < n_rows;
+      bok[r] = bok[r] && row_ok;
+      brow[r] = ((tc & 1) ? a.hS : a.hT) + size_t(row_ok ? row : 0) * a.H;
+    } else {
+      brow[r] = a.h + size_t(tc) * a.H;
+    }
+  }
+
   uint4 ra[LDA], rb[LDB];
   auto load = [&](int k0) {
     const uint4 z = make_uint4(0, 0, 0, 0);
@@ -120,12 +153,8 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
     }
 #pragma unroll
     for (int r = 0; r < LDB; ++r) {
-      const int idx = tid + r * NT;
-      const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
-      const int t = t0 + row;
-      const u16* p = (MODE == kModeDh) ? a.G + size_t(t) * a.Vp + k0 + cc
-                                       : a.h + size_t(t) * a.H + k0 + cc;
-      rb[r] = (interior || t < a.T) ? ld16(p) : z;
+      const int cc = ((tid + r * NT) % (BKK / 8)) * 8;
+      rb[r] = bok[r] ? ld16(brow[r] + k0 + cc) : z;
     }
   };
   auto store = [&](u16* sA) {
@@ -235,6 +264,78 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
           *reinterpret_cast<uint2*>(out + arow0 + i * 32 + q4 * 8 + g * 4) = wv;
         }
     }
+  } else if (MODE == kModeKL) {
+    // lanes c (even, teacher) and c + 1 (student) hold the same vocabulary
+    // rows of one leaf; each lane keeps its own (max, sum of exp) and the
+    // teacher also accumulates sum exp(zT - mT) * (zT - zS)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int t = t0 + wt * WTOK + j * 32 + c;
+      const int leaf = t >> 1;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = arow0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+          if (v < a.V) mx = fmaxf(mx, acc[i][j][r] * kLog2e);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mu = mx == -INFINITY ? 0.f : mx;
+      float sm = 0.f, cross = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = arow0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+          const float z = acc[i][j][r];
+          const float zo = __shfl_xor(z, 1);  // the partner row's logit
+          const float e = v < a.V ? fast_exp2(z * kLog2e - mu) : 0.f;
+          sm += e;
+          cross += e * (z - zo);
+        }
+      sm += __shfl_xor(sm, 32);
+      cross += __shfl_xor(cross, 32);
+      if (g == 0 && leaf < a.n_leaves) {
+        const size_t o = size_t(leaf) * a.n_chunks + arow0 / 128;
+        if (t & 1)
+          a.partS[o] = make_float2(mx, sm);
+        else
+          a.partT[o] = make_float4(mx, sm, cross, 0.f);
+      }
+    }
+  } else if (MODE == kModeKLGrad) {
+    // student lanes write G = dkl * (q - p) for their leaf
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int t = t0 + wt * WTOK + j * 32 + c;
+      const int leaf = t >> 1;
+      const bool student = (t & 1) && leaf < a.n_leaves;
+      const int lc = leaf < a.n_leaves ? leaf : 0;
+      const float gl = a.dkl[lc];
+      const float lS = a.lseS[lc] * kLog2e, lT = a.lseT[lc] * kLog2e;
+      u16* out = a.Gout + size_t(lc) * a.Vp;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          float vals[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int v = arow0 + i * 32 + q4 * 8 + g * 4 + u;
+            const float zS = acc[i][j][q4 * 4 + u];
+            const float zT = __shfl_xor(zS, 1);
+            const float q = fast_exp2(zS * kLog2e - lS), pt = fast_exp2(zT * kLog2e - lT);
+            vals[u] = v < a.V ? gl * (q - pt) : 0.f;
+          }
+          if (student) {
+            uint2 wv;
+            wv.x = pack2(vals[0], vals[1]);
+            wv.y = pack2(vals[2], vals[3]);
+            *reinterpret_cast<uint2*>(out + arow0 + i * 32 + q4 * 8 + g * 4) = wv;
+          }
+        }
+    }
   } else {
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
@@ -284,6 +385,59 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(LmArgs a, const float* 
     ratio[t] = r;
     clipped[t] = fminf(fmaxf(r, 1.f - eps_lo), 1.f + eps_hi);
   }
+}
+
+// Merge one leaf's per-chunk teacher and student partials into both LSEs and
+// KL(p || q) = sum_v p_v (zT_v - zS_v) - lseT + lseS.
+__global__ __launch_bounds__(256) void kl_combine_kernel(LmArgs a, float* kl, float* lseT,
+                                                         float* lseS) {
+  const int leaf = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (leaf >= a.n_leaves) return;
+  const float4* pt = a.partT + size_t(leaf) * a.n_chunks;
+  const float2* ps = a.partS + size_t(leaf) * a.n_chunks;
+  float mt = -INFINITY, ms = -INFINITY;
+  for (int i = lane; i < a.n_chunks; i += 64) {
+    mt = fmaxf(mt, pt[i].x);
+    ms = fmaxf(ms, ps[i].x);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    mt = fmaxf(mt, __shfl_xor(mt, off));
+    ms = fmaxf(ms, __shfl_xor(ms, off));
+  }
+  float st = 0.f, cr = 0.f, ss = 0.f;
+  for (int i = lane; i < a.n_chunks; i += 64) {
+    const float wt = fast_exp2(pt[i].x - mt);
+    st += pt[i].y * wt;
+    cr += pt[i].z * wt;
+    ss += ps[i].y * fast_exp2(ps[i].x - ms);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    st += __shfl_xor(st, off);
+    cr += __shfl_xor(cr, off);
+    ss += __shfl_xor(ss, off);
+  }
+  if (lane != 0) return;
+  const float l2t = __log2f(st), l2s = __log2f(ss);
+  lseT[leaf] = (mt + l2t) * kLn2;
+  lseS[leaf] = (ms + l2s) * kLn2;
+  // lseS - lseT from the differences of its parts: no cancellation between
+  // two terms of size log V, and exactly zero when both sides agree
+  kl[leaf] = cr / st + ((ms - mt) + (l2s - l2t)) * kLn2;
+}
+
+size_t kl_fwd_ws_bytes(int n, int H, int V) {
+  (void)H;
+  const int n_chunks = vocab_pad(V) / 128;
+  return align256(size_t(n) * n_chunks * sizeof(float4)) +
+         align256(size_t(n) * n_chunks * sizeof(float2)) + 256;
+}
+
+size_t kl_bwd_ws_bytes(int n, int H, int V) {
+  (void)H;
+  return align256(size_t(n) * vocab_pad(V) * sizeof(u16)) + 256;
 }
 
 size_t logprob_fwd_ws_bytes(int T, int H, int V) {
@@ -367,6 +521,89 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
     ProfScope p("lm_dh", stream);
     hipLaunchKernelGGL((lm_gemm_kernel<kModeDh, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
                        stream, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_kl_fwd(int n, int H, int V, const void* hT, int nT, const int32_t* rowsT,
+                         const void* hS, int nS, const int32_t* rowsS, const void* weight,
+                         float* kl, float* lseT, float* lseS, void* ws, hipStream_t stream) {
+  LmArgs a{};
+  a.n_rows_T = nT;
+  a.n_rows_S = nS;
+  a.w = static_cast<const u16*>(weight);
+  a.hT = static_cast<const u16*>(hT);
+  a.hS = static_cast<const u16*>(hS);
+  a.rowsT = rowsT;
+  a.rowsS = rowsS;
+  a.n_leaves = n;
+  a.T = 2 * n;
+  a.H = H;
+  a.V = V;
+  a.Vp = vocab_pad(V);
+  a.n_chunks = a.Vp / 128;
+  char* base = align_ptr(ws);
+  a.partT = reinterpret_cast<float4*>(base);
+  a.partS = reinterpret_cast<float2*>(base + align256(size_t(n) * a.n_chunks * sizeof(float4)));
+  a.nA = a.Vp / BA;
+  a.nT = (a.T + BT - 1) / BT;
+  {
+    ProfScope p("kl_logits", stream);
+    hipLaunchKernelGGL((lm_gemm_kernel<kModeKL, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
+                       stream, a);
+  }
+  {
+    ProfScope p("kl_combine", stream);
+    hipLaunchKernelGGL(kl_combine_kernel, dim3((n + 3) / 4), dim3(256), 0, stream, a, kl, lseT,
+                       lseS);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_kl_bwd(int n, int H, int V, const void* hT, int nT, const int32_t* rowsT,
+                         const void* hS, int nS, const int32_t* rowsS, const void* weight,
+                         const float* lseT, const float* lseS, const float* dkl, void* dh,
+                         void* ws, hipStream_t stream) {
+  LmArgs a{};
+  a.n_rows_T = nT;
+  a.n_rows_S = nS;
+  a.w = static_cast<const u16*>(weight);
+  a.hT = static_cast<const u16*>(hT);
+  a.hS = static_cast<const u16*>(hS);
+  a.rowsT = rowsT;
+  a.rowsS = rowsS;
+  a.lseT = lseT;
+  a.lseS = lseS;
+  a.dkl = dkl;
+  a.n_leaves = n;
+  a.T = 2 * n;
+  a.H = H;
+  a.V = V;
+  a.Vp = vocab_pad(V);
+  u16* G = reinterpret_cast<u16*>(align_ptr(ws));
+  a.Gout = G;
+  a.nA = a.Vp / BA;
+  a.nT = (a.T + BT - 1) / BT;
+  {
+    ProfScope p("kl_grad", stream);
+    hipLaunchKernelGGL((lm_gemm_kernel<kModeKLGrad, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
+                       stream, a);
+  }
+  // dh = G W over the leaves
+  LmArgs b{};
+  b.w = a.w;
+  b.G = G;
+  b.dh = static_cast<u16*>(dh);
+  b.T = n;
+  b.H = H;
+  b.V = V;
+  b.Vp = a.Vp;
+  b.nA = (H + BA - 1) / BA;
+  b.nT = (n + BT - 1) / BT;
+  {
+    ProfScope p("kl_dh", stream);
+    hipLaunchKernelGGL((lm_gemm_kernel<kModeDh, NWAVES>), gemm_grid(b), dim3(NWAVES * 64), 0,
+                       stream, b);
   }
   return hipGetLastError();
 }

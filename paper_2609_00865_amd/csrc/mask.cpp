@@ -83,6 +83,35 @@ mv_status validate_and_fill_omega(const mv_trajectory* trajs, int32_t n_traj, in
   return MV_OK;
 }
 
+// Diverging leaves (Definition "trajectory tree", Appendix B.1; Section 5.1):
+// a token t that survives every edit is scored under the live view of row t-1
+// and, on the final compressed walk, under the row of the last surviving
+// token before t.  The two conditioning sets differ iff some key before t is
+// evicted by an edit that fires at row t or later, i.e. iff the largest
+// death row among evicted keys j < t is >= t.  Computed from the live omega.
+void build_leaves(mv_view_mask& m, const mv_trajectory* trajs, int32_t n_traj) {
+  m.leaf_token.clear();
+  m.leaf_teacher.clear();
+  m.leaf_student.clear();
+  for (int32_t k = 0; k < n_traj; ++k) {
+    const int32_t b = trajs[k].begin, e = trajs[k].end;
+    int32_t latest_death = -1, last_survivor = -1;
+    for (int32_t t = b + 1; t < e; ++t) {
+      const int32_t j = t - 1;
+      if (m.omega[j] < e)
+        latest_death = std::max(latest_death, m.omega[j]);
+      else
+        last_survivor = j;
+      if (m.omega[t] == e && latest_death >= t && last_survivor >= 0) {
+        m.leaf_token.push_back(t);
+        m.leaf_teacher.push_back(t - 1);
+        m.leaf_student.push_back(last_survivor);
+      }
+    }
+  }
+  m.stats.n_leaves = int32_t(m.leaf_token.size());
+}
+
 void build_stats(mv_view_mask& m) {
   const int32_t T = m.T;
   int64_t pairs = 0;
@@ -215,20 +244,31 @@ void layout_device(mv_view_mask& m) {
 
 extern "C" {
 
-mv_status mv_build_view_mask(const mv_trajectory* trajs, int32_t n_traj, int32_t total_tokens,
-                             mv_view_mask** out) {
+mv_status mv_build_view_mask_kind(const mv_trajectory* trajs, int32_t n_traj,
+                                  int32_t total_tokens, int32_t kind, mv_view_mask** out) {
   if (out == nullptr) return bad(MV_ERR_INVALID_ARG, "out is null");
   *out = nullptr;
   if (trajs == nullptr || n_traj <= 0) return bad(MV_ERR_INVALID_ARG, "no trajectories");
   if (total_tokens <= 0 || total_tokens > (1 << 30))
     return bad(MV_ERR_INVALID_ARG, "total_tokens must be in [1, 2^30]");
+  if (kind != MV_VIEW_LIVE && kind != MV_VIEW_FINAL)
+    return bad(MV_ERR_INVALID_ARG, "kind must be MV_VIEW_LIVE or MV_VIEW_FINAL");
   try {
     auto* m = new mv_view_mask();
     m->T = total_tokens;
+    m->kind = kind;
     mv_status s = validate_and_fill_omega(trajs, n_traj, total_tokens, m->omega);
     if (s != MV_OK) {
       delete m;
       return s;
+    }
+    build_leaves(*m, trajs, n_traj);
+    if (kind == MV_VIEW_FINAL) {
+      // the final compressed walk applies every edit: an evicted key is seen
+      // by its own row only
+      for (int32_t t = 0; t < n_traj; ++t)
+        for (int32_t j = trajs[t].begin; j < trajs[t].end; ++j)
+          if (m->omega[j] < trajs[t].end) m->omega[j] = j + 1;
     }
     build_stats(*m);
     build_fwd_schedule(*m);
@@ -239,6 +279,31 @@ mv_status mv_build_view_mask(const mv_trajectory* trajs, int32_t n_traj, int32_t
   } catch (const std::exception& e) {
     return bad(MV_ERR_INVALID_ARG, std::string("host allocation failed: ") + e.what());
   }
+}
+
+mv_status mv_build_view_mask(const mv_trajectory* trajs, int32_t n_traj, int32_t total_tokens,
+                             mv_view_mask** out) {
+  return mv_build_view_mask_kind(trajs, n_traj, total_tokens, MV_VIEW_LIVE, out);
+}
+
+mv_status mv_view_mask_leaves(const mv_view_mask* m, int32_t* tokens, int32_t* teacher_rows,
+                              int32_t* student_rows, int32_t capacity, int32_t* n_out) {
+  if (m == nullptr || n_out == nullptr) return bad(MV_ERR_INVALID_ARG, "null argument");
+  const int32_t n = int32_t(m->leaf_token.size());
+  *n_out = n;
+  if (capacity < n) {
+    if (tokens == nullptr && teacher_rows == nullptr && student_rows == nullptr && capacity == 0)
+      return MV_OK;  // size query
+    return bad(MV_ERR_WORKSPACE, "leaf arrays smaller than the number of diverging leaves");
+  }
+  if (n > 0 && (tokens == nullptr || teacher_rows == nullptr || student_rows == nullptr))
+    return bad(MV_ERR_INVALID_ARG, "null leaf array");
+  for (int32_t i = 0; i < n; ++i) {
+    tokens[i] = m->leaf_token[i];
+    teacher_rows[i] = m->leaf_teacher[i];
+    student_rows[i] = m->leaf_student[i];
+  }
+  return MV_OK;
 }
 
 size_t mv_view_mask_device_bytes(const mv_view_mask* m) { return m ? m->bytes : 0; }

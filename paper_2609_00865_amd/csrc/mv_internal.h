@@ -60,6 +60,8 @@ struct mv_view_mask {
   std::vector<int32_t> omega, kt_minmax, q_ptr, k_list, qt_order;
   std::vector<int32_t> bwd_items, bwd_tiles, bwd_red;
   int32_t n_slots = 0;
+  int32_t kind = MV_VIEW_LIVE;
+  std::vector<int32_t> leaf_token, leaf_teacher, leaf_student;  // diverging leaves
   mv_mask_stats stats{};
   // device copy
   size_t off[8] = {0};

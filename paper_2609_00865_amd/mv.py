@@ -54,7 +54,7 @@ class MaskStats(ctypes.Structure):
                 ("max_view", ctypes.c_int32), ("n_segments", ctypes.c_int32),
                 ("tiles_full", ctypes.c_int32), ("tiles_partial", ctypes.c_int32),
                 ("tiles_skipped", ctypes.c_int32), ("bwd_items", ctypes.c_int32),
-                ("bwd_partial_slots", ctypes.c_int32)]
+                ("bwd_partial_slots", ctypes.c_int32), ("n_leaves", ctypes.c_int32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -70,6 +70,12 @@ class LogprobShape(ctypes.Structure):
     _fields_ = [("n_tokens", ctypes.c_int32), ("hidden", ctypes.c_int32),
                 ("vocab", ctypes.c_int32), ("eps_low", ctypes.c_float),
                 ("eps_high", ctypes.c_float)]
+
+
+class KLShape(ctypes.Structure):
+    _fields_ = [("n_leaves", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("n_rows_teacher", ctypes.c_int32),
+                ("n_rows_student", ctypes.c_int32)]
 
 
 _vp, _sz, _i32, _f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_float
@@ -88,6 +94,10 @@ mv_last_error = _sig("mv_last_error", ctypes.c_char_p)
 mv_version = _sig("mv_version", _i32)
 mv_build_view_mask = _sig("mv_build_view_mask", ctypes.c_int, _P(TrajectoryC), _i32, _i32,
                           _P(_vp))
+mv_build_view_mask_kind = _sig("mv_build_view_mask_kind", ctypes.c_int, _P(TrajectoryC), _i32,
+                               _i32, _i32, _P(_vp))
+mv_view_mask_leaves = _sig("mv_view_mask_leaves", ctypes.c_int, _vp, _vp, _vp, _vp, _i32,
+                           _P(_i32))
 mv_view_mask_device_bytes = _sig("mv_view_mask_device_bytes", _sz, _vp)
 mv_view_mask_upload = _sig("mv_view_mask_upload", ctypes.c_int, _vp, _vp, _sz, _vp)
 mv_view_mask_stats = _sig("mv_view_mask_stats", ctypes.c_int, _vp, _P(MaskStats))
@@ -112,6 +122,13 @@ mv_token_logprob_bwd = _sig("mv_token_logprob_bwd", ctypes.c_int, _P(LogprobShap
                             _vp, _vp, _vp, _vp, _vp, _sz, _vp)
 mv_ppo_clip_dlogp = _sig("mv_ppo_clip_dlogp", ctypes.c_int, _i32, _vp, _vp, _f32, _f32, _f32,
                          _vp, _vp)
+mv_sdcc_kl_workspace_bytes = _sig("mv_sdcc_kl_workspace_bytes", _sz, _P(KLShape))
+mv_sdcc_kl = _sig("mv_sdcc_kl", ctypes.c_int, _P(KLShape), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                  _vp, _sz, _vp)
+mv_sdcc_kl_bwd_workspace_bytes = _sig("mv_sdcc_kl_bwd_workspace_bytes", _sz, _P(KLShape))
+mv_sdcc_kl_bwd = _sig("mv_sdcc_kl_bwd", ctypes.c_int, _P(KLShape), _vp, _vp, _vp, _vp, _vp, _vp,
+                      _vp, _vp, _vp, _vp, _sz, _vp)
+mv_sdcc_lambda = _sig("mv_sdcc_lambda", _f32, _i32, _i32, _f32, _f32)
 
 mv_profile_enable = _sig("mv_profile_enable", ctypes.c_int, _i32)
 mv_profile_read = _sig("mv_profile_read", ctypes.c_int, ctypes.c_char_p, _P(ctypes.c_double),
@@ -123,7 +140,11 @@ EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_ma
             "mv_view_mask_free", "mv_attn_fwd", "mv_attn_bwd_workspace_bytes", "mv_attn_bwd",
             "mv_token_logprob_workspace_bytes", "mv_token_logprob",
             "mv_token_logprob_bwd_workspace_bytes", "mv_token_logprob_bwd", "mv_ppo_clip_dlogp",
+            "mv_build_view_mask_kind", "mv_view_mask_leaves", "mv_sdcc_kl_workspace_bytes",
+            "mv_sdcc_kl", "mv_sdcc_kl_bwd_workspace_bytes", "mv_sdcc_kl_bwd", "mv_sdcc_lambda",
             "mv_profile_enable", "mv_profile_read"]
+
+VIEW_LIVE, VIEW_FINAL = 0, 1
 
 
 def check(status: int) -> None:
@@ -154,7 +175,8 @@ def _aligned_buffer(nbytes: int, device) -> tuple:
 class ViewMask:
     """Owns a libmv mask object built from trajectories (host), optionally uploaded."""
 
-    def __init__(self, trajectories: Sequence, total_tokens: Optional[int] = None):
+    def __init__(self, trajectories: Sequence, total_tokens: Optional[int] = None,
+                 kind: int = 0):
         keep = []
         trajs = (TrajectoryC * len(trajectories))()
         for ti, t in enumerate(trajectories):
@@ -171,7 +193,8 @@ class ViewMask:
             trajs[ti] = TrajectoryC(int(t.begin), int(t.end), len(t.edits), edits)
         T = total_tokens if total_tokens is not None else int(trajectories[-1].end)
         handle = ctypes.c_void_p()
-        check(mv_build_view_mask(trajs, len(trajectories), T, ctypes.byref(handle)))
+        check(mv_build_view_mask_kind(trajs, len(trajectories), T, int(kind),
+                                      ctypes.byref(handle)))
         self._h = handle
         self.total_tokens = T
         self._dev = None
@@ -195,6 +218,15 @@ class ViewMask:
         out = torch.empty(self.total_tokens, dtype=torch.int32)
         check(mv_view_mask_death(self._h, _ptr(out)))
         return out
+
+    def leaves(self):
+        """(tokens, teacher_rows, student_rows): int32 host tensors, one entry per leaf."""
+        n = ctypes.c_int32()
+        check(mv_view_mask_leaves(self._h, None, None, None, 0, ctypes.byref(n)))
+        out = [torch.empty(n.value, dtype=torch.int32) for _ in range(3)]
+        check(mv_view_mask_leaves(self._h, _ptr(out[0]), _ptr(out[1]), _ptr(out[2]), n.value,
+                                  ctypes.byref(n)))
+        return tuple(out)
 
     def device_bytes(self) -> int:
         return int(mv_view_mask_device_bytes(self._h))
@@ -327,10 +359,65 @@ def ppo_clip_dlogp(ratio, adv, eps_low=0.2, eps_high=0.2, scale=1.0, stream=None
 
 
 # ---------------------------------------------------------------------------
+# SDCC junction KL
+# ---------------------------------------------------------------------------
+def _kl_shape(h_teacher, rows_teacher, h_student, weight):
+    return KLShape(rows_teacher.numel(), weight.shape[1], weight.shape[0], h_teacher.shape[0],
+                   h_student.shape[0])
+
+
+def _need_rows(*ts):
+    for t in ts:
+        if t.dtype != torch.int32 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError("expected contiguous int32 CUDA row indices")
+
+
+def sdcc_kl(h_teacher, rows_teacher, h_student, rows_student, weight, workspace=None,
+            stream=None):
+    """Per-leaf KL(p_teacher || q_student) and both log-partition values."""
+    _need_bf16_cuda(h_teacher, h_student, weight)
+    _need_rows(rows_teacher, rows_student)
+    s = _kl_shape(h_teacher, rows_teacher, h_student, weight)
+    n, dev = rows_teacher.numel(), weight.device
+    kl, lse_t, lse_s = (torch.empty(n, dtype=torch.float32, device=dev) for _ in range(3))
+    if workspace is None:
+        workspace = torch.empty(int(mv_sdcc_kl_workspace_bytes(ctypes.byref(s))),
+                                dtype=torch.uint8, device=dev)
+    check(mv_sdcc_kl(ctypes.byref(s), _ptr(h_teacher), _ptr(rows_teacher), _ptr(h_student),
+                     _ptr(rows_student), _ptr(weight), _ptr(kl), _ptr(lse_t), _ptr(lse_s),
+                     _ptr(workspace), workspace.numel(), _stream(stream)))
+    return kl, lse_t, lse_s
+
+
+def sdcc_kl_bwd(h_teacher, rows_teacher, h_student, rows_student, weight, lse_t, lse_s, dkl,
+                workspace=None, stream=None):
+    """Gradient of sum_p dkl[p] KL_p into the student hidden row of each leaf: bf16 [n, H]."""
+    _need_bf16_cuda(h_teacher, h_student, weight)
+    _need_rows(rows_teacher, rows_student)
+    s = _kl_shape(h_teacher, rows_teacher, h_student, weight)
+    n, dev = rows_teacher.numel(), weight.device
+    dh = torch.empty((n, weight.shape[1]), dtype=torch.bfloat16, device=dev)
+    if workspace is None:
+        workspace = torch.empty(int(mv_sdcc_kl_bwd_workspace_bytes(ctypes.byref(s))),
+                                dtype=torch.uint8, device=dev)
+    check(mv_sdcc_kl_bwd(ctypes.byref(s), _ptr(h_teacher), _ptr(rows_teacher), _ptr(h_student),
+                         _ptr(rows_student), _ptr(weight), _ptr(lse_t), _ptr(lse_s), _ptr(dkl),
+                         _ptr(dh), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return dh
+
+
+def sdcc_lambda(step: int, total_steps: int, lambda_max: float = 0.1,
+                warmup_frac: float = 0.2) -> float:
+    return float(mv_sdcc_lambda(int(step), int(total_steps), float(lambda_max),
+                                float(warmup_frac)))
+
+
+# ---------------------------------------------------------------------------
 # kernel timing
 # ---------------------------------------------------------------------------
 KERNELS = ["attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq",
-           "lm_logits", "lm_combine", "lm_grad", "lm_dh", "materialize", "ppo_clip"]
+           "lm_logits", "lm_combine", "lm_grad", "lm_dh", "kl_logits", "kl_combine", "kl_grad", "kl_dh",
+           "materialize", "ppo_clip"]
 
 
 def profile_enable(on: bool = True) -> None:

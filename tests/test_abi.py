@@ -91,6 +91,26 @@ def test_logprob_argument_errors():
     assert _status(mv.mv_token_logprob_bwd(ctypes.byref(s), *([FAKE] * 7), nb - 1, None)) == "MV_ERR_WORKSPACE"
 
 
+def test_sdcc_argument_errors():
+    s = mv.KLShape(8, 100, 50, 16, 16)
+    assert _status(mv.mv_sdcc_kl(ctypes.byref(s), *([FAKE] * 9), 1 << 30, None)) == "MV_ERR_UNSUPPORTED"
+    s = mv.KLShape(8, 128, 50, -1, 16)
+    assert _status(mv.mv_sdcc_kl(ctypes.byref(s), *([FAKE] * 9), 1 << 30, None)) == "MV_ERR_SHAPE"
+    s = mv.KLShape(8, 128, 50, 16, 16)
+    need = mv.mv_sdcc_kl_workspace_bytes(ctypes.byref(s))
+    assert need > 0
+    assert _status(mv.mv_sdcc_kl(ctypes.byref(s), *([FAKE] * 9), need - 1, None)) == "MV_ERR_WORKSPACE"
+    a = [FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE]
+    assert _status(mv.mv_sdcc_kl(ctypes.byref(s), *a, need, None)) == "MV_ERR_INVALID_ARG"
+    nb = mv.mv_sdcc_kl_bwd_workspace_bytes(ctypes.byref(s))
+    assert nb >= 8 * 256 * 2
+    assert _status(mv.mv_sdcc_kl_bwd(ctypes.byref(s), *([FAKE] * 10), nb - 1, None)) == "MV_ERR_WORKSPACE"
+    empty = mv.KLShape(0, 128, 50, 0, 0)
+    assert _status(mv.mv_sdcc_kl(ctypes.byref(empty), *([None] * 9), 0, None)) == "MV_OK"
+    h = ctypes.c_void_p()
+    assert _status(mv.mv_build_view_mask_kind(None, 0, 10, 0, ctypes.byref(h))) == "MV_ERR_INVALID_ARG"
+
+
 def test_mask_buffer_errors():
     m = _mask()
     assert _status(mv.mv_view_mask_upload(m.handle, None, 1 << 20, None)) == "MV_ERR_INVALID_ARG"
