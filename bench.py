@@ -46,12 +46,17 @@ def parse():
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one plain 1 GiB device copy (PMC byte-counter calibration)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-sdcc", action="store_true",
+                    help="skip the separately timed SDCC junction-KL pass")
     return ap.parse_args()
 
 
-def kernel_flops(P, d, hq, T_lm, H, V):
+def kernel_flops(P, d, hq, T_lm, H, V, n_leaves=0):
     """Algorithmic FLOPs of one launch of each kernel."""
     return {
+        "kl_logits": 4.0 * n_leaves * H * V,  # teacher and student logits of every leaf
+        "kl_grad": 4.0 * n_leaves * H * V,    # both recomputed for q - p
+        "kl_dh": 2.0 * n_leaves * H * V,      # (q - p) W into the student rows
         "attn_fwd": 4.0 * d * P * hq,         # S = Q K^T and O = P V over visible pairs
         "attn_bwd_dkdv": 8.0 * d * P * hq,    # S, dP recomputed; dV = P^T dO, dK = dS^T Q
         "attn_bwd_dq": 6.0 * d * P * hq,      # S, dP recomputed; dQ = dS K
@@ -96,10 +101,10 @@ def cpu_baseline(trajs, wl, lmw, attn_flops_step, lm_flops_step):
     from paper_2609_00865_amd import synth
 
     cores = torch.get_num_threads()
-    # attention: first trajectory, KV group 0, rows [0, R), fp32 forward + backward
+    # attention: first trajectory, KV groups 0 and 1, rows [0, R), fp32 forward + backward
     R = 24576
     G = wl.n_heads_q // wl.n_heads_kv
-    heads = list(range(G))
+    heads = list(range(2 * G))
     t0 = trajs[0]
     sub = [synth.Trajectory(t0.begin, t0.begin + R,
                             tuple(e for e in t0.edits if e.junction < t0.begin + R))]
@@ -114,8 +119,8 @@ def cpu_baseline(trajs, wl, lmw, attn_flops_step, lm_flops_step):
     a_s = time.perf_counter() - a0
     attn_rate = 14.0 * wl.head_dim * pairs * len(heads) / a_s
     log(f"cpu oracle attention sample: {a_s:.2f}s, {attn_rate / 1e9:.1f} GFLOP/s")
-    # LM head: 1024 tokens, fp32 forward + backward
-    n = 1024
+    # LM head: 2048 tokens, fp32 forward + backward
+    n = 2048
     h, w, y, old, g = synth.make_logprob_inputs(n, lmw.hidden, lmw.vocab, 0)
     l0 = time.perf_counter()
     OL.token_logprob(h, w, y, old, dtype=torch.float32)
@@ -129,10 +134,70 @@ def cpu_baseline(trajs, wl, lmw, attn_flops_step, lm_flops_step):
         "unit": "TFLOP/s",
         "cores": cores,
         "kind": "oracle",
-        "sample": (f"attention: trajectory 0 rows [0,{R}) x KV group 0 ({len(heads)} heads), "
+        "sample": (f"attention: trajectory 0 rows [0,{R}) x KV groups 0-1 ({len(heads)} heads), "
                    f"fp32 LogitTree fwd+bwd, {a_s:.2f}s; lm-head: {n} tokens x full vocab, "
                    f"fp32 fwd+bwd, {l_s:.2f}s; scaled to one step by useful FLOPs "
                    f"(oracle step = {step_s:.0f}s)"),
+    }
+
+
+def time_sdcc(args, mv, synth, mask, wl, lmw, dev):
+    """The SDCC junction KL (forward + student gradient) over the diverging
+    leaves of the same packed batch, timed on its own after the step: teacher
+    rows of a live-view pass, student rows of a final-walk pass (hidden states
+    drawn like the LM head's), the LM head's vocabulary and width."""
+    import torch
+    _, rows_t, rows_s = mask.leaves()
+    n = rows_t.numel()
+    T, H, V = wl.total_tokens, lmw.hidden, lmw.vocab
+    hT, w, _, _, _ = synth.make_logprob_inputs(T, H, V, args.seed, device="cuda")
+    hS, _, _, _, _ = synth.make_logprob_inputs(T, H, V, args.seed + 1, device="cuda")
+    rt, rs = rows_t.to(dev), rows_s.to(dev)
+    dkl = torch.full((n,), 0.1, dtype=torch.float32, device=dev)   # lambda at the ramp's end
+    s = mv.KLShape(n, H, V, T, T)
+    import ctypes
+    ws_f = torch.empty(int(mv.mv_sdcc_kl_workspace_bytes(ctypes.byref(s))), dtype=torch.uint8,
+                       device=dev)
+    ws_b = torch.empty(int(mv.mv_sdcc_kl_bwd_workspace_bytes(ctypes.byref(s))),
+                       dtype=torch.uint8, device=dev)
+
+    def kl_step():
+        kl, lt, ls = mv.sdcc_kl(hT, rt, hS, rs, w, workspace=ws_f)
+        mv.sdcc_kl_bwd(hT, rt, hS, rs, w, lt, ls, dkl, workspace=ws_b)
+        return kl
+
+    for _ in range(args.warmup):
+        kl_step()
+    torch.cuda.synchronize()
+    mv.profile_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    stream = torch.cuda.current_stream()
+    e0.record(stream)
+    for _ in range(args.steps):
+        kl = kl_step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    kt = {}
+    for name in ("kl_logits", "kl_combine", "kl_grad", "kl_dh"):
+        tot, cnt = mv.profile_read(name)
+        if cnt:
+            kt[name] = round(tot / cnt, 3)
+    mv.profile_enable(False)
+    flops = 10.0 * n * H * V
+    tflops = flops / (ms * 1e-3) / 1e12
+    log(f"sdcc: {n} leaves, {ms:.2f} ms fwd+bwd, {tflops:.0f} TFLOP/s")
+    return {
+        "leaves": n,
+        "ms": round(ms, 3),
+        "tflop": round(flops / 1e12, 3),
+        "tflops": round(tflops, 2),
+        "frac_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "leaves_per_s": round(n / (ms * 1e-3), 1),
+        "kl_mean": round(float(kl.mean()), 5),
+        "kernels_ms": kt,
+        "flop_convention": "forward 4nHV (teacher + student logits), backward 6nHV "
+                           "(both recomputed, then the student dH)",
     }
 
 
@@ -210,6 +275,7 @@ def main():
             kt[name] = {"ms_per_launch": tot / n, "launches": n}
     mv.profile_enable(False)
     log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step (host wall {wall_ms:.2f})")
+    sdcc = None if args.no_sdcc else time_sdcc(args, mv, synth, mask, wl, lmw, dev)
 
     d, hq = wl.head_dim, wl.n_heads_q
     T_lm, H, V = lmw.n_tokens, lmw.hidden, lmw.vocab
@@ -217,6 +283,7 @@ def main():
     lm_useful = 6.0 * T_lm * H * V
     step_flops = attn_useful + lm_useful
     per_launch = kernel_flops(P, d, hq, T_lm, H, V)
+    per_launch = {n: f for n, f in per_launch.items() if not n.startswith("kl")}
     attn_ms = sum(kt[n]["ms_per_launch"] for n in kt if n.startswith("attn"))
     lm_ms = sum(kt[n]["ms_per_launch"] for n in kt if n.startswith("lm"))
     dom = max((n for n in kt if n in per_launch), key=lambda n: kt[n]["ms_per_launch"])
@@ -276,6 +343,8 @@ def main():
             "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated)",
         },
     }
+    if sdcc is not None:
+        out["sdcc"] = sdcc
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(trajs, wl, lmw, attn_useful, lm_useful)
