@@ -277,6 +277,53 @@ mv_status mv_ppo_clip_dlogp(int32_t n, const float* ratio, const float* adv,
                             float* dlogp, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * GRPO token loss and drift diagnostics (training recipe of Appendix F; the
+ * ratio, advantage weight and KL term of a token all use its live-view
+ * log-prob, Propositions "rl_tree" / "rl_4d"; drift is Eq. "logdiff").
+ *
+ * Trajectories are packed back to back: traj_ptr (device int32 [n_traj + 1])
+ * holds their first token positions, traj_ptr[0] = 0 and traj_ptr[n_traj] =
+ * n_tokens, non-decreasing (a malformed array gives unspecified results but
+ * no access outside the arrays).  Consecutive runs of group_size trajectories
+ * are the sample groups of one prompt.
+ *
+ *   A_i      = (r_i - mean_group r) / (std_group r + adv_eps)   (sample std,
+ *              n - 1; 0 for a group of one)
+ *   rho_t    = exp(logp_t - logp_old_t)          (logp_old: rollout log-prob)
+ *   surr_t   = min(rho_t A, clamp(rho_t, 1 - eps_low, 1 + eps_high) A)
+ *   k3_t     = exp(ref_t - logp_t) - (ref_t - logp_t) - 1   (reference KL)
+ *   loss     = mean over loss tokens of (-surr_t + beta k3_t)
+ *   dlogp_t  = d loss / d logp_t (0 off the loss mask), the upstream gradient
+ *              of mv_token_logprob_bwd.
+ * Inputs fp32 [n_tokens] (device); loss_mask uint8 [n_tokens] (null: every
+ * token); logp_ref may be null only with beta == 0.  advantage (fp32
+ * [n_traj], nullable) receives A.  stats (device) receives, in order: loss,
+ * logdiff (mean |logp - logp_old| over loss tokens), the fractions of loss
+ * tokens whose clipped term is active on the low and the high side, mean k3,
+ * mean ratio, the number of loss tokens, mean |A| over trajectories.  Every
+ * reduction runs in a fixed order (bitwise reproducible).
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t n_tokens, n_traj, group_size;
+  float eps_low, eps_high;        /* clip pair, each in [0, 1)            */
+  float beta;                     /* reference-KL weight (0: off)         */
+  float adv_eps;                  /* added to the group std               */
+} mv_grpo_shape;
+
+typedef struct {
+  float loss, logdiff, clip_frac_low, clip_frac_high, kl_ref, ratio_mean, n_loss_tokens,
+      adv_abs_mean;
+} mv_grpo_stats;
+
+size_t mv_grpo_loss_workspace_bytes(const mv_grpo_shape* shape);
+
+mv_status mv_grpo_loss(const mv_grpo_shape* shape, const int32_t* traj_ptr, const float* reward,
+                       const float* logp, const float* logp_old, const float* logp_ref,
+                       const uint8_t* loss_mask, float* advantage, float* dlogp,
+                       mv_grpo_stats* stats, void* workspace, size_t workspace_bytes,
+                       hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * SDCC junction KL (Section 5.1, Eq. "soft_loss"; forward KL, teacher first).
  *
  * At each diverging leaf p the teacher distribution p = softmax(W h_T[p]) (the
@@ -338,7 +385,7 @@ float mv_sdcc_lambda(int32_t step, int32_t total_steps, float lambda_max, float 
  * the summed duration (ms) and launch count of the kernels named `kernel`
  * (one of "attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce",
  * "attn_bwd_dq", "lm_logits", "lm_combine", "lm_grad", "lm_dh", "kl_logits",
- * "kl_combine", "kl_grad", "kl_dh", "materialize", "ppo_clip").  Not for use
+ * "kl_combine", "kl_grad", "kl_dh", "grpo", "materialize", "ppo_clip").  Not for use
  * under stream capture.
  * ------------------------------------------------------------------------ */
 mv_status mv_profile_enable(int32_t on);

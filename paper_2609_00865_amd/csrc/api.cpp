@@ -75,6 +75,12 @@ hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, c
 hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const void* weight,
                               const int32_t* target, const float* lse, const float* dlogp,
                               void* dhidden, void* ws, hipStream_t stream);
+size_t grpo_ws_bytes(int T, int n_traj);
+hipError_t launch_grpo(int T, int n_traj, int G, float eps_lo, float eps_hi, float beta,
+                       float adv_eps, const int32_t* traj_ptr, const float* reward,
+                       const float* logp, const float* logp_old, const float* logp_ref,
+                       const uint8_t* mask, float* adv_out, float* dlogp, float* stats, void* ws,
+                       hipStream_t stream);
 size_t kl_fwd_ws_bytes(int n, int H, int V);
 size_t kl_bwd_ws_bytes(int n, int H, int V);
 hipError_t launch_kl_fwd(int n, int H, int V, const void* hT, int nT, const int32_t* rowsT,
@@ -146,6 +152,19 @@ mv_status check_logprob(const mv_logprob_shape* s) {
     return fail(MV_ERR_UNSUPPORTED, "hidden/weight larger than 2^31 elements");
   if (!(s->eps_low >= 0.f && s->eps_low < 1.f && s->eps_high >= 0.f && std::isfinite(s->eps_high)))
     return fail(MV_ERR_INVALID_ARG, "clip range must satisfy 0 <= eps_low < 1, 0 <= eps_high");
+  return MV_OK;
+}
+
+mv_status check_grpo(const mv_grpo_shape* s) {
+  if (s == nullptr) return fail(MV_ERR_INVALID_ARG, "null shape");
+  if (s->n_tokens < 0 || s->n_traj <= 0 || s->group_size <= 0)
+    return fail(MV_ERR_SHAPE, "n_tokens >= 0, n_traj > 0, group_size > 0 required");
+  if (s->n_traj % s->group_size != 0)
+    return fail(MV_ERR_SHAPE, "n_traj must be a multiple of group_size");
+  if (!(s->eps_low >= 0.f && s->eps_low < 1.f && s->eps_high >= 0.f && s->eps_high < 1.f))
+    return fail(MV_ERR_INVALID_ARG, "clip eps must lie in [0, 1)");
+  if (!(s->beta >= 0.f) || !(s->adv_eps >= 0.f))
+    return fail(MV_ERR_INVALID_ARG, "beta and adv_eps must be >= 0");
   return MV_OK;
 }
 
@@ -358,6 +377,35 @@ mv_status mv_profile_read(const char* kernel, double* total_ms, int32_t* count) 
   *total_ms = tot;
   *count = n;
   return MV_OK;
+}
+
+size_t mv_grpo_loss_workspace_bytes(const mv_grpo_shape* s) {
+  if (check_grpo(s) != MV_OK) return 0;
+  return mv::grpo_ws_bytes(s->n_tokens, s->n_traj);
+}
+
+mv_status mv_grpo_loss(const mv_grpo_shape* s, const int32_t* traj_ptr, const float* reward,
+                       const float* logp, const float* logp_old, const float* logp_ref,
+                       const uint8_t* loss_mask, float* advantage, float* dlogp,
+                       mv_grpo_stats* stats, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (mv_status st = check_grpo(s); st != MV_OK) return st;
+  if (traj_ptr == nullptr || reward == nullptr || stats == nullptr || ws == nullptr)
+    return fail(MV_ERR_INVALID_ARG, "traj_ptr, reward, stats and workspace are required");
+  if (s->n_tokens > 0 && (logp == nullptr || logp_old == nullptr || dlogp == nullptr))
+    return fail(MV_ERR_INVALID_ARG, "logp, logp_old and dlogp are required");
+  if (logp_ref == nullptr && s->beta != 0.f)
+    return fail(MV_ERR_INVALID_ARG, "beta > 0 needs logp_ref");
+  const size_t need = mv::grpo_ws_bytes(s->n_tokens, s->n_traj);
+  if (ws_bytes < need) {
+    std::ostringstream os;
+    os << "GRPO workspace has " << ws_bytes << " bytes, needs " << need;
+    return fail(MV_ERR_WORKSPACE, os.str());
+  }
+  return hip_status(mv::launch_grpo(s->n_tokens, s->n_traj, s->group_size, s->eps_low,
+                                    s->eps_high, s->beta, s->adv_eps, traj_ptr, reward, logp,
+                                    logp_old, logp_ref, loss_mask, advantage, dlogp,
+                                    reinterpret_cast<float*>(stats), ws, stream),
+                    "GRPO loss launch");
 }
 
 mv_status mv_ppo_clip_dlogp(int32_t n, const float* ratio, const float* adv, float eps_low,

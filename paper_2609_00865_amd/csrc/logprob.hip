@@ -21,6 +21,8 @@
 // Tiles are ordered so that the blocks resident on one XCD at a time form a
 // compact 2-D patch (a few token tiles x several A tiles) and share operand
 // slices in that XCD's L2.
+#include <algorithm>
+
 #include "mv_device.h"
 
 namespace mv {
@@ -65,6 +67,11 @@ struct LmArgs {
   int n_leaves, n_rows_T, n_rows_S;
   int T, H, V, Vp, n_chunks;
   int nA, nT;         // tiles along the A side and along tokens
+  // dH mode split over the vocabulary (K) when there are too few output
+  // tiles to fill the chip: split s covers k slices [s*nk_split, ...) and
+  // writes fp32 partials dh_part[s][t][H], summed in order by dh_reduce_kernel
+  int k_split, nk_split;
+  float* dh_part;
 };
 
 template <int MODE, int NW>
@@ -78,12 +85,15 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
 
   // Blocks are dealt to XCDs round-robin; give each XCD a contiguous range of
   // the rasterised tile order (groups of GROUP_T token tiles x all A tiles).
-  const int n_tiles = a.nA * a.nT;
+  const int n_out = a.nA * a.nT;
+  const int n_tiles = n_out * (MODE == kModeDh ? a.k_split : 1);
   const int per_xcd = (n_tiles + kNumXcd - 1) / kNumXcd;
   int xcd, local;
   xcd_split(xcd, local);
-  const int L = xcd * per_xcd + local;
-  if (local >= per_xcd || L >= n_tiles) return;
+  const int Lx = xcd * per_xcd + local;
+  if (local >= per_xcd || Lx >= n_tiles) return;
+  const int split = Lx / n_out;            // 0 unless the dH product is split
+  const int L = Lx % n_out;
   const int grp = L / (GROUP_T * a.nA);
   const int rem = L % (GROUP_T * a.nA);
   const int t_in = min(GROUP_T, a.nT - grp * GROUP_T);
@@ -97,7 +107,8 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
 
   const int K = (MODE == kModeDh) ? a.Vp : a.H;
   const int a_rows = (MODE == kModeDh) ? a.H : a.V;
-  const int nk = K / BKK;
+  const int kbeg = (MODE == kModeDh) ? split * a.nk_split : 0;
+  const int nk = (MODE == kModeDh) ? min(K / BKK - kbeg, a.nk_split) : K / BKK;
   // tiles wholly inside the operands skip the per-load bounds checks
   const bool interior = (t0 + BT <= a.T) && (MODE == kModeDh ? (a0 + BA <= a.H) : (a0 + BA <= a_rows));
 
@@ -178,10 +189,12 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
     }
   };
 
-  load(0);
-  store(smem);
-  if (nk > 1) load(BKK);
-  __syncthreads();
+  if (nk > 0) {  // block-uniform
+    load(kbeg * BKK);
+    store(smem);
+    if (nk > 1) load((kbeg + 1) * BKK);
+    __syncthreads();
+  }
   for (int kk = 0; kk < nk; ++kk) {
     const u16* sA = smem + (kk & 1) * STAGE;
     const u16* sB = sA + BA * PAD;
@@ -203,7 +216,7 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
     }
     if (kk + 1 < nk) {
       store(smem + ((kk + 1) & 1) * STAGE);
-      if (kk + 2 < nk) load((kk + 2) * BKK);
+      if (kk + 2 < nk) load((kbeg + kk + 2) * BKK);
     }
     __syncthreads();
   }
@@ -336,6 +349,23 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
           }
         }
     }
+  } else if (a.k_split > 1) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int t = t0 + wt * WTOK + j * 32 + c;
+      if (t >= a.T) continue;
+      float* out = a.dh_part + (size_t(split) * a.T + t) * a.H;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int hcol = arow0 + i * 32 + q4 * 8 + g * 4;
+          if (hcol >= a.H) continue;
+          *reinterpret_cast<float4*>(out + hcol) =
+              make_float4(acc[i][j][q4 * 4 + 0], acc[i][j][q4 * 4 + 1], acc[i][j][q4 * 4 + 2],
+                          acc[i][j][q4 * 4 + 3]);
+        }
+    }
   } else {
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
@@ -428,6 +458,30 @@ __global__ __launch_bounds__(256) void kl_combine_kernel(LmArgs a, float* kl, fl
   kl[leaf] = cr / st + ((ms - mt) + (l2s - l2t)) * kLn2;
 }
 
+// Vocabulary splits for a dH product: none when the output tiles already
+// cover the CUs several times, otherwise the count (<= 8) with the least time
+// per split slice, rounds of 256 resident blocks / splits (a larger count must
+// gain 5% to be taken: each split adds an fp32 partial to write and reduce).
+static int dh_splits(int n_tokens, int H) {
+  const int tiles = ((H + BA - 1) / BA) * ((n_tokens + BT - 1) / BT);
+  if (tiles >= 4 * 256) return 1;
+  int best = 1;
+  double best_t = (tiles + 255) / 256;
+  for (int s = 2; s <= 8; ++s) {
+    const double t = double((tiles * s + 255) / 256) / s;
+    if (t < 0.95 * best_t) {
+      best_t = t;
+      best = s;
+    }
+  }
+  return best;
+}
+
+static size_t dh_part_bytes(int T, int H) {
+  const int splits = dh_splits(T, H);
+  return splits > 1 ? align256(size_t(splits) * T * H * sizeof(float)) : 0;
+}
+
 size_t kl_fwd_ws_bytes(int n, int H, int V) {
   (void)H;
   const int n_chunks = vocab_pad(V) / 128;
@@ -436,8 +490,7 @@ size_t kl_fwd_ws_bytes(int n, int H, int V) {
 }
 
 size_t kl_bwd_ws_bytes(int n, int H, int V) {
-  (void)H;
-  return align256(size_t(n) * vocab_pad(V) * sizeof(u16)) + 256;
+  return align256(size_t(n) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(n, H) + 256;
 }
 
 size_t logprob_fwd_ws_bytes(int T, int H, int V) {
@@ -448,17 +501,66 @@ size_t logprob_fwd_ws_bytes(int T, int H, int V) {
 }
 
 size_t logprob_bwd_ws_bytes(int T, int H, int V) {
-  (void)H;
-  return align256(size_t(T) * vocab_pad(V) * sizeof(u16)) + 256;
+  return align256(size_t(T) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(T, H) + 256;
 }
 
 static char* align_ptr(void* p) {
   return reinterpret_cast<char*>((reinterpret_cast<uintptr_t>(p) + 255) & ~uintptr_t(255));
 }
 
+
 static dim3 gemm_grid(const LmArgs& a) {
-  const int per_xcd = (a.nA * a.nT + kNumXcd - 1) / kNumXcd;
+  const int splits = a.k_split > 1 ? a.k_split : 1;
+  const int per_xcd = (a.nA * a.nT * splits + kNumXcd - 1) / kNumXcd;
   return dim3(per_xcd * kNumXcd);
+}
+
+// dH[t][h] = sum over splits of the fp32 partials, in split order (the
+// result does not depend on scheduling), rounded once to bf16.
+__global__ __launch_bounds__(256) void dh_reduce_kernel(const float* part, u16* dh, int splits,
+                                                        size_t n4) {
+  const size_t i = size_t(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= n4) return;
+  const float4* p = reinterpret_cast<const float4*>(part) + i;
+  float4 acc = p[0];
+  for (int s = 1; s < splits; ++s) {
+    const float4 v = p[size_t(s) * n4];
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  uint2 w;
+  w.x = pack2(acc.x, acc.y);
+  w.y = pack2(acc.z, acc.w);
+  reinterpret_cast<uint2*>(dh)[i] = w;
+}
+
+
+
+// dh[T, H] = G[T, Vp] W[Vp, H] (bf16 out), split over the vocabulary when the
+// output alone would leave CUs idle; `part` is the fp32 partial area of the
+// workspace (dh_part_bytes).
+static hipError_t launch_dh(LmArgs b, float* part, const char* name, hipStream_t stream) {
+  const int nk_total = b.Vp / BKK;
+  int splits = std::min(dh_splits(b.T, b.H), nk_total);
+  b.nk_split = (nk_total + splits - 1) / splits;
+  splits = (nk_total + b.nk_split - 1) / b.nk_split;  // no empty split
+  b.k_split = splits;
+  b.dh_part = part;
+  b.nA = (b.H + BA - 1) / BA;
+  b.nT = (b.T + BT - 1) / BT;
+  {
+    ProfScope p(name, stream);
+    hipLaunchKernelGGL((lm_gemm_kernel<kModeDh, NWAVES>), gemm_grid(b), dim3(NWAVES * 64), 0,
+                       stream, b);
+    if (splits > 1) {
+      const size_t n4 = size_t(b.T) * b.H / 4;
+      hipLaunchKernelGGL(dh_reduce_kernel, dim3(unsigned((n4 + 255) / 256)), dim3(256), 0, stream,
+                         part, b.dh, splits, n4);
+    }
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, const void* hidden,
@@ -516,13 +618,10 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
     hipLaunchKernelGGL((lm_gemm_kernel<kModeGrad, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
                        stream, a);
   }
-  a.nA = (H + BA - 1) / BA;
-  {
-    ProfScope p("lm_dh", stream);
-    hipLaunchKernelGGL((lm_gemm_kernel<kModeDh, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
-                       stream, a);
-  }
-  return hipGetLastError();
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(G) +
+                                         align256(size_t(T) * a.Vp * sizeof(u16)));
+  return launch_dh(a, part, "lm_dh", stream);
 }
 
 hipError_t launch_kl_fwd(int n, int H, int V, const void* hT, int nT, const int32_t* rowsT,
@@ -589,6 +688,7 @@ hipError_t launch_kl_bwd(int n, int H, int V, const void* hT, int nT, const int3
     hipLaunchKernelGGL((lm_gemm_kernel<kModeKLGrad, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
                        stream, a);
   }
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   // dh = G W over the leaves
   LmArgs b{};
   b.w = a.w;
@@ -598,14 +698,9 @@ hipError_t launch_kl_bwd(int n, int H, int V, const void* hT, int nT, const int3
   b.H = H;
   b.V = V;
   b.Vp = a.Vp;
-  b.nA = (H + BA - 1) / BA;
-  b.nT = (n + BT - 1) / BT;
-  {
-    ProfScope p("kl_dh", stream);
-    hipLaunchKernelGGL((lm_gemm_kernel<kModeDh, NWAVES>), gemm_grid(b), dim3(NWAVES * 64), 0,
-                       stream, b);
-  }
-  return hipGetLastError();
+  float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(G) +
+                                         align256(size_t(n) * a.Vp * sizeof(u16)));
+  return launch_dh(b, part, "kl_dh", stream);
 }
 
 }  // namespace mv

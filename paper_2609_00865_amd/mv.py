@@ -78,6 +78,16 @@ class KLShape(ctypes.Structure):
                 ("n_rows_student", ctypes.c_int32)]
 
 
+class GrpoShape(ctypes.Structure):
+    _fields_ = [("n_tokens", ctypes.c_int32), ("n_traj", ctypes.c_int32),
+                ("group_size", ctypes.c_int32), ("eps_low", ctypes.c_float),
+                ("eps_high", ctypes.c_float), ("beta", ctypes.c_float),
+                ("adv_eps", ctypes.c_float)]
+
+
+GRPO_STATS = ["loss", "logdiff", "clip_frac_low", "clip_frac_high", "kl_ref", "ratio_mean",
+              "n_loss_tokens", "adv_abs_mean"]
+
 _vp, _sz, _i32, _f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_float
 _P = ctypes.POINTER
 
@@ -122,6 +132,9 @@ mv_token_logprob_bwd = _sig("mv_token_logprob_bwd", ctypes.c_int, _P(LogprobShap
                             _vp, _vp, _vp, _vp, _vp, _sz, _vp)
 mv_ppo_clip_dlogp = _sig("mv_ppo_clip_dlogp", ctypes.c_int, _i32, _vp, _vp, _f32, _f32, _f32,
                          _vp, _vp)
+mv_grpo_loss_workspace_bytes = _sig("mv_grpo_loss_workspace_bytes", _sz, _P(GrpoShape))
+mv_grpo_loss = _sig("mv_grpo_loss", ctypes.c_int, _P(GrpoShape), _vp, _vp, _vp, _vp, _vp, _vp,
+                    _vp, _vp, _vp, _vp, _sz, _vp)
 mv_sdcc_kl_workspace_bytes = _sig("mv_sdcc_kl_workspace_bytes", _sz, _P(KLShape))
 mv_sdcc_kl = _sig("mv_sdcc_kl", ctypes.c_int, _P(KLShape), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                   _vp, _sz, _vp)
@@ -142,6 +155,7 @@ EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_ma
             "mv_token_logprob_bwd_workspace_bytes", "mv_token_logprob_bwd", "mv_ppo_clip_dlogp",
             "mv_build_view_mask_kind", "mv_view_mask_leaves", "mv_sdcc_kl_workspace_bytes",
             "mv_sdcc_kl", "mv_sdcc_kl_bwd_workspace_bytes", "mv_sdcc_kl_bwd", "mv_sdcc_lambda",
+            "mv_grpo_loss_workspace_bytes", "mv_grpo_loss",
             "mv_profile_enable", "mv_profile_read"]
 
 VIEW_LIVE, VIEW_FINAL = 0, 1
@@ -359,6 +373,28 @@ def ppo_clip_dlogp(ratio, adv, eps_low=0.2, eps_high=0.2, scale=1.0, stream=None
 
 
 # ---------------------------------------------------------------------------
+# GRPO loss and drift diagnostics
+# ---------------------------------------------------------------------------
+def grpo_loss(traj_ptr, reward, logp, logp_old, logp_ref=None, loss_mask=None, group_size=16,
+              eps_low=0.2, eps_high=0.28, beta=0.0, adv_eps=1e-6, workspace=None, stream=None):
+    """(advantage [n_traj], dlogp [T], stats fp32 [8] in GRPO_STATS order), all on device."""
+    T, n_traj = logp.numel(), reward.numel()
+    s = GrpoShape(T, n_traj, int(group_size), float(eps_low), float(eps_high), float(beta),
+                  float(adv_eps))
+    dev = logp.device
+    adv = torch.empty(n_traj, dtype=torch.float32, device=dev)
+    dlogp = torch.empty(T, dtype=torch.float32, device=dev)
+    stats = torch.empty(8, dtype=torch.float32, device=dev)
+    if workspace is None:
+        workspace = torch.empty(int(mv_grpo_loss_workspace_bytes(ctypes.byref(s))),
+                                dtype=torch.uint8, device=dev)
+    check(mv_grpo_loss(ctypes.byref(s), _ptr(traj_ptr), _ptr(reward), _ptr(logp),
+                       _ptr(logp_old), _ptr(logp_ref), _ptr(loss_mask), _ptr(adv), _ptr(dlogp),
+                       _ptr(stats), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return adv, dlogp, stats
+
+
+# ---------------------------------------------------------------------------
 # SDCC junction KL
 # ---------------------------------------------------------------------------
 def _kl_shape(h_teacher, rows_teacher, h_student, weight):
@@ -417,6 +453,7 @@ def sdcc_lambda(step: int, total_steps: int, lambda_max: float = 0.1,
 # ---------------------------------------------------------------------------
 KERNELS = ["attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq",
            "lm_logits", "lm_combine", "lm_grad", "lm_dh", "kl_logits", "kl_combine", "kl_grad", "kl_dh",
+           "grpo",
            "materialize", "ppo_clip"]
 
 

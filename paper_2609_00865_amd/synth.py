@@ -316,3 +316,27 @@ def make_logprob_inputs(n_tokens: int, hidden: int, vocab: int, seed: int = 0,
     old = -2.0 + torch.randn((n_tokens,), generator=gen, device=device)
     g = torch.randn((n_tokens,), generator=gen, device=device)
     return h, w, tgt.to(torch.int32), old.float(), g.float()
+
+
+def make_grpo_inputs(lengths: Sequence[int], seed: int = 0, logp_noise: float = 0.1,
+                     ref_noise: float = 0.05, mask_frac: float = 0.8):
+    """Per-token inputs of the GRPO loss for trajectories of the given lengths:
+    traj_ptr int32 [n+1], reward fp32 [n] (EM in {0, 0.2, 1}, as the recipe's
+    exact-match reward with a format bonus), logp fp32 [T] ~ -2 + N(0, 1),
+    logp_old = logp + N(0, logp_noise^2) (so both clip edges and the interior
+    occur), logp_ref = logp + N(0, ref_noise^2), loss mask uint8 with the
+    given fraction of ones."""
+    gen = torch.Generator().manual_seed(tensor_seed("grpo", seed))
+    ptr = [0]
+    for n in lengths:
+        ptr.append(ptr[-1] + int(n))
+    T = ptr[-1]
+    pick = torch.randint(0, 3, (len(lengths),), generator=gen)
+    reward = torch.tensor([0.0, 0.2, 1.0])[pick]
+    logp = -2.0 + torch.randn(T, generator=gen)
+    old = logp + logp_noise * torch.randn(T, generator=gen)
+    ref = logp + ref_noise * torch.randn(T, generator=gen)
+    mask = (torch.rand(T, generator=gen) < mask_frac).to(torch.uint8)
+    return (torch.tensor(ptr, dtype=torch.int32), reward.float(), logp.float(), old.float(),
+            ref.float(), mask)
+
