@@ -30,7 +30,9 @@ namespace mv {
 namespace {
 constexpr int BA = 256, BT = 256, BKK = 64;
 constexpr int PAD = BKK + 8;               // LDS row stride (bf16), conflict-free operand reads
-constexpr int WPAD = BA + 16;              // row stride of the row-major W slice of the dH pass
+// row stride of the row-major W slice of the dH pass: 576 bytes, so the four
+// rows one transposing read touches start 16 banks apart
+constexpr int WPAD = BA + 32;
 constexpr int STAGE = (BA + BT) * PAD;     // one k slice of both operands
 static_assert(BKK * WPAD <= BA * PAD, "dH pass W slice must fit the A region");
 constexpr int NWAVES = 8;                 // waves per tile (2 x NWAVES/2 grid)
@@ -55,6 +57,7 @@ struct LmArgs {
   float2* part;       // [T, n_chunks] (logits mode)
   float* tlogit;      // [T] (logits mode)
   // KL modes: token row 2i is leaf i's teacher row, 2i + 1 its student row
+  const u16* zero_row; // [H] zeros: the row read for an out-of-range leaf row index
   const u16* hT;      // teacher hidden states [*, H]
   const u16* hS;      // student hidden states [*, H]
   const int32_t* rowsT;
@@ -109,7 +112,11 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
   const int a_rows = (MODE == kModeDh) ? a.H : a.V;
   const int kbeg = (MODE == kModeDh) ? split * a.nk_split : 0;
   const int nk = (MODE == kModeDh) ? min(K / BKK - kbeg, a.nk_split) : K / BKK;
-  // tiles wholly inside the operands skip the per-load bounds checks
+  // Out-of-range operand rows and columns are read from clamped (valid)
+  // addresses instead of being masked, so loads never wait on a select: the
+  // products they feed land in output rows, columns or vocabulary padding that
+  // the epilogues skip or zero (and padding columns of G are stored as zero).
+  // Tiles wholly inside the operands skip even the clamping.
   const bool interior = (t0 + BT <= a.T) && (MODE == kModeDh ? (a0 + BA <= a.H) : (a0 + BA <= a_rows));
 
   f32x16 acc[4][NJ];
@@ -122,12 +129,10 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
 
   // each thread's token rows are fixed across k slices: resolve them once
   const u16* brow[LDB];
-  bool bok[LDB];
 #pragma unroll
   for (int r = 0; r < LDB; ++r) {
     const int t = t0 + (tid + r * NT) / (BKK / 8);
-    bok[r] = interior || t < a.T;
-    const int tc = bok[r] ? t : 0;
+    const int tc = (interior || t < a.T) ? t : 0;
     if (MODE == kModeDh) {
       brow[r] = a.G + size_t(tc) * a.Vp;
     } else if (MODE == kModeKL || MODE == kModeKLGrad) {
@@ -135,8 +140,7 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
       const int row = (tc & 1) ? a.rowsS[tc >> 1] : a.rowsT[tc >> 1];
       const int n_rows = (tc & 1) ? a.n_rows_S : a.n_rows_T;
       const bool row_ok = row >= 0 && row < n_rows;
-      bok[r] = bok[r] && row_ok;
-      brow[r] = ((tc & 1) ? a.hS : a.hT) + size_t(row_ok ? row : 0) * a.H;
+      brow[r] = row_ok ? ((tc & 1) ? a.hS : a.hT) + size_t(row) * a.H : a.zero_row;
     } else {
       brow[r] = a.h + size_t(tc) * a.H;
     }
@@ -144,7 +148,6 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
 
   uint4 ra[LDA], rb[LDB];
   auto load = [&](int k0) {
-    const uint4 z = make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int r = 0; r < LDA; ++r) {
       const int idx = tid + r * NT;
@@ -153,19 +156,19 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
         // operand is read across its rows with the transposing LDS read
         const int row = idx / (BA / 8), cc = (idx % (BA / 8)) * 8;
         const int v = k0 + row;
-        const u16* p = a.w + size_t(v) * a.H + a0 + cc;
-        ra[r] = (interior && v < a.V) || (v < a.V && a0 + cc < a.H) ? ld16(p) : z;
+        const u16* p = a.w + size_t(min(v, a.V - 1)) * a.H + min(a0 + cc, a.H - 8);
+        ra[r] = ld16(p);
       } else {
         const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
         const int v = a0 + row;
-        const u16* p = a.w + size_t(v) * a.H + k0 + cc;
-        ra[r] = (interior || v < a_rows) ? ld16(p) : z;
+        const u16* p = a.w + size_t(min(v, a_rows - 1)) * a.H + k0 + cc;
+        ra[r] = ld16(p);
       }
     }
 #pragma unroll
     for (int r = 0; r < LDB; ++r) {
       const int cc = ((tid + r * NT) % (BKK / 8)) * 8;
-      rb[r] = bok[r] ? ld16(brow[r] + k0 + cc) : z;
+      rb[r] = ld16(brow[r] + k0 + cc);
     }
   };
   auto store = [&](u16* sA) {
@@ -198,6 +201,13 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
   for (int kk = 0; kk < nk; ++kk) {
     const u16* sA = smem + (kk & 1) * STAGE;
     const u16* sB = sA + BA * PAD;
+    // The next slice goes to the other buffer first (every wave finished
+    // reading it before the last barrier), then the slice after it is
+    // requested from HBM, so both overlap this slice's MFMAs.
+    if (kk + 1 < nk) {
+      store(smem + ((kk + 1) & 1) * STAGE);
+      if (kk + 2 < nk) load((kbeg + kk + 2) * BKK);
+    }
 #pragma unroll
     for (int ks = 0; ks < BKK / 16; ++ks) {
       bf16x8 af[4], bf[NJ];
@@ -213,10 +223,6 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
-    }
-    if (kk + 1 < nk) {
-      store(smem + ((kk + 1) & 1) * STAGE);
-      if (kk + 2 < nk) load((kbeg + kk + 2) * BKK);
     }
     __syncthreads();
   }
@@ -483,14 +489,25 @@ static size_t dh_part_bytes(int T, int H) {
 }
 
 size_t kl_fwd_ws_bytes(int n, int H, int V) {
-  (void)H;
   const int n_chunks = vocab_pad(V) / 128;
   return align256(size_t(n) * n_chunks * sizeof(float4)) +
-         align256(size_t(n) * n_chunks * sizeof(float2)) + 256;
+         align256(size_t(n) * n_chunks * sizeof(float2)) + align256(size_t(H) * sizeof(u16)) +
+         256;
 }
 
 size_t kl_bwd_ws_bytes(int n, int H, int V) {
-  return align256(size_t(n) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(n, H) + 256;
+  return align256(size_t(n) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(n, H) +
+         align256(size_t(H) * sizeof(u16)) + 256;
+}
+
+__global__ __launch_bounds__(256) void zero_u16_kernel(u16* p, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+static hipError_t zero_row(u16* p, int H, hipStream_t stream) {
+  hipLaunchKernelGGL(zero_u16_kernel, dim3((H + 255) / 256), dim3(256), 0, stream, p, H);
+  return hipGetLastError();
 }
 
 size_t logprob_fwd_ws_bytes(int T, int H, int V) {
@@ -644,6 +661,10 @@ hipError_t launch_kl_fwd(int n, int H, int V, const void* hT, int nT, const int3
   char* base = align_ptr(ws);
   a.partT = reinterpret_cast<float4*>(base);
   a.partS = reinterpret_cast<float2*>(base + align256(size_t(n) * a.n_chunks * sizeof(float4)));
+  u16* zrow = reinterpret_cast<u16*>(base + align256(size_t(n) * a.n_chunks * sizeof(float4)) +
+                                     align256(size_t(n) * a.n_chunks * sizeof(float2)));
+  a.zero_row = zrow;
+  if (hipError_t e = zero_row(zrow, H, stream); e != hipSuccess) return e;
   a.nA = a.Vp / BA;
   a.nT = (a.T + BT - 1) / BT;
   {
@@ -683,6 +704,11 @@ hipError_t launch_kl_bwd(int n, int H, int V, const void* hT, int nT, const int3
   a.Gout = G;
   a.nA = a.Vp / BA;
   a.nT = (a.T + BT - 1) / BT;
+  u16* zrow = reinterpret_cast<u16*>(reinterpret_cast<char*>(G) +
+                                     align256(size_t(n) * a.Vp * sizeof(u16)) +
+                                     dh_part_bytes(n, H));
+  a.zero_row = zrow;
+  if (hipError_t e = zero_row(zrow, H, stream); e != hipSuccess) return e;
   {
     ProfScope p("kl_grad", stream);
     hipLaunchKernelGGL((lm_gemm_kernel<kModeKLGrad, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
