@@ -69,7 +69,7 @@ template <int D>
 __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
   constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
   constexpr int KS = D / 16, DB = D / 32;
-  constexpr int RPAD = D + 8;
+  constexpr int RPAD = D + 48;
   constexpr int RLD = BK * D / 8 / 256;          // row-major K and V loads per thread
 
   __shared__ __align__(16) u16 sK[BK * RPAD];
@@ -218,7 +218,7 @@ template <int D>
 __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   constexpr int BK = kBwdTileK, BQ = kBwdBlockQ;
   constexpr int KS = D / 16, DB = D / 32;
-  constexpr int RPAD = D + 8;
+  constexpr int RPAD = D + 48;
   constexpr int RLD = BQ * (D / 8) / 256;  // 16-byte row loads per thread per tensor
 
   // Q and dO blocks are staged row-major only; their transposed operands are

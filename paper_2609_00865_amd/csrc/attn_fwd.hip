@@ -32,7 +32,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   constexpr int KS = D / 16;          // MFMA k-steps over the head dimension
   constexpr int DB = D / 32;          // 32-row blocks of O^T
   constexpr int KPAD = D + 8;         // K row stride (bf16): row reads across 32 lanes hit distinct banks
-  constexpr int VPAD = D + 16;        // V row stride: the 4 rows of a transposing read hit distinct banks
+  constexpr int VPAD = D + 32;        // V row stride: the 4 rows of a transposing read hit distinct banks
   constexpr int KLD = BK * D / 8 / 256;        // 16-byte K (and V) loads per thread
   static_assert(KLD >= 1, "tile too small for 256 threads");
 

@@ -80,7 +80,7 @@ struct LmArgs {
 template <int MODE, int NW>
 __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
   constexpr int NT = NW * 64;              // threads
-  constexpr int WTOK = 256 / (NW / 2);     // tokens per wave (2 waves along the A side)
+  constexpr int WTOK = BT / (NW / 2);      // tokens per wave (2 waves along the A side)
   constexpr int NJ = WTOK / 32;            // 32-token MFMA blocks per wave
   constexpr int LDA = (BA * BKK / 8) / NT; // 16-byte loads per thread, A slice
   constexpr int LDB = (BT * BKK / 8) / NT; // 16-byte loads per thread, token slice
