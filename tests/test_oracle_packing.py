@@ -1,0 +1,148 @@
+"""Pins of the branch-replicated packing oracle (CPU only).
+
+The running example's packed segments against Table "running-prefixes"; the
+packed length identity of Appendix G; owner rows covering each physical row
+once, at the position the token had in its live context; the block-diagonal
+mask reproducing every view; RoPE against its complex-product form, a hand
+example, norm preservation and the relative-position property; multi-layer
+exactness of the packed stream against per-branch forwards, with the union
+form failing under RoPE at any depth and without positions from the second
+layer on (the reason the paper's training loop packs)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as OA
+from oracle import packing as OP
+from oracle import views as V
+from paper_2609_00865_amd import synth
+from tests.fixtures import load, trajectory_from
+
+F64 = torch.float64
+
+
+def test_running_example_segments():
+    fix = load("running_example.json")
+    traj, pos = trajectory_from(fix)
+    names = {i: n for n, i in pos.items()}
+    pk = OP.branch_pack([traj])
+    assert len(pk["seg_begin"]) - 1 == 4            # K + 1 branch layers
+    assert pk["seg_begin"][-1] == 7 + 9 + 10 + 11
+    # each leaf's decoding row r = t - 1 sits in one segment; the segment's
+    # prefix up to that slot is the live prefix the table lists (plus s)
+    for e in fix["leaves"]:
+        r = pos[e["leaf"]] - 1
+        slot = [i for i in range(len(pk["src"])) if pk["src"][i] == r and pk["owner"][i]]
+        assert len(slot) == 1
+        slot = slot[0]
+        b = max(x for x in pk["seg_begin"] if x <= slot)
+        seq = [names[j] for j in pk["src"][b:slot + 1] if j != pos["s"]]
+        assert seq == e["live"]
+        assert pk["pos"][slot] == len(e["live"])        # s at position 0
+        assert pk["target"][slot] == pos[e["leaf"]]
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_layout_properties(seed):
+    rng = np.random.default_rng(3000 + seed)
+    lens = [int(x) for x in rng.integers(1, 200, size=int(rng.integers(1, 4)))]
+    trajs = synth.random_trajectories(rng, lens, max_edits=6, max_span=30, summary_max=8)
+    T = trajs[-1].end
+    pk = OP.branch_pack(trajs)
+    N = pk["seg_begin"][-1]
+    assert N == sum(len(b) + (e - f) for tr in trajs for f, e, b in V.branch_layers(tr))
+    assert N >= T
+    own = [s for s, o in zip(pk["src"], pk["owner"]) if o]
+    assert sorted(own) == list(range(T))               # every row owned exactly once
+    M = OA.visibility(trajs)
+    B = OP.block_causal_mask(pk["seg_begin"])
+    src = torch.tensor(pk["src"])
+    sizes = {tr_r: s for tr in trajs for tr_r, s in zip(range(tr.begin, tr.end), V.view_sizes(tr))}
+    for i in range(N):
+        if not pk["owner"][i]:
+            continue
+        r = pk["src"][i]
+        seen = torch.zeros(T, dtype=torch.bool)
+        seen[src[B[i]]] = True
+        assert torch.equal(seen, M[r])                 # the packed row sees exactly View(r)
+        assert pk["pos"][i] == sizes[r] - 1            # gap-free logical position
+
+
+def test_rope_forms_and_properties():
+    gen = torch.Generator().manual_seed(0)
+    x = torch.randn(50, 3, 16, generator=gen, dtype=F64)
+    pos = torch.randint(0, 40000, (50,), generator=gen)
+    a = OP.rope(x, pos, 1e6)
+    assert torch.allclose(a, OP.rope_complex(x, pos, 1e6), atol=1e-12)
+    assert torch.allclose(OP.rope(x, torch.zeros(50), 1e6), x)
+    assert torch.allclose(a.norm(dim=-1), x.norm(dim=-1), atol=1e-12)
+    assert torch.allclose(OP.rope(a, pos, 1e6, inverse=True), x, atol=1e-10)
+    # <R(m) q, R(n) k> = <R(m - n) q, k>
+    q, k = x[:25], x[25:]
+    m, n = pos[:25], pos[25:]
+    lhs = (OP.rope(q, m, 1e4) * OP.rope(k, n, 1e4)).sum(-1)
+    rhs = (OP.rope(q, m - n, 1e4) * k).sum(-1)
+    assert torch.allclose(lhs, rhs, atol=1e-9)
+    # hand example: d = 4, theta = 100, position 1: frequencies 1 and 0.1
+    v = torch.tensor([[[1.0, 2.0, 3.0, 4.0]]], dtype=F64)
+    got = OP.rope(v, [1], 100.0)[0, 0]
+    c1, s1, c2, s2 = math.cos(1), math.sin(1), math.cos(0.1), math.sin(0.1)
+    want = [1 * c1 - 3 * s1, 2 * c2 - 4 * s2, 3 * c1 + 1 * s1, 4 * c2 + 2 * s2]
+    assert torch.allclose(got, torch.tensor(want, dtype=F64), atol=1e-14)
+
+
+def _toy(seed, W, H, n_layers):
+    gen = torch.Generator().manual_seed(seed)
+    d = W // H
+    return [{"wq": torch.randn(W, W, generator=gen, dtype=F64) / math.sqrt(W),
+             "wk": torch.randn(W, W, generator=gen, dtype=F64) / math.sqrt(W),
+             "wv": torch.randn(W, W, generator=gen, dtype=F64) / math.sqrt(W),
+             "wo": torch.randn(W, W, generator=gen, dtype=F64) / math.sqrt(W)}
+            for _ in range(n_layers)], d
+
+
+@pytest.mark.parametrize("n_layers", [1, 2, 3])
+def test_packed_stream_is_exact_over_layers(n_layers):
+    traj, _ = trajectory_from(load("running_example.json"))
+    rng = np.random.default_rng(7)
+    trajs = [traj] + synth.random_trajectories(rng, [90], max_edits=4, max_span=12)
+    trajs[1] = synth.Trajectory(14, 14 + 90, tuple(
+        synth.Edit(e.junction + 14, tuple((b + 14, x + 14) for b, x in e.evict),
+                   (e.summary[0] + 14, e.summary[1] + 14)) for e in trajs[1].edits))
+    T = trajs[-1].end
+    W, H = 16, 2
+    layers, d = _toy(n_layers, W, H, n_layers)
+    x0 = torch.randn(T, W, generator=torch.Generator().manual_seed(1), dtype=F64)
+    ref = OP.toy_logittree(trajs, x0, layers, H, d, 1e4)
+    got = OP.toy_packed(trajs, x0, layers, H, d, 1e4)
+    assert torch.allclose(got, ref, atol=1e-10)
+    # The union form: one position per token cannot be right for every row
+    # (a key's index in a later row's view shifts once a span before it is
+    # evicted), so with RoPE it misses even one layer; without positions it
+    # matches one layer and misses a stack (keys past an evicted span carry
+    # hidden states computed with the span visible).
+    logical = [s - 1 for tr in trajs for s in V.view_sizes(tr)]
+    uni = OP.toy_union(trajs, x0, layers, H, d, 1e4, positions=logical)
+    assert float((uni - ref).abs().max()) > 1e-3
+    ref0 = OP.toy_logittree(trajs, x0, layers, H, d, 0.0)
+    assert torch.allclose(OP.toy_packed(trajs, x0, layers, H, d, 0.0), ref0, atol=1e-10)
+    err0 = float((OP.toy_union(trajs, x0, layers, H, d, 0.0) - ref0).abs().max())
+    if n_layers == 1:
+        assert err0 < 1e-10
+    else:
+        assert err0 > 1e-3
+
+
+def test_unpack_is_the_adjoint_of_the_gather():
+    rng = np.random.default_rng(5)
+    trajs = synth.random_trajectories(rng, [120, 80], max_edits=5, max_span=15)
+    pk = OP.branch_pack(trajs)
+    T, N = trajs[-1].end, pk["seg_begin"][-1]
+    gen = torch.Generator().manual_seed(2)
+    x = torch.randn(T, 6, generator=gen, dtype=F64)
+    g = torch.randn(N, 6, generator=gen, dtype=F64)
+    lhs = (x[pk["src"]] * g).sum()
+    rhs = (x * OP.unpack_sum(pk, g, T)).sum()
+    assert abs(float(lhs - rhs)) < 1e-10
