@@ -182,6 +182,72 @@ mv_status mv_view_mask_materialize_host(const mv_view_mask* m, int32_t row_begin
 void mv_view_mask_free(mv_view_mask* m);
 
 /* ---------------------------------------------------------------------------
+ * Branch-replicated packing (Appendix G; the branch layers of Appendix B.1,
+ * forwarded as in Section 4.1) for exact multi-layer scoring.
+ *
+ * Each branch layer k of a trajectory (rows [J_k, J_{k+1})) becomes one
+ * segment of a packed stream: the keys live just before J_k in physical
+ * order, then the layer's rows.  Under the block-diagonal causal mask every
+ * packed row of a layer sees exactly its live view at every depth of a
+ * model, and position ids restart per segment, so every copy carries the
+ * position its token had in the live context (rotary phases match the
+ * rollout).  Per slot: src (physical token copied), pos (index inside its
+ * segment), owner (1 for the layer's own rows, which carry their loss; 0 for
+ * trunk copies), target (the physical row whose token the slot predicts:
+ * src + 1 for owner slots that are not their trajectory's last row, else -1).
+ * The packed length is the sum of the layers' lengths, >= total_tokens.
+ * Host construction is synchronous; the record rules and errors are those of
+ * mv_build_view_mask.
+ * ------------------------------------------------------------------------ */
+typedef struct mv_branch_pack mv_branch_pack;   /* opaque */
+
+typedef struct {
+  int32_t total_tokens;   /* physical rows L                                  */
+  int32_t n_packed;       /* packed slots N                                   */
+  int32_t n_segments;     /* branch layers over all trajectories              */
+  int32_t max_copies;     /* most copies of one physical token                */
+  int64_t causal_pairs;   /* sum over segments of l (l + 1) / 2               */
+} mv_pack_stats;
+
+mv_status mv_build_branch_pack(const mv_trajectory* trajs, int32_t n_traj,
+                               int32_t total_tokens, mv_branch_pack** out);
+mv_status mv_branch_pack_stats(const mv_branch_pack* p, mv_pack_stats* out);
+/* Host copies of the layout; every array is optional (null: skipped).
+ * src, pos, target: int32 [n_packed]; owner: uint8 [n_packed];
+ * seg_begin: int32 [n_segments + 1] (first slot of each segment, then N). */
+mv_status mv_branch_pack_layout(const mv_branch_pack* p, int32_t* src, int32_t* pos,
+                                uint8_t* owner, int32_t* target, int32_t* seg_begin);
+/* The block-diagonal causal mask over the packed stream (each segment a
+ * trajectory without edits), owned by the pack: upload it and pass it to the
+ * attention entry points like any mask; never free it separately. */
+mv_view_mask* mv_branch_pack_mask(mv_branch_pack* p);
+/* Device bytes of the layout arrays (src, pos and the per-token copy lists),
+ * not counting the mask's own buffer. */
+size_t mv_branch_pack_device_bytes(const mv_branch_pack* p);
+/* Copy the layout to a caller-owned device buffer (256-byte aligned) that
+ * must outlive every call using it; as mv_view_mask_upload. */
+mv_status mv_branch_pack_upload(mv_branch_pack* p, void* dev_buf, size_t bytes,
+                                hipStream_t stream);
+void mv_branch_pack_free(mv_branch_pack* p);
+
+/* out[slot, :] = in[src[slot], :]: bf16 rows of `width` elements (width % 8
+ * == 0), in [total_tokens, width], out [n_packed, width]. */
+mv_status mv_pack_rows(const mv_branch_pack* p, const void* in, int32_t width, void* out,
+                       hipStream_t stream);
+/* The adjoint of mv_pack_rows: out[t, :] = sum over the copies of token t, in
+ * increasing slot order, of in[slot, :] (fp32 sums), stored as bf16
+ * (out_fp32 == 0) or fp32.  Deterministic. */
+mv_status mv_unpack_rows_sum(const mv_branch_pack* p, const void* in, int32_t width,
+                             int32_t out_fp32, void* out, hipStream_t stream);
+/* Rotary embedding of x [n_packed, n_heads, head_dim] (bf16) by each slot's
+ * position id: pairs (i, i + head_dim/2) rotate by pos * theta^(-2i/head_dim)
+ * (angles in double precision, rotation in fp32, one rounding to bf16).
+ * direction +1 applies the rotation, -1 its inverse (which is also its
+ * backward).  out may alias x.  head_dim even, <= 256. */
+mv_status mv_rope(const mv_branch_pack* p, const void* x, int32_t n_heads, int32_t head_dim,
+                  float theta, int32_t direction, void* out, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * View-masked attention (Section 4.2, the packed single forward; its
  * equivalence with one causal forward per branch is Theorem "hard_equiv",
  * Section 4.3 and Appendix C.3).
@@ -385,7 +451,8 @@ float mv_sdcc_lambda(int32_t step, int32_t total_steps, float lambda_max, float 
  * the summed duration (ms) and launch count of the kernels named `kernel`
  * (one of "attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce",
  * "attn_bwd_dq", "lm_logits", "lm_combine", "lm_grad", "lm_dh", "kl_logits",
- * "kl_combine", "kl_grad", "kl_dh", "grpo", "materialize", "ppo_clip").  Not for use
+ * "kl_combine", "kl_grad", "kl_dh", "grpo", "pack", "unpack", "rope", "materialize",
+ * "ppo_clip").  Not for use
  * under stream capture.
  * ------------------------------------------------------------------------ */
 mv_status mv_profile_enable(int32_t on);

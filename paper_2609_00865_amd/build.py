@@ -12,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libmv.so")
 SOURCES = ["api.cpp", "mask.cpp", "mask_kernels.hip", "attn_fwd.hip", "attn_bwd.hip",
-           "logprob.hip", "grpo.hip"]
+           "logprob.hip", "grpo.hip", "pack.cpp", "pack.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed-fp32 instructions are disabled for all device code.
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang",

@@ -70,3 +70,30 @@ struct mv_view_mask {
   int device = -1;
   mv_mask_dev d{};
 };
+
+struct mv_branch_pack {
+  int32_t T = 0, N = 0;
+  std::vector<int32_t> src, pos, target, seg_begin;
+  std::vector<uint8_t> owner;
+  std::vector<int32_t> copy_ptr, copy_slot;  // per physical token, its slots in order
+  mv_pack_stats stats{};
+  mv_view_mask* mask = nullptr;              // block-diagonal causal mask, owned
+  // device copy
+  size_t off[4] = {0};
+  size_t bytes = 0;
+  void* dev = nullptr;
+  int device = -1;
+  const int32_t* d_src = nullptr;
+  const int32_t* d_pos = nullptr;
+  const int32_t* d_copy_ptr = nullptr;
+  const int32_t* d_copy_slot = nullptr;
+};
+
+namespace mv {
+hipError_t launch_pack_rows(const mv_branch_pack& p, const void* in, int W, void* out,
+                            hipStream_t stream);
+hipError_t launch_unpack_sum(const mv_branch_pack& p, const void* in, int W, bool out_fp32,
+                             void* out, hipStream_t stream);
+hipError_t launch_rope(const mv_branch_pack& p, const void* x, int H, int d, float theta,
+                       int direction, void* out, hipStream_t stream);
+}  // namespace mv

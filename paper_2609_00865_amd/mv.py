@@ -72,6 +72,15 @@ class LogprobShape(ctypes.Structure):
                 ("eps_high", ctypes.c_float)]
 
 
+class PackStats(ctypes.Structure):
+    _fields_ = [("total_tokens", ctypes.c_int32), ("n_packed", ctypes.c_int32),
+                ("n_segments", ctypes.c_int32), ("max_copies", ctypes.c_int32),
+                ("causal_pairs", ctypes.c_int64)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
 class KLShape(ctypes.Structure):
     _fields_ = [("n_leaves", ctypes.c_int32), ("hidden", ctypes.c_int32),
                 ("vocab", ctypes.c_int32), ("n_rows_teacher", ctypes.c_int32),
@@ -132,6 +141,17 @@ mv_token_logprob_bwd = _sig("mv_token_logprob_bwd", ctypes.c_int, _P(LogprobShap
                             _vp, _vp, _vp, _vp, _vp, _sz, _vp)
 mv_ppo_clip_dlogp = _sig("mv_ppo_clip_dlogp", ctypes.c_int, _i32, _vp, _vp, _f32, _f32, _f32,
                          _vp, _vp)
+mv_build_branch_pack = _sig("mv_build_branch_pack", ctypes.c_int, _P(TrajectoryC), _i32, _i32,
+                            _P(_vp))
+mv_branch_pack_stats = _sig("mv_branch_pack_stats", ctypes.c_int, _vp, _P(PackStats))
+mv_branch_pack_layout = _sig("mv_branch_pack_layout", ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp)
+mv_branch_pack_mask = _sig("mv_branch_pack_mask", _vp, _vp)
+mv_branch_pack_device_bytes = _sig("mv_branch_pack_device_bytes", _sz, _vp)
+mv_branch_pack_upload = _sig("mv_branch_pack_upload", ctypes.c_int, _vp, _vp, _sz, _vp)
+mv_branch_pack_free = _sig("mv_branch_pack_free", None, _vp)
+mv_pack_rows = _sig("mv_pack_rows", ctypes.c_int, _vp, _vp, _i32, _vp, _vp)
+mv_unpack_rows_sum = _sig("mv_unpack_rows_sum", ctypes.c_int, _vp, _vp, _i32, _i32, _vp, _vp)
+mv_rope = _sig("mv_rope", ctypes.c_int, _vp, _vp, _i32, _i32, _f32, _i32, _vp, _vp)
 mv_grpo_loss_workspace_bytes = _sig("mv_grpo_loss_workspace_bytes", _sz, _P(GrpoShape))
 mv_grpo_loss = _sig("mv_grpo_loss", ctypes.c_int, _P(GrpoShape), _vp, _vp, _vp, _vp, _vp, _vp,
                     _vp, _vp, _vp, _vp, _sz, _vp)
@@ -155,7 +175,10 @@ EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_ma
             "mv_token_logprob_bwd_workspace_bytes", "mv_token_logprob_bwd", "mv_ppo_clip_dlogp",
             "mv_build_view_mask_kind", "mv_view_mask_leaves", "mv_sdcc_kl_workspace_bytes",
             "mv_sdcc_kl", "mv_sdcc_kl_bwd_workspace_bytes", "mv_sdcc_kl_bwd", "mv_sdcc_lambda",
-            "mv_grpo_loss_workspace_bytes", "mv_grpo_loss",
+            "mv_grpo_loss_workspace_bytes", "mv_grpo_loss", "mv_build_branch_pack",
+            "mv_branch_pack_stats", "mv_branch_pack_layout", "mv_branch_pack_mask",
+            "mv_branch_pack_device_bytes", "mv_branch_pack_upload", "mv_branch_pack_free",
+            "mv_pack_rows", "mv_unpack_rows_sum", "mv_rope",
             "mv_profile_enable", "mv_profile_read"]
 
 VIEW_LIVE, VIEW_FINAL = 0, 1
@@ -186,38 +209,55 @@ def _aligned_buffer(nbytes: int, device) -> tuple:
 # ---------------------------------------------------------------------------
 # view mask
 # ---------------------------------------------------------------------------
+def _trajectories_c(trajectories: Sequence):
+    """ctypes array of mv_trajectory plus the arrays it points into."""
+    keep = []
+    trajs = (TrajectoryC * len(trajectories))()
+    for ti, t in enumerate(trajectories):
+        edits = (EditC * max(1, len(t.edits)))()
+        for ei, e in enumerate(t.edits):
+            spans = (Span * max(1, len(e.evict)))()
+            for si, (b, x) in enumerate(e.evict):
+                spans[si] = Span(int(b), int(x))
+            keep.append(spans)
+            summ = getattr(e, "summary", (0, 0))
+            edits[ei] = EditC(int(e.junction), len(e.evict), spans,
+                              Span(int(summ[0]), int(summ[1])))
+        keep.append(edits)
+        trajs[ti] = TrajectoryC(int(t.begin), int(t.end), len(t.edits), edits)
+    return trajs, keep
+
 class ViewMask:
     """Owns a libmv mask object built from trajectories (host), optionally uploaded."""
 
     def __init__(self, trajectories: Sequence, total_tokens: Optional[int] = None,
                  kind: int = 0):
-        keep = []
-        trajs = (TrajectoryC * len(trajectories))()
-        for ti, t in enumerate(trajectories):
-            edits = (EditC * max(1, len(t.edits)))()
-            for ei, e in enumerate(t.edits):
-                spans = (Span * max(1, len(e.evict)))()
-                for si, (b, x) in enumerate(e.evict):
-                    spans[si] = Span(int(b), int(x))
-                keep.append(spans)
-                summ = getattr(e, "summary", (0, 0))
-                edits[ei] = EditC(int(e.junction), len(e.evict), spans,
-                                  Span(int(summ[0]), int(summ[1])))
-            keep.append(edits)
-            trajs[ti] = TrajectoryC(int(t.begin), int(t.end), len(t.edits), edits)
+        trajs, keep = _trajectories_c(trajectories)
         T = total_tokens if total_tokens is not None else int(trajectories[-1].end)
         handle = ctypes.c_void_p()
         check(mv_build_view_mask_kind(trajs, len(trajectories), T, int(kind),
                                       ctypes.byref(handle)))
         self._h = handle
+        self._owned = True
         self.total_tokens = T
         self._dev = None
 
+    @classmethod
+    def _borrowed(cls, handle, total_tokens: int, owner) -> "ViewMask":
+        """A mask owned by another library object (kept alive through `owner`)."""
+        m = cls.__new__(cls)
+        m._h = ctypes.c_void_p(handle)
+        m._owned = False
+        m._owner = owner
+        m.total_tokens = total_tokens
+        m._dev = None
+        return m
+
     def __del__(self, _free=mv_view_mask_free):
         h = getattr(self, "_h", None)
-        if h is not None and h.value:
+        if h is not None and h.value and getattr(self, "_owned", False):
             _free(h)
-            self._h = None
+        self._h = None
 
     @property
     def handle(self):
@@ -373,6 +413,89 @@ def ppo_clip_dlogp(ratio, adv, eps_low=0.2, eps_high=0.2, scale=1.0, stream=None
 
 
 # ---------------------------------------------------------------------------
+# branch-replicated packing
+# ---------------------------------------------------------------------------
+class BranchPack:
+    """Owns a libmv branch packing built from trajectories."""
+
+    def __init__(self, trajectories: Sequence, total_tokens: Optional[int] = None):
+        trajs, keep = _trajectories_c(trajectories)
+        T = total_tokens if total_tokens is not None else int(trajectories[-1].end)
+        handle = ctypes.c_void_p()
+        check(mv_build_branch_pack(trajs, len(trajectories), T, ctypes.byref(handle)))
+        self._h = handle
+        self.total_tokens = T
+        st = self.stats()
+        self.n_packed = st["n_packed"]
+        self.n_segments = st["n_segments"]
+        self.mask = ViewMask._borrowed(mv_branch_pack_mask(handle), self.n_packed, self)
+        self._dev = None
+
+    def __del__(self, _free=mv_branch_pack_free):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            _free(h)
+            self._h = None
+
+    def stats(self) -> dict:
+        s = PackStats()
+        check(mv_branch_pack_stats(self._h, ctypes.byref(s)))
+        return s.as_dict()
+
+    def layout(self) -> dict:
+        N = self.n_packed
+        out = {"src": torch.empty(N, dtype=torch.int32), "pos": torch.empty(N, dtype=torch.int32),
+               "owner": torch.empty(N, dtype=torch.uint8),
+               "target": torch.empty(N, dtype=torch.int32),
+               "seg_begin": torch.empty(self.n_segments + 1, dtype=torch.int32)}
+        check(mv_branch_pack_layout(self._h, _ptr(out["src"]), _ptr(out["pos"]),
+                                    _ptr(out["owner"]), _ptr(out["target"]),
+                                    _ptr(out["seg_begin"])))
+        return out
+
+    def upload(self, device="cuda", stream=None) -> "BranchPack":
+        n = int(mv_branch_pack_device_bytes(self._h))
+        buf, addr = _aligned_buffer(n, device)
+        check(mv_branch_pack_upload(self._h, ctypes.c_void_p(addr), n, _stream(stream)))
+        self._dev = buf
+        self.mask.upload(device, stream)
+        return self
+
+    @property
+    def handle(self):
+        return self._h
+
+
+def pack_rows(pack: BranchPack, x, stream=None):
+    """x [T, ...] bf16 -> [n_packed, ...] gathered by each slot's physical token."""
+    _need_bf16_cuda(x)
+    W = x[0].numel()
+    out = torch.empty((pack.n_packed,) + tuple(x.shape[1:]), dtype=x.dtype, device=x.device)
+    check(mv_pack_rows(pack.handle, _ptr(x), W, _ptr(out), _stream(stream)))
+    return out
+
+
+def unpack_rows_sum(pack: BranchPack, g, out_fp32: bool = False, stream=None):
+    """g [n_packed, ...] bf16 -> [T, ...]: each token's copies summed (fp32 accumulation)."""
+    _need_bf16_cuda(g)
+    W = g[0].numel()
+    out = torch.empty((pack.total_tokens,) + tuple(g.shape[1:]),
+                      dtype=torch.float32 if out_fp32 else g.dtype, device=g.device)
+    check(mv_unpack_rows_sum(pack.handle, _ptr(g), W, 1 if out_fp32 else 0, _ptr(out),
+                             _stream(stream)))
+    return out
+
+
+def rope(pack: BranchPack, x, theta: float = 1e6, inverse: bool = False, out=None, stream=None):
+    """Rotary embedding of x [n_packed, H, d] bf16 by each slot's position id."""
+    _need_bf16_cuda(x)
+    out = torch.empty_like(x) if out is None else out
+    check(mv_rope(pack.handle, _ptr(x), x.shape[1], x.shape[2], float(theta),
+                  -1 if inverse else 1, _ptr(out), _stream(stream)))
+    return out
+
+
+# ---------------------------------------------------------------------------
 # GRPO loss and drift diagnostics
 # ---------------------------------------------------------------------------
 def grpo_loss(traj_ptr, reward, logp, logp_old, logp_ref=None, loss_mask=None, group_size=16,
@@ -453,7 +576,7 @@ def sdcc_lambda(step: int, total_steps: int, lambda_max: float = 0.1,
 # ---------------------------------------------------------------------------
 KERNELS = ["attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq",
            "lm_logits", "lm_combine", "lm_grad", "lm_dh", "kl_logits", "kl_combine", "kl_grad", "kl_dh",
-           "grpo",
+           "grpo", "pack", "unpack", "rope",
            "materialize", "ppo_clip"]
 
 

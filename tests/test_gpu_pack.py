@@ -1,0 +1,143 @@
+"""GPU parity of the branch-replicated packing (gather, its adjoint, rotary
+embedding by per-segment positions) and of attention over the packed stream,
+against the oracle, through the C ABI; plus a two-layer model run on the
+packed stream against per-branch forwards of the whole stack.
+
+Gates: the gather is bit-exact; fp32 sums of the copies 1e-6 relative; bf16
+outputs as everywhere else (2e-2 + 2^-8 |ref| elementwise, 1e-2 relative
+Frobenius); the rotation is computed in fp32 from exact angles, so its error
+beyond the final bf16 rounding stays below 1e-5 x max|x|.  The two-layer
+model keeps bf16 activations between layers (as a bf16 model does): its gate
+is a relative Frobenius error of 2e-2, and the union form must miss it by far.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as OA
+from oracle import packing as OP
+from paper_2609_00865_amd import mv, synth
+from tests.parity import assert_bf16_close, errors
+
+pytestmark = pytest.mark.gpu
+F64 = torch.float64
+BF = torch.bfloat16
+
+
+def _records(seed, lens=(300, 257, 180)):
+    rng = np.random.default_rng(seed)
+    return synth.random_trajectories(rng, list(lens), max_edits=6, max_span=40, summary_max=12)
+
+
+def test_pack_and_unpack():
+    trajs = _records(1)
+    pk = mv.BranchPack(trajs).upload()
+    lay = OP.branch_pack(trajs)
+    T, N = trajs[-1].end, pk.n_packed
+    print(f"[gpu] pack rows T={T} N={N}", flush=True)
+    gen = torch.Generator().manual_seed(3)
+    x = torch.randn(T, 3, 64, generator=gen).to(BF)
+    got = mv.pack_rows(pk, x.cuda()).cpu()
+    assert torch.equal(got, x[lay["src"]])
+    g = torch.randn(N, 3, 64, generator=gen).to(BF)
+    ref = OP.unpack_sum(lay, g, T)
+    s32 = mv.unpack_rows_sum(pk, g.cuda(), out_fp32=True).cpu()
+    s16 = mv.unpack_rows_sum(pk, g.cuda()).cpu()
+    torch.cuda.synchronize()
+    rel = float(((s32.double() - ref).abs() / ref.abs().clamp(min=1e-3)).max())
+    assert rel < 1e-6, rel
+    assert_bf16_close(s16, ref, "unpack bf16")
+
+
+@pytest.mark.parametrize("d,theta", [(64, 1e4), (128, 1e6)])
+def test_rope(d, theta):
+    trajs = _records(2, lens=(900, 400))
+    pk = mv.BranchPack(trajs).upload()
+    lay = OP.branch_pack(trajs)
+    N = pk.n_packed
+    print(f"[gpu] rope N={N} d={d}", flush=True)
+    gen = torch.Generator().manual_seed(4)
+    x = torch.randn(N, 4, d, generator=gen).to(BF)
+    xd = x.cuda()
+    y = mv.rope(pk, xd, theta).cpu()
+    back = mv.rope(pk, y.cuda(), theta, inverse=True).cpu()
+    inplace = xd.clone()
+    mv.rope(pk, inplace, theta, out=inplace)
+    torch.cuda.synchronize()
+    ref = OP.rope(x, lay["pos"], theta)
+    excess = float(((y.double() - ref).abs() - 2.0 ** -8 * ref.abs()).max())
+    assert excess <= 1e-5 * float(x.abs().max()), excess
+    assert torch.equal(inplace.cpu(), y)
+    assert_bf16_close(back, x.double(), "rope round trip")
+
+
+def test_packed_attention_forward_backward():
+    """One layer over the packed stream: owner rows give every row's view
+    output; the copies' gradients summed back give the per-branch dK, dV."""
+    trajs = synth.make_trajectories("tiny", 0)
+    q, k, v, do = synth.make_attn_tensors("tiny", 0)
+    q = q.repeat(1, 2, 1).contiguous()
+    do = do.repeat(1, 2, 1).contiguous()
+    pk = mv.BranchPack(trajs).upload()
+    lay = pk.layout()
+    own = lay["owner"].bool()
+    print(f"[gpu] packed attention T={q.shape[0]} N={pk.n_packed}", flush=True)
+    qp, kp, vp = (mv.pack_rows(pk, x.cuda()) for x in (q, k, v))
+    dop = mv.pack_rows(pk, do.cuda())
+    dop[~own.cuda()] = 0                       # only a row's own copy carries its loss
+    o, lse = mv.attn_fwd(pk.mask, qp, kp, vp)
+    dq, dk, dv = mv.attn_bwd(pk.mask, qp, kp, vp, o, dop, lse)
+    dK = mv.unpack_rows_sum(pk, dk, out_fp32=True).cpu()
+    dV = mv.unpack_rows_sum(pk, dv, out_fp32=True).cpu()
+    torch.cuda.synchronize()
+    O, L, dQ, rdK, rdV = OA.logittree(trajs, q.to(F64), k.to(F64), v.to(F64), dout=do.to(F64))
+    src = lay["src"].long()
+    o_own = torch.zeros_like(O)
+    o_own[src[own]] = o.cpu()[own].double()
+    assert_bf16_close(o_own, O, "packed O (owner rows)")
+    dq_own = torch.zeros_like(dQ)
+    dq_own[src[own]] = dq.cpu()[own].double()
+    assert_bf16_close(dq_own, dQ, "packed dQ (owner rows)")
+    # summed over copies: a bf16 rounding per copy, then fp32 sums
+    assert_bf16_close(dK, rdK, "packed dK summed over copies")
+    assert_bf16_close(dV, rdV, "packed dV summed over copies")
+
+
+def _bf(x):
+    return x.to(BF)
+
+
+def test_two_layer_model_on_the_packed_stream():
+    trajs = synth.make_trajectories("tiny", 1)
+    T = trajs[-1].end
+    W, H, d, theta, n_layers = 128, 2, 64, 1e4, 2
+    gen = torch.Generator().manual_seed(11)
+    layers = [{n: _bf(torch.randn(W, W, generator=gen) / math.sqrt(W)).double()
+               for n in ("wq", "wk", "wv", "wo")} for _ in range(n_layers)]
+    x0 = _bf(torch.randn(T, W, generator=gen)).double()
+    ref = OP.toy_logittree(trajs, x0, layers, H, d, theta)
+    uni = OP.toy_union(trajs, x0, layers, H, d, theta)
+    pk = mv.BranchPack(trajs).upload()
+    print(f"[gpu] two-layer model T={T} N={pk.n_packed}", flush=True)
+    x = mv.pack_rows(pk, _bf(x0).cuda())
+    for prm in layers:
+        w = {n: t.float().cuda() for n, t in prm.items()}
+        xf = x.float()
+        q = _bf(xf @ w["wq"]).reshape(-1, H, d).contiguous()
+        k = _bf(xf @ w["wk"]).reshape(-1, H, d).contiguous()
+        v = _bf(xf @ w["wv"]).reshape(-1, H, d).contiguous()
+        q, k = mv.rope(pk, q, theta), mv.rope(pk, k, theta)
+        o, _ = mv.attn_fwd(pk.mask, q, k, v)
+        x = _bf(xf + o.float().reshape(-1, W) @ w["wo"])
+    torch.cuda.synchronize()
+    lay = pk.layout()
+    own = lay["owner"].bool()
+    got = torch.zeros(T, W, dtype=F64)
+    got[lay["src"].long()[own]] = x.cpu()[own].double()
+    _, rel, _ = errors(got, ref)
+    _, rel_uni, _ = errors(uni, ref)
+    print(f"two-layer: packed rel_fro={rel:.3e}  union-form rel_fro={rel_uni:.3e}", flush=True)
+    assert rel <= 2e-2
+    assert rel_uni >= 10 * rel
