@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-sdcc", action="store_true",
                     help="skip the separately timed SDCC junction-KL pass")
+    ap.add_argument("--no-packed", action="store_true",
+                    help="skip the separately timed branch-replicated attention layer")
     return ap.parse_args()
 
 
@@ -201,6 +203,65 @@ def time_sdcc(args, mv, synth, mask, wl, lmw, dev):
     }
 
 
+def time_packed(args, mv, synth, trajs, wl, dev):
+    """One exact attention layer on the branch-replicated packed stream of the
+    same batch (the form that stays exact through a stack of layers): rotary
+    embedding of Q and K by per-branch positions, attention forward and
+    backward under the block-diagonal mask, the inverse rotation of dQ and dK.
+    Timed on its own after the step; useful FLOPs 14 d P Hq with P the packed
+    stream's causal pairs."""
+    import torch
+    pk = mv.BranchPack(trajs).upload(dev)
+    st = pk.stats()
+    N = st["n_packed"]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(synth.tensor_seed("packed", args.seed))
+    mk = lambda h: torch.randn((N, h, wl.head_dim), generator=gen, device="cuda").to(torch.bfloat16)
+    q, k, v, do = mk(wl.n_heads_q), mk(wl.n_heads_kv), mk(wl.n_heads_kv), mk(wl.n_heads_q)
+    ws = mv.attn_bwd_workspace(pk.mask, q, k)
+    qr, kr = torch.empty_like(q), torch.empty_like(k)
+
+    def layer():
+        mv.rope(pk, q, 1e6, out=qr)
+        mv.rope(pk, k, 1e6, out=kr)
+        o, lse = mv.attn_fwd(pk.mask, qr, kr, v)
+        dq, dk, dv = mv.attn_bwd(pk.mask, qr, kr, v, o, do, lse, workspace=ws)
+        mv.rope(pk, dq, 1e6, inverse=True, out=dq)
+        mv.rope(pk, dk, 1e6, inverse=True, out=dk)
+
+    for _ in range(args.warmup):
+        layer()
+    torch.cuda.synchronize()
+    mv.profile_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    stream = torch.cuda.current_stream()
+    e0.record(stream)
+    for _ in range(args.steps):
+        layer()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    kt = {}
+    for name in ("rope", "attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce",
+                 "attn_bwd_dq"):
+        tot, cnt = mv.profile_read(name)
+        if cnt:
+            kt[name] = round(tot / cnt, 3)
+    mv.profile_enable(False)
+    useful = 14.0 * wl.head_dim * st["causal_pairs"] * wl.n_heads_q
+    tflops = useful / (ms * 1e-3) / 1e12
+    log(f"packed stream: N={N}, {ms:.2f} ms per exact layer fwd+bwd, {tflops:.0f} TFLOP/s")
+    return {
+        "n_packed": N,
+        "segments": st["n_segments"],
+        "causal_pairs": st["causal_pairs"],
+        "ms": round(ms, 3),
+        "useful_tflops": round(tflops, 2),
+        "frac_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "kernels_ms": kt,
+    }
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -276,6 +337,7 @@ def main():
     mv.profile_enable(False)
     log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step (host wall {wall_ms:.2f})")
     sdcc = None if args.no_sdcc else time_sdcc(args, mv, synth, mask, wl, lmw, dev)
+    packed = None if args.no_packed else time_packed(args, mv, synth, trajs, wl, dev)
 
     d, hq = wl.head_dim, wl.n_heads_q
     T_lm, H, V = lmw.n_tokens, lmw.hidden, lmw.vocab
@@ -345,6 +407,10 @@ def main():
     }
     if sdcc is not None:
         out["sdcc"] = sdcc
+    if packed is not None:
+        packed["pairs_vs_union"] = round(packed["causal_pairs"] / P, 4)
+        packed["ms_vs_union_attention"] = round(packed["ms"] / attn_ms, 4)
+        out["branch_packed"] = packed
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(trajs, wl, lmw, attn_useful, lm_useful)
