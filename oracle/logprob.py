@@ -18,7 +18,8 @@ Gradient into the hidden state for upstream g_t = dL/dlogp_t:
 
     dH_t = g_t * (W[y_t] - sum_v softmax(z_t)_v W[v])
 
-which is the textbook derivative of log-softmax at one index.
+which is the textbook derivative of log-softmax at one index; into the
+weights, dW = G^T H with G_tv = g_t (1[v = y_t] - softmax(z_t)_v).
 """
 from __future__ import annotations
 
@@ -67,6 +68,26 @@ def token_logprob_bwd(hidden, weight, target, dlogp, dtype=torch.float64, chunk:
         ok = (y >= 0).to(dtype)
         g = dlogp[c0:c1].to(dtype) * ok
         out[c0:c1] = g[:, None] * (W[y.clamp(min=0)] - p @ W)
+    return out
+
+
+def token_logprob_dweight(hidden, weight, target, dlogp, dtype=torch.float64, chunk: int = 256):
+    """Gradient into the LM-head weights: dW = G^T H with G = g (onehot - softmax(z)),
+    i.e. dW[v] = sum_t g_t (1[v = y_t] - p_tv) h_t (zero contribution from target -1)."""
+    T, H = hidden.shape
+    W = weight.to(dtype)
+    out = torch.zeros(W.shape, dtype=dtype)
+    tgt = target.to(torch.long)
+    for c0 in range(0, T, chunk):
+        c1 = min(T, c0 + chunk)
+        h = hidden[c0:c1].to(dtype)
+        p = torch.softmax(h @ W.T, dim=1)
+        y = tgt[c0:c1]
+        ok = (y >= 0).to(dtype)
+        g = dlogp[c0:c1].to(dtype) * ok
+        G = -g[:, None] * p
+        G[torch.arange(c1 - c0), y.clamp(min=0)] += g
+        out += G.T @ h
     return out
 
 

@@ -112,3 +112,32 @@ def test_ppo_clip_gradient_matches_finite_difference(adv):
     d = 1e-7
     fd = (obj(logr + d) - obj(logr - d)) / (2 * d)
     assert torch.allclose(g, fd, atol=1e-6)
+
+
+def test_weight_gradient_finite_differences_and_autograd():
+    """dW = G^T H against central differences of sum_t g_t logp_t in W, against
+    autograd, and its invariant: the vocabulary rows of G sum to zero, so the
+    rows of dW do too."""
+    gen = torch.Generator().manual_seed(21)
+    T, H, V = 7, 5, 11
+    h = torch.randn(T, H, generator=gen, dtype=F64)
+    w = torch.randn(V, H, generator=gen, dtype=F64)
+    y = torch.randint(0, V, (T,), generator=gen)
+    y[3] = -1
+    g = torch.randn(T, generator=gen, dtype=F64)
+    dW = LP.token_logprob_dweight(h, w, y, g)
+    assert torch.allclose(dW.sum(dim=0), torch.zeros(H, dtype=F64), atol=1e-12)
+    def f(wm):
+        lp, _, _, _ = LP.token_logprob(h, wm, y)
+        return float((lp * g).sum())
+    eps = 1e-6
+    for v in range(V):
+        for k in range(H):
+            wp, wm = w.clone(), w.clone()
+            wp[v, k] += eps
+            wm[v, k] -= eps
+            assert abs((f(wp) - f(wm)) / (2 * eps) - float(dW[v, k])) < 1e-7
+    wa = w.clone().requires_grad_(True)
+    lp = torch.log_softmax(h @ wa.T, dim=1).gather(1, y.clamp(min=0)[:, None])[:, 0]
+    ((lp * (y >= 0)) * g).sum().backward()
+    assert torch.allclose(wa.grad, dW, atol=1e-12)
