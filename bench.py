@@ -203,6 +203,27 @@ def time_sdcc(args, mv, synth, mask, wl, lmw, dev):
     }
 
 
+def time_dweight(args, mv, h, w, ws):
+    """The LM-head weight gradient dW = G^T H over the step's tokens (G left in
+    the backward workspace by the step), timed on its own: 2 T H V FLOPs."""
+    import torch
+    for _ in range(args.warmup):
+        dw = mv.token_logprob_dweight(h, w, ws)
+    torch.cuda.synchronize()
+    mv.profile_enable(True)
+    for _ in range(args.steps):
+        dw = mv.token_logprob_dweight(h, w, ws)
+    torch.cuda.synchronize()
+    tot, cnt = mv.profile_read("lm_dw")
+    mv.profile_enable(False)
+    del dw
+    ms = tot / cnt
+    tflops = 2.0 * h.shape[0] * h.shape[1] * w.shape[0] / (ms * 1e-3) / 1e12
+    log(f"lm-head dW: {ms:.2f} ms, {tflops:.0f} TFLOP/s")
+    return {"ms": round(ms, 3), "tflops": round(tflops, 2),
+            "frac_peak": round(tflops / PEAK_BF16_TFLOPS, 4)}
+
+
 def time_packed(args, mv, synth, trajs, wl, dev):
     """One exact attention layer on the branch-replicated packed stream of the
     same batch (the form that stays exact through a stack of layers): rotary
@@ -336,6 +357,7 @@ def main():
             kt[name] = {"ms_per_launch": tot / n, "launches": n}
     mv.profile_enable(False)
     log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step (host wall {wall_ms:.2f})")
+    dweight = time_dweight(args, mv, h, w, lpb_ws)
     sdcc = None if args.no_sdcc else time_sdcc(args, mv, synth, mask, wl, lmw, dev)
     packed = None if args.no_packed else time_packed(args, mv, synth, trajs, wl, dev)
 
@@ -405,6 +427,7 @@ def main():
             "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated)",
         },
     }
+    out["lmhead"]["dweight"] = dweight
     if sdcc is not None:
         out["sdcc"] = sdcc
     if packed is not None:

@@ -335,6 +335,17 @@ mv_status mv_token_logprob_bwd(const mv_logprob_shape* shape, const void* hidden
                                hipStream_t stream);
 
 /*
+ * Gradient into the LM-head weights, dweight = G^T hidden (fp32 [vocab,
+ * hidden]) with G_tv = dlogp_t (1[v = y_t] - softmax(z_t)_v), the same G that
+ * mv_token_logprob_bwd writes into its workspace: call it with that workspace
+ * after the backward, before the workspace is reused (the G it holds is not
+ * validated).  n_tokens == 0 is a no-op (dweight is not written).
+ */
+mv_status mv_token_logprob_dweight(const mv_logprob_shape* shape, const void* hidden,
+                                   const void* workspace, size_t workspace_bytes,
+                                   float* dweight, hipStream_t stream);
+
+/*
  * dlogp_t = d/dlogp_t [ -scale * min(ratio_t A_t, clamp(ratio_t) A_t) ]: the
  * clipped surrogate's gradient, zero where the clipped branch is active.
  */
@@ -450,7 +461,7 @@ float mv_sdcc_lambda(int32_t step, int32_t total_steps, float lambda_max, float 
  * previous records; mv_profile_read waits for the recorded events and returns
  * the summed duration (ms) and launch count of the kernels named `kernel`
  * (one of "attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce",
- * "attn_bwd_dq", "lm_logits", "lm_combine", "lm_grad", "lm_dh", "kl_logits",
+ * "attn_bwd_dq", "lm_logits", "lm_combine", "lm_grad", "lm_dh", "lm_dw", "kl_logits",
  * "kl_combine", "kl_grad", "kl_dh", "grpo", "pack", "unpack", "rope", "materialize",
  * "ppo_clip").  Not for use
  * under stream capture.

@@ -75,6 +75,8 @@ hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, c
 hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const void* weight,
                               const int32_t* target, const float* lse, const float* dlogp,
                               void* dhidden, void* ws, hipStream_t stream);
+hipError_t launch_logprob_dweight(int T, int H, int V, const void* hidden, const void* ws,
+                                  float* dw, hipStream_t stream);
 size_t grpo_ws_bytes(int T, int n_traj);
 hipError_t launch_grpo(int T, int n_traj, int G, float eps_lo, float eps_hi, float beta,
                        float adv_eps, const int32_t* traj_ptr, const float* reward,
@@ -377,6 +379,23 @@ mv_status mv_profile_read(const char* kernel, double* total_ms, int32_t* count) 
   *total_ms = tot;
   *count = n;
   return MV_OK;
+}
+
+mv_status mv_token_logprob_dweight(const mv_logprob_shape* s, const void* hidden,
+                                   const void* ws, size_t ws_bytes, float* dweight,
+                                   hipStream_t stream) {
+  if (mv_status st = check_logprob(s); st != MV_OK) return st;
+  if (s->n_tokens == 0) return MV_OK;
+  if (mv_status st = check_ptrs({hidden, ws, dweight}); st != MV_OK) return st;
+  const size_t need = mv::logprob_bwd_ws_bytes(s->n_tokens, s->hidden, s->vocab);
+  if (ws_bytes < need) {
+    std::ostringstream os;
+    os << "workspace has " << ws_bytes << " bytes, the backward's holds " << need;
+    return fail(MV_ERR_WORKSPACE, os.str());
+  }
+  return hip_status(mv::launch_logprob_dweight(s->n_tokens, s->hidden, s->vocab, hidden, ws,
+                                               dweight, stream),
+                    "LM-head weight gradient launch");
 }
 
 size_t mv_grpo_loss_workspace_bytes(const mv_grpo_shape* s) {

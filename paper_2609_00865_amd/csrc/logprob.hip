@@ -35,6 +35,7 @@ constexpr int PAD = BKK + 8;               // LDS row stride (bf16), conflict-fr
 constexpr int WPAD = BA + 32;
 constexpr int STAGE = (BA + BT) * PAD;     // one k slice of both operands
 static_assert(BKK * WPAD <= BA * PAD, "dH pass W slice must fit the A region");
+static_assert(BKK * WPAD <= BT * PAD, "dW pass hidden slice must fit the token region");
 constexpr int NWAVES = 8;                 // waves per tile (2 x NWAVES/2 grid)
 constexpr int GROUP_T = 4;                 // token tiles per raster group
 constexpr float kLog2e = 1.4426950408889634f;
@@ -43,7 +44,7 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int vocab_pad(int V) { return (V + BA - 1) / BA * BA; }
 }  // namespace
 
-enum { kModeLogits = 0, kModeGrad = 1, kModeDh = 2, kModeKL = 3, kModeKLGrad = 4 };
+enum { kModeLogits = 0, kModeGrad = 1, kModeDh = 2, kModeKL = 3, kModeKLGrad = 4, kModeDw = 5 };
 
 struct LmArgs {
   const u16* h;       // [T, H]
@@ -75,6 +76,7 @@ struct LmArgs {
   // writes fp32 partials dh_part[s][t][H], summed in order by dh_reduce_kernel
   int k_split, nk_split;
   float* dh_part;
+  float* dw;          // [V, H] fp32 (dW mode)
 };
 
 template <int MODE, int NW>
@@ -108,16 +110,19 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
   const int c = lane & 31, g = lane >> 5;
   const int wa = wave / (NW / 2), wt = wave % (NW / 2);
 
-  const int K = (MODE == kModeDh) ? a.Vp : a.H;
+  // dW mode: A rows = vocabulary, B "tokens" = hidden columns, k = tokens
+  constexpr bool kT = (MODE == kModeDh || MODE == kModeDw);  // both stages k-major
+  const int K = (MODE == kModeDh) ? a.Vp : (MODE == kModeDw ? a.T : a.H);
   const int a_rows = (MODE == kModeDh) ? a.H : a.V;
+  const int b_rows = (MODE == kModeDw) ? a.H : a.T;
   const int kbeg = (MODE == kModeDh) ? split * a.nk_split : 0;
-  const int nk = (MODE == kModeDh) ? min(K / BKK - kbeg, a.nk_split) : K / BKK;
+  const int nk = (MODE == kModeDh) ? min(K / BKK - kbeg, a.nk_split) : (K + BKK - 1) / BKK;
   // Out-of-range operand rows and columns are read from clamped (valid)
   // addresses instead of being masked, so loads never wait on a select: the
   // products they feed land in output rows, columns or vocabulary padding that
   // the epilogues skip or zero (and padding columns of G are stored as zero).
   // Tiles wholly inside the operands skip even the clamping.
-  const bool interior = (t0 + BT <= a.T) && (MODE == kModeDh ? (a0 + BA <= a.H) : (a0 + BA <= a_rows));
+  const bool interior = (t0 + BT <= b_rows) && (MODE == kModeDh ? (a0 + BA <= a.H) : (a0 + BA <= a_rows));
 
   f32x16 acc[4][NJ];
 #pragma unroll
@@ -133,7 +138,9 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
   for (int r = 0; r < LDB; ++r) {
     const int t = t0 + (tid + r * NT) / (BKK / 8);
     const int tc = (interior || t < a.T) ? t : 0;
-    if (MODE == kModeDh) {
+    if (MODE == kModeDw) {
+      brow[r] = nullptr;  // the dW stages are addressed per k slice
+    } else if (MODE == kModeDh) {
       brow[r] = a.G + size_t(tc) * a.Vp;
     } else if (MODE == kModeKL || MODE == kModeKLGrad) {
       // a row index outside its matrix reads as a zero hidden state
@@ -148,6 +155,35 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
 
   uint4 ra[LDA], rb[LDB];
   auto load = [&](int k0) {
+    if (MODE == kModeDw) {
+      // G slice [64 tokens][256 vocabulary] and H slice [64 tokens][256
+      // hidden], both staged k-major and read with the transposing LDS read.
+      // Token rows past T must add nothing (k is summed): the tail slice
+      // zeroes them (a block-uniform branch, taken once per tile).
+      auto stage = [&](bool tail) {
+#pragma unroll
+        for (int r = 0; r < LDA; ++r) {
+          const int idx = tid + r * NT;
+          const int row = idx / (BA / 8), cc = (idx % (BA / 8)) * 8;
+          const int t = k0 + row;
+          ra[r] = ld16(a.G + size_t(min(t, a.T - 1)) * a.Vp + a0 + cc);
+          if (tail && t >= a.T) ra[r] = make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int r = 0; r < LDB; ++r) {
+          const int idx = tid + r * NT;
+          const int row = idx / (BT / 8), cc = (idx % (BT / 8)) * 8;
+          const int t = k0 + row;
+          rb[r] = ld16(a.h + size_t(min(t, a.T - 1)) * a.H + min(t0 + cc, a.H - 8));
+          if (tail && t >= a.T) rb[r] = make_uint4(0, 0, 0, 0);
+        }
+      };
+      if (k0 + BKK > a.T)
+        stage(true);
+      else
+        stage(false);
+      return;
+    }
 #pragma unroll
     for (int r = 0; r < LDA; ++r) {
       const int idx = tid + r * NT;
@@ -176,7 +212,7 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
 #pragma unroll
     for (int r = 0; r < LDA; ++r) {
       const int idx = tid + r * NT;
-      if (MODE == kModeDh) {
+      if (kT) {
         const int row = idx / (BA / 8), cc = (idx % (BA / 8)) * 8;
         st16(&sA[row * WPAD + cc], ra[r]);
       } else {
@@ -187,8 +223,13 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
 #pragma unroll
     for (int r = 0; r < LDB; ++r) {
       const int idx = tid + r * NT;
-      const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
-      st16(&sB[row * PAD + cc], rb[r]);
+      if (MODE == kModeDw) {
+        const int row = idx / (BT / 8), cc = (idx % (BT / 8)) * 8;
+        st16(&sB[row * WPAD + cc], rb[r]);
+      } else {
+        const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
+        st16(&sB[row * PAD + cc], rb[r]);
+      }
     }
   };
 
@@ -213,12 +254,13 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
       bf16x8 af[4], bf[NJ];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        af[i] = (MODE == kModeDh)
-                    ? ld_operand_tr<WPAD, true>(sA, ks * 16, wa * 128 + i * 32)
-                    : as_bf16x8(ld16(&sA[(wa * 128 + i * 32 + c) * PAD + ks * 16 + g * 8]));
+        af[i] = kT ? ld_operand_tr<WPAD, true>(sA, ks * 16, wa * 128 + i * 32)
+                   : as_bf16x8(ld16(&sA[(wa * 128 + i * 32 + c) * PAD + ks * 16 + g * 8]));
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
-        bf[j] = as_bf16x8(ld16(&sB[(wt * WTOK + j * 32 + c) * PAD + ks * 16 + g * 8]));
+        bf[j] = (MODE == kModeDw)
+                    ? ld_operand_tr<WPAD, true>(sB, ks * 16, wt * WTOK + j * 32)
+                    : as_bf16x8(ld16(&sB[(wt * WTOK + j * 32 + c) * PAD + ks * 16 + g * 8]));
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -353,6 +395,19 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
             wv.y = pack2(vals[2], vals[3]);
             *reinterpret_cast<uint2*>(out + arow0 + i * 32 + q4 * 8 + g * 4) = wv;
           }
+        }
+    }
+  } else if (MODE == kModeDw) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int hcol = t0 + wt * WTOK + j * 32 + c;
+      if (hcol >= a.H) continue;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = arow0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+          if (v < a.V) a.dw[size_t(v) * a.H + hcol] = acc[i][j][r];
         }
     }
   } else if (a.k_split > 1) {
@@ -639,6 +694,25 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
   float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(G) +
                                          align256(size_t(T) * a.Vp * sizeof(u16)));
   return launch_dh(a, part, "lm_dh", stream);
+}
+
+// dW = G^T H from the G that launch_logprob_bwd left in its workspace.
+hipError_t launch_logprob_dweight(int T, int H, int V, const void* hidden, const void* ws,
+                                  float* dw, hipStream_t stream) {
+  LmArgs a{};
+  a.h = static_cast<const u16*>(hidden);
+  a.G = reinterpret_cast<const u16*>(align_ptr(const_cast<void*>(ws)));
+  a.dw = dw;
+  a.T = T;
+  a.H = H;
+  a.V = V;
+  a.Vp = vocab_pad(V);
+  a.nA = a.Vp / BA;
+  a.nT = (H + BT - 1) / BT;
+  ProfScope p("lm_dw", stream);
+  hipLaunchKernelGGL((lm_gemm_kernel<kModeDw, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
+                     stream, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_kl_fwd(int n, int H, int V, const void* hT, int nT, const int32_t* rowsT,

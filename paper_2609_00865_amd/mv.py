@@ -139,6 +139,8 @@ mv_token_logprob_bwd_workspace_bytes = _sig("mv_token_logprob_bwd_workspace_byte
                                             _P(LogprobShape))
 mv_token_logprob_bwd = _sig("mv_token_logprob_bwd", ctypes.c_int, _P(LogprobShape), _vp, _vp,
                             _vp, _vp, _vp, _vp, _vp, _sz, _vp)
+mv_token_logprob_dweight = _sig("mv_token_logprob_dweight", ctypes.c_int, _P(LogprobShape), _vp,
+                                _vp, _sz, _vp, _vp)
 mv_ppo_clip_dlogp = _sig("mv_ppo_clip_dlogp", ctypes.c_int, _i32, _vp, _vp, _f32, _f32, _f32,
                          _vp, _vp)
 mv_build_branch_pack = _sig("mv_build_branch_pack", ctypes.c_int, _P(TrajectoryC), _i32, _i32,
@@ -178,7 +180,7 @@ EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_ma
             "mv_grpo_loss_workspace_bytes", "mv_grpo_loss", "mv_build_branch_pack",
             "mv_branch_pack_stats", "mv_branch_pack_layout", "mv_branch_pack_mask",
             "mv_branch_pack_device_bytes", "mv_branch_pack_upload", "mv_branch_pack_free",
-            "mv_pack_rows", "mv_unpack_rows_sum", "mv_rope",
+            "mv_pack_rows", "mv_unpack_rows_sum", "mv_rope", "mv_token_logprob_dweight",
             "mv_profile_enable", "mv_profile_read"]
 
 VIEW_LIVE, VIEW_FINAL = 0, 1
@@ -405,6 +407,16 @@ def token_logprob_bwd(hidden, weight, target, lse, dlogp, workspace=None, stream
     return dh
 
 
+def token_logprob_dweight(hidden, weight, workspace, stream=None):
+    """dW = G^T H (fp32 [V, H]) from the G that token_logprob_bwd left in `workspace`."""
+    _need_bf16_cuda(hidden, weight)
+    s = _lp_shape(hidden, weight, 0.2, 0.2)
+    dw = torch.empty(weight.shape, dtype=torch.float32, device=hidden.device)
+    check(mv_token_logprob_dweight(ctypes.byref(s), _ptr(hidden), _ptr(workspace),
+                                   workspace.numel(), _ptr(dw), _stream(stream)))
+    return dw
+
+
 def ppo_clip_dlogp(ratio, adv, eps_low=0.2, eps_high=0.2, scale=1.0, stream=None):
     out = torch.empty_like(ratio)
     check(mv_ppo_clip_dlogp(ratio.numel(), _ptr(ratio), _ptr(adv), eps_low, eps_high, scale,
@@ -575,7 +587,7 @@ def sdcc_lambda(step: int, total_steps: int, lambda_max: float = 0.1,
 # kernel timing
 # ---------------------------------------------------------------------------
 KERNELS = ["attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq",
-           "lm_logits", "lm_combine", "lm_grad", "lm_dh", "kl_logits", "kl_combine", "kl_grad", "kl_dh",
+           "lm_logits", "lm_combine", "lm_grad", "lm_dh", "lm_dw", "kl_logits", "kl_combine", "kl_grad", "kl_dh",
            "grpo", "pack", "unpack", "rope",
            "materialize", "ppo_clip"]
 

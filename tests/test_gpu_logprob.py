@@ -98,3 +98,39 @@ def test_full_size_sampled():
     assert_rel_close(clipped.cpu()[idx], rc, "lmhead clipped", rel=2e-3)
     ref_dh = OL.token_logprob_bwd(hc[idx], wc, yc[idx], gc[idx], dtype=torch.float32)
     assert_bf16_close(dh.cpu()[idx], ref_dh, "lmhead dH")
+
+
+@pytest.mark.parametrize("T,H,V", [(300, 256, 1000), (257, 192, 600), (64, 128, 256),
+                                   (1, 64, 17)])
+def test_dweight_small_ragged(T, H, V):
+    h, w, y, old, g = _inputs(T, H, V, 6, skip_every=5)
+    print(f"[gpu] dweight T={T} H={H} V={V}", flush=True)
+    hd, wd, yd, gd = h.cuda(), w.cuda(), y.cuda(), g.cuda()
+    _, _, _, lse = mv.token_logprob(hd, wd, yd)
+    ws = mv.token_logprob_bwd_workspace(hd, wd)
+    mv.token_logprob_bwd(hd, wd, yd, lse, gd, workspace=ws)
+    dw = mv.token_logprob_dweight(hd, wd, ws).cpu()
+    torch.cuda.synchronize()
+    ref = OL.token_logprob_dweight(h, w, y, g)
+    assert_bf16_close(dw, ref, f"dW {T}x{H}x{V}")
+    # every row of G sums to zero, so do the columns of dW over the vocabulary
+    assert float(dw.double().sum(dim=0).abs().max()) < 1e-2 * float(ref.abs().max()) + 1e-3
+
+
+@pytest.mark.slow
+def test_dweight_full_width():
+    """320 tokens (a ragged last k slice) at the full 3584 x 152064 head; the
+    targets' rows and every 6007th row checked (fp32 oracle)."""
+    wl = synth.LOGPROB_WORKLOADS["lmhead"]
+    T = 320
+    h, w, y, old, g = synth.make_logprob_inputs(T, wl.hidden, wl.vocab, 3)
+    print("[gpu] dweight full width", flush=True)
+    hd, wd, yd, gd = h.cuda(), w.cuda(), y.cuda(), g.cuda()
+    _, _, _, lse = mv.token_logprob(hd, wd, yd)
+    ws = mv.token_logprob_bwd_workspace(hd, wd)
+    mv.token_logprob_bwd(hd, wd, yd, lse, gd, workspace=ws)
+    dw = mv.token_logprob_dweight(hd, wd, ws)
+    torch.cuda.synchronize()
+    rows = torch.tensor(sorted(set(y[:40].long().tolist()) | set(range(0, wl.vocab, 6007))))
+    ref = OL.token_logprob_dweight(h, w, y, g, dtype=torch.float32)[rows]
+    assert_bf16_close(dw.cpu()[rows], ref, "dW full width (sampled rows)")
