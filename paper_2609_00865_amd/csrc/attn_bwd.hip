@@ -72,9 +72,10 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
   constexpr int RPAD = D + 48;
   constexpr int RLD = BK * D / 8 / 256;          // row-major K and V loads per thread
 
-  __shared__ __align__(16) u16 sK[BK * RPAD];
-  __shared__ __align__(16) u16 sV[BK * RPAD];
-  __shared__ __align__(16) int sOm[BK];
+  // two buffers: key tile e+1 is written while tile e is read
+  __shared__ __align__(16) u16 sKbuf[2 * BK * RPAD];
+  __shared__ __align__(16) u16 sVbuf[2 * BK * RPAD];
+  __shared__ __align__(16) int sOmbuf[2 * BK];
 
   int xcd, local;
   xcd_split(xcd, local);
@@ -125,30 +126,39 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
     }
     if (tid < BK) omreg = (j0 + tid < T) ? a.mask.omega[j0 + tid] : 0;
   };
-  auto store_tile = [&]() {
+  auto store_tile = [&](int buf) {
+    u16* k_ = sKbuf + buf * BK * RPAD;
+    u16* v_ = sVbuf + buf * BK * RPAD;
 #pragma unroll
     for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      st16(&sV[row * RPAD + col], vreg[r]);
-      st16(&sK[row * RPAD + col], kreg[r]);
+      st16(&v_[row * RPAD + col], vreg[r]);
+      st16(&k_[row * RPAD + col], kreg[r]);
     }
-    if (tid < BK) sOm[tid] = omreg;
+    if (tid < BK) sOmbuf[buf * BK + tid] = omreg;
   };
 
+  // Tile e+1 is stored into the idle buffer (read by every wave before the
+  // last barrier) and tile e+2 requested before tile e's MFMAs; one barrier
+  // per tile.  Every row tile lists at least its diagonal key tile.
   const int e0 = a.mask.q_ptr[qt], e1 = a.mask.q_ptr[qt + 1];
-  int ent = a.mask.k_list[e0];
-  load_tile(ent >> 1);
+  load_tile(a.mask.k_list[e0] >> 1);
+  store_tile(0);
+  if (e0 + 1 < e1) load_tile(a.mask.k_list[e0 + 1] >> 1);
+  __syncthreads();
   for (int e = e0; e < e1; ++e) {
+    const int ent = a.mask.k_list[e];
     const int kt = ent >> 1;
     const bool full = ent & 1;
-    __syncthreads();
-    store_tile();
-    __syncthreads();
+    const int buf = (e - e0) & 1;
     if (e + 1 < e1) {
-      ent = a.mask.k_list[e + 1];
-      load_tile(ent >> 1);
+      store_tile(buf ^ 1);
+      if (e + 2 < e1) load_tile(a.mask.k_list[e + 2] >> 1);
     }
+    const u16* sK = sKbuf + buf * BK * RPAD;
+    const u16* sV = sVbuf + buf * BK * RPAD;
+    const int* sOm = sOmbuf + buf * BK;
     const int j0 = kt * BK;
 
     f32x16 s[2], dp[2];
@@ -195,6 +205,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
         // K^T operand: column block db of keys ks*16.. in accumulator order
         acc[db] = mfma32(ld_operand_tr<RPAD>(sK, ks * 16, db * 32), dsf[ks], acc[db]);
       }
+    __syncthreads();
   }
 
   if (!qok) return;
@@ -218,15 +229,18 @@ template <int D>
 __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   constexpr int BK = kBwdTileK, BQ = kBwdBlockQ;
   constexpr int KS = D / 16, DB = D / 32;
+  constexpr int MB = BQ / 32;              // 32-row MFMA blocks of a row block
+  constexpr int KQ = BQ / 16;              // 16-row k steps of the dV / dK products
   constexpr int RPAD = D + 48;
   constexpr int RLD = BQ * (D / 8) / 256;  // 16-byte row loads per thread per tensor
 
   // Q and dO blocks are staged row-major only; their transposed operands are
   // read with the transposing LDS read (ld_operand_tr).
-  __shared__ __align__(16) u16 sQ[BQ * RPAD];
-  __shared__ __align__(16) u16 sdO[BQ * RPAD];
-  __shared__ __align__(16) float sL[BQ];
-  __shared__ __align__(16) float sD[BQ];
+  // two buffers: block b+1 is written while block b is read
+  __shared__ __align__(16) u16 sQbuf[2 * BQ * RPAD];
+  __shared__ __align__(16) u16 sdObuf[2 * BQ * RPAD];
+  __shared__ __align__(16) float sLbuf[2 * BQ];
+  __shared__ __align__(16) float sDbuf[2 * BQ];
 
   int xcd, local;
   xcd_split(xcd, local);
@@ -286,38 +300,49 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       dreg1 = i < T ? a.Dd[size_t(hh) * T + i] : 0.f;
     }
   };
-  auto store_block = [&]() {
+  auto store_block = [&](int buf) {
+    u16* q_ = sQbuf + buf * BQ * RPAD;
+    u16* d_ = sdObuf + buf * BQ * RPAD;
 #pragma unroll
     for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), cc = idx % (D / 8);
-      st16(&sQ[row * RPAD + cc * 8], qreg[r]);
-      st16(&sdO[row * RPAD + cc * 8], dreg[r]);
+      st16(&q_[row * RPAD + cc * 8], qreg[r]);
+      st16(&d_[row * RPAD + cc * 8], dreg[r]);
     }
     if (tid < BQ) {
-      sL[tid] = lreg;
-      sD[tid] = dreg1;
+      sLbuf[buf * BQ + tid] = lreg;
+      sDbuf[buf * BQ + tid] = dreg1;
     }
   };
 
   const int nqb = qb1 - qb0;
   const int steps = nqb * G;
   const int h0 = hk * G;
+  // Block st+1 is stored into the idle buffer (read by every wave before the
+  // last barrier) and block st+2 requested before block st's MFMAs, so the
+  // stores and the HBM latency overlap the math; one barrier per block.
   load_block(h0, qb0);
+  store_block(0);
+  if (steps > 1) load_block(h0 + 1 / nqb, qb0 + 1 % nqb);
+  __syncthreads();
   for (int st = 0; st < steps; ++st) {
-    const int hh = h0 + st / nqb;
     const int qb = qb0 + st % nqb;
-    (void)hh;
-    __syncthreads();
-    store_block();
-    __syncthreads();
-    if (st + 1 < steps) load_block(h0 + (st + 1) / nqb, qb0 + (st + 1) % nqb);
+    const int buf = st & 1;
+    if (st + 1 < steps) {
+      store_block(buf ^ 1);
+      if (st + 2 < steps) load_block(h0 + (st + 2) / nqb, qb0 + (st + 2) % nqb);
+    }
+    const u16* sQ = sQbuf + buf * BQ * RPAD;
+    const u16* sdO = sdObuf + buf * BQ * RPAD;
+    const float* sL = sLbuf + buf * BQ;
+    const float* sD = sDbuf + buf * BQ;
     const int i0 = qb * BQ;
     const bool full = (i0 >= j1 - 1) && (i0 + BQ <= om_min);
 
-    f32x16 s[2], dp[2];
+    f32x16 s[MB], dp[MB];
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
+    for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         s[mb][r] = 0.f;
@@ -332,7 +357,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     }
     // P and dS in place; rows of s/dp are queries mb*32 + q4*8 + g*4 + u
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
+    for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
         const int qo = mb * 32 + q4 * 8 + g * 4;
@@ -349,20 +374,21 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
         }
       }
     }
-    bf16x8 pf[4], dsf[4];
+    bf16x8 pf[KQ], dsf[KQ];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < KQ; ++ks) {
       pf[ks] = to_operand(s[ks >> 1], (ks & 1) * 8);
       dsf[ks] = to_operand(dp[ks >> 1], (ks & 1) * 8);
     }
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
+      for (int ks = 0; ks < KQ; ++ks) {
         // dO^T and Q^T operands: columns db*32.. of rows ks*16.. in accumulator order
         dv[db] = mfma32(ld_operand_tr<RPAD>(sdO, ks * 16, db * 32), pf[ks], dv[db]);
         dk[db] = mfma32(ld_operand_tr<RPAD>(sQ, ks * 16, db * 32), dsf[ks], dk[db]);
       }
+    __syncthreads();
   }
 
   if (!kok) return;

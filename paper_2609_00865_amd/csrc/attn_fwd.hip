@@ -36,9 +36,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   constexpr int KLD = BK * D / 8 / 256;        // 16-byte K (and V) loads per thread
   static_assert(KLD >= 1, "tile too small for 256 threads");
 
-  __shared__ __align__(16) u16 sK[BK * KPAD];
-  __shared__ __align__(16) u16 sV[BK * VPAD];
-  __shared__ __align__(16) int sOm[BK];
+  // two buffers: key tile e+1 is written while tile e is read
+  __shared__ __align__(16) u16 sKbuf[2 * BK * KPAD];
+  __shared__ __align__(16) u16 sVbuf[2 * BK * VPAD];
+  __shared__ __align__(16) int sOmbuf[2 * BK];
 
   int xcd, local;
   xcd_split(xcd, local);
@@ -88,30 +89,39 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     }
     if (tid < BK) omreg = (j0 + tid < T) ? a.mask.omega[j0 + tid] : 0;
   };
-  auto store_tile = [&]() {
+  auto store_tile = [&](int buf) {
+    u16* k_ = sKbuf + buf * BK * KPAD;
+    u16* v_ = sVbuf + buf * BK * VPAD;
 #pragma unroll
     for (int r = 0; r < KLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      st16(&sK[row * KPAD + col], kreg[r]);
-      st16(&sV[row * VPAD + col], vreg[r]);
+      st16(&k_[row * KPAD + col], kreg[r]);
+      st16(&v_[row * VPAD + col], vreg[r]);
     }
-    if (tid < BK) sOm[tid] = omreg;
+    if (tid < BK) sOmbuf[buf * BK + tid] = omreg;
   };
 
+  // Tile e+1 is stored into the idle buffer (read by every wave before the
+  // last barrier) and tile e+2 requested before tile e's MFMAs; one barrier
+  // per tile.  Every row tile lists at least its diagonal key tile.
   const int e0 = a.mask.q_ptr[qt], e1 = a.mask.q_ptr[qt + 1];
-  int ent = a.mask.k_list[e0];
-  load_tile(ent >> 1);
+  load_tile(a.mask.k_list[e0] >> 1);
+  store_tile(0);
+  if (e0 + 1 < e1) load_tile(a.mask.k_list[e0 + 1] >> 1);
+  __syncthreads();
   for (int e = e0; e < e1; ++e) {
+    const int ent = a.mask.k_list[e];
     const int kt = ent >> 1;
     const bool full = ent & 1;
-    __syncthreads();
-    store_tile();
-    __syncthreads();
+    const int buf = (e - e0) & 1;
     if (e + 1 < e1) {
-      ent = a.mask.k_list[e + 1];
-      load_tile(ent >> 1);
+      store_tile(buf ^ 1);
+      if (e + 2 < e1) load_tile(a.mask.k_list[e + 2] >> 1);
     }
+    const u16* sK = sKbuf + buf * BK * KPAD;
+    const u16* sV = sVbuf + buf * BK * VPAD;
+    const int* sOm = sOmbuf + buf * BK;
     const int j0 = kt * BK;
 
     // S^T for keys [kb*32, kb*32+32) of the tile
@@ -178,6 +188,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
         // V^T operand: column block db of keys ks*16.. in accumulator order
         oacc[db] = mfma32(ld_operand_tr<VPAD>(sV, ks * 16, db * 32), pf[ks], oacc[db]);
       }
+    __syncthreads();
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
