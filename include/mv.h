@@ -68,9 +68,10 @@ int32_t mv_version(void);
  *
  * Equivalently every key j has the lifetime [j, omega(j)) of Eq.
  * "4d-mask-def" (Section 4.2), with omega(j) = J_k if j is in E_k and the end
- * of its trajectory otherwise: row i sees key j iff j <= i < omega(j).
- * Several trajectories are packed back to back; a row never sees another
- * trajectory's keys.
+ * of its trajectory otherwise: row i sees key j iff j <= i < omega(j).  A key
+ * that a later edit restores (R_k) gains further intervals [J_k, next death);
+ * row i sees it iff i lies in one of them.  Several trajectories are packed
+ * back to back; a row never sees another trajectory's keys.
  * ------------------------------------------------------------------------ */
 typedef struct {
   int32_t begin, end;            /* half-open physical positions [begin, end) */
@@ -85,6 +86,12 @@ typedef struct {
   mv_span summary;               /* metadata only (begin == end: none); summary
                                     tokens are ordinary keys born at their row;
                                     must lie in the trajectory and not meet E_k */
+  int32_t n_restore;             /* number of spans in R_k (0: a plain eviction)   */
+  const mv_span* restore;        /* R_k: sorted, disjoint spans of tokens evicted by
+                                    earlier edits and not yet restored, live again
+                                    from row J_k on at their own positions (an
+                                    offload / retrieve memory: a key may leave the
+                                    view and re-enter, Appendix E); must not meet E_k */
 } mv_edit;
 
 typedef struct {
@@ -161,8 +168,16 @@ mv_status mv_view_mask_upload(mv_view_mask* m, void* dev_buf, size_t bytes,
 
 mv_status mv_view_mask_stats(const mv_view_mask* m, mv_mask_stats* out);
 
-/* Copy omega (int32[total_tokens], host memory) out of the mask. */
+/* Copy omega (int32[total_tokens], host memory) out of the mask: for every
+ * key the end of its first live interval. */
 mv_status mv_view_mask_death(const mv_view_mask* m, int32_t* host_out);
+
+/* The further live intervals of keys that edits restore: iv_ptr (int32
+ * [total_tokens + 1], nullable) gets, per key, the range of its entries, and
+ * iv (int32 [2 * capacity], nullable) the (begin, end) row pairs in time
+ * order; *n_out receives the number of intervals.  Host only. */
+mv_status mv_view_mask_intervals(const mv_view_mask* m, int32_t* iv_ptr, int32_t* iv,
+                                 int32_t capacity, int32_t* n_out);
 
 /*
  * Write the visibility bits the attention kernels act on for rows

@@ -11,7 +11,11 @@ is applied *before* row J_k is evaluated; rows < J_k still see E_k, rows >= J_k
 do not.  Summary tokens are ordinary tokens born at their own row.
 
 Trajectories are any objects with ``begin``, ``end`` and ``edits``; an edit has
-``junction`` and ``evict`` (iterable of half-open physical spans).
+``junction`` and ``evict`` (iterable of half-open physical spans), and
+optionally ``restore``: spans evicted by earlier edits that are live again
+from the junction on (an offload / retrieve memory, where a token can leave
+the view and re-enter it, Appendix E).  A restored token re-enters at its own
+physical position, so the live list stays in physical order.
 """
 from __future__ import annotations
 
@@ -29,8 +33,15 @@ def _evicted_positions(edit) -> List[int]:
     return out
 
 
-def _edits_by_row(traj) -> Dict[int, list]:
-    by_row: Dict[int, list] = {}
+def _restored_positions(edit) -> List[int]:
+    out: List[int] = []
+    for b, e in getattr(edit, "restore", ()):
+        out.extend(range(int(b), int(e)))
+    return out
+
+
+def _edits_by_row(traj) -> Dict[int, tuple]:
+    by_row: Dict[int, tuple] = {}
     last = None
     for ed in traj.edits:
         J = int(ed.junction)
@@ -39,7 +50,7 @@ def _edits_by_row(traj) -> Dict[int, list]:
         if last is not None and J <= last:
             raise BadRecord("junctions must be strictly increasing")
         last = J
-        by_row[J] = _evicted_positions(ed)
+        by_row[J] = (_evicted_positions(ed), _restored_positions(ed))
     return by_row
 
 
@@ -53,10 +64,17 @@ def replay(traj) -> Iterator[Tuple[int, List[int]]]:
     by_row = _edits_by_row(traj)
     live: Dict[int, None] = {}          # insertion-ordered set
     for r in range(traj.begin, traj.end):
-        for p in by_row.get(r, ()):
+        evict, restore = by_row.get(r, ((), ()))
+        for p in evict:
             if p not in live:
                 raise BadRecord(f"edit at row {r} evicts {p}, which is not live")
             del live[p]
+        if restore:
+            for p in restore:
+                if p in live or not (traj.begin <= p < r) or p in evict:
+                    raise BadRecord(f"edit at row {r} restores {p}, which is not evicted")
+                live[p] = None
+            live = dict.fromkeys(sorted(live))
         live[r] = None
         yield r, live
 
@@ -75,32 +93,48 @@ def death_rows(traj) -> List[int]:
     """For every key of the trajectory, the first row that no longer sees it.
 
     This is omega(j) of Eq. "4d-mask-def" (Section 4.2) with +infinity written
-    as the trajectory's end.  Derived from the replay: the row at which the key
-    leaves the live list.
+    as the trajectory's end (for a key that re-enters, the end of its first
+    live interval; see ``lifetimes``).  Derived from the record by replaying
+    the live set: the row at which the key first leaves it.
     """
+    return [iv[0][1] for iv in lifetimes(traj)]
+
+
+def lifetimes(traj) -> List[List[Tuple[int, int]]]:
+    """For every key, the maximal runs of rows [b, e) whose view holds it,
+    replayed edit by edit (the same checks as ``replay``)."""
     by_row = _edits_by_row(traj)
-    out = [traj.end] * (traj.end - traj.begin)
-    live = set()
+    out: List[List[Tuple[int, int]]] = [[] for _ in range(traj.end - traj.begin)]
+    open_at: Dict[int, int] = {}
     for r in range(traj.begin, traj.end):
-        for p in by_row.get(r, ()):
-            if p not in live:
+        evict, restore = by_row.get(r, ((), ()))
+        for p in evict:
+            if p not in open_at:
                 raise BadRecord(f"edit at row {r} evicts {p}, which is not live")
-            live.discard(p)
-            out[p - traj.begin] = r
-        live.add(r)
+            out[p - traj.begin].append((open_at.pop(p), r))
+        for p in restore:
+            if p in open_at or not (traj.begin <= p < r) or p in evict:
+                raise BadRecord(f"edit at row {r} restores {p}, which is not evicted")
+            open_at[p] = r
+        open_at[r] = r
+    for p, b in open_at.items():
+        out[p - traj.begin].append((b, traj.end))
+    for iv in out:
+        iv.sort()
     return out
 
 
 def view_by_definition(traj, r: int) -> frozenset:
     """View(r) straight from the definition, without incremental state.
 
-    Key j is visible to row r iff j <= r and no edit that has fired by row r
-    (J_k <= r) lists j in E_k.
+    Key j is visible to row r iff j <= r and the last edit fired by row r
+    (J_k <= r) that names j does not evict it.
     """
     gone = set()
-    for ed in traj.edits:
+    for ed in sorted(traj.edits, key=lambda e: int(e.junction)):
         if int(ed.junction) <= r:
             gone.update(_evicted_positions(ed))
+            gone.difference_update(_restored_positions(ed))
     return frozenset(j for j in range(traj.begin, r + 1) if j not in gone)
 
 
@@ -146,10 +180,8 @@ def naive_views(traj, kind: str) -> List[frozenset]:
     if kind == "full":
         return [frozenset(range(traj.begin, r + 1)) for r in range(traj.begin, traj.end)]
     if kind == "compressed":
-        gone = set()
-        for ed in traj.edits:
-            gone.update(_evicted_positions(ed))
-        return [frozenset(j for j in range(traj.begin, r + 1) if j not in gone or j == r)
+        kept = set(final_walk(traj))
+        return [frozenset(j for j in range(traj.begin, r + 1) if j in kept or j == r)
                 for r in range(traj.begin, traj.end)]
     raise ValueError(kind)
 

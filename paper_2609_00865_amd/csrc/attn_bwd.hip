@@ -189,7 +189,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
           float p = fast_exp2(s[kb][r] * a.scale_log2 - lse2);
           if (!full) {
             const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
-            if (!mv_visible(qrow, key, omv[u])) p = 0.f;
+            if (!mv_visible_iv(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv)) p = 0.f;
           }
           s[kb][r] = p * (dp[kb][r] - Di);
         }
@@ -368,7 +368,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
         for (int u = 0; u < 4; ++u) {
           const int r = q4 * 4 + u;
           float p = fast_exp2(s[mb][r] * a.scale_log2 - lv[u]);
-          if (!full && !mv_visible(i0 + qo + u, key, om)) p = 0.f;
+          if (!full && !mv_visible_iv(i0 + qo + u, key, om, a.mask.iv_ptr, a.mask.iv)) p = 0.f;
           s[mb][r] = p;
           dp[mb][r] = p * (dp[mb][r] - dd[u]);
         }

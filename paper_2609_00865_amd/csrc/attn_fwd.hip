@@ -151,7 +151,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
           float x = s[kb][r] * a.scale_log2;
           if (!full) {
             const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
-            if (!mv_visible(qrow, key, omv[u])) x = -INFINITY;
+            if (!mv_visible_iv(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv)) x = -INFINITY;
           }
           s[kb][r] = x;
           mx = fmaxf(mx, x);

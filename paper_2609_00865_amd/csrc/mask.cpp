@@ -6,6 +6,7 @@
 // kernel (Appendix B.3).  Here the mask is never materialised: each key keeps
 // one integer, and the passes visit only tiles holding a visible pair.
 #include <algorithm>
+#include <array>
 #include <cstring>
 #include <numeric>
 #include <sstream>
@@ -22,10 +23,35 @@ mv_status bad(mv_status s, const std::string& msg) {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-mv_status validate_and_fill_omega(const mv_trajectory* trajs, int32_t n_traj, int32_t T,
-                                  std::vector<int32_t>& omega) {
+// Lifetimes of every key from the record: a key is live from its own row
+// until an edit evicts it (omega, the end of its first interval), and again
+// from each edit that restores it until the next eviction or the trajectory
+// end (the further intervals of keys that re-enter, kept in a per-key list).
+mv_status validate_and_fill_lifetimes(const mv_trajectory* trajs, int32_t n_traj, int32_t T,
+                                      std::vector<int32_t>& omega, std::vector<int32_t>& iv_ptr,
+                                      std::vector<int32_t>& iv) {
   omega.assign(T, 0);
+  std::vector<int32_t> open_at(T, -1);     // start of the key's current live interval
+  std::vector<uint8_t> first_closed(T, 0);
+  std::vector<std::array<int32_t, 3>> extra;  // (key, begin, end)
   int32_t pos = 0;
+  auto check_spans = [&](int32_t t, int32_t k, const char* what, const mv_span* sp, int32_t n,
+                         int32_t lo, int32_t hi) -> mv_status {
+    if (n < 0 || (n > 0 && sp == nullptr))
+      return bad(MV_ERR_INVALID_ARG, std::string("edit ") + what + ": null pointer or negative count");
+    int32_t prev_end = lo;
+    for (int32_t s = 0; s < n; ++s) {
+      if (sp[s].begin < prev_end || sp[s].end <= sp[s].begin || sp[s].end > hi) {
+        std::ostringstream os;
+        os << "trajectory " << t << " edit " << k << " " << what << " span " << s << " ["
+           << sp[s].begin << ", " << sp[s].end
+           << ") must be non-empty, sorted, disjoint and inside [" << lo << ", " << hi << ")";
+        return bad(MV_ERR_BAD_RECORD, os.str());
+      }
+      prev_end = sp[s].end;
+    }
+    return MV_OK;
+  };
   for (int32_t t = 0; t < n_traj; ++t) {
     const mv_trajectory& tr = trajs[t];
     if (tr.begin != pos || tr.end <= tr.begin || tr.end > T) {
@@ -34,7 +60,7 @@ mv_status validate_and_fill_omega(const mv_trajectory* trajs, int32_t n_traj, in
          << ") does not continue the packing at " << pos;
       return bad(MV_ERR_BAD_RECORD, os.str());
     }
-    for (int32_t j = tr.begin; j < tr.end; ++j) omega[j] = tr.end;
+    for (int32_t j = tr.begin; j < tr.end; ++j) open_at[j] = j;
     if (tr.n_edits < 0 || (tr.n_edits > 0 && tr.edits == nullptr))
       return bad(MV_ERR_INVALID_ARG, "trajectory edits: null pointer or negative count");
     int32_t last_j = tr.begin;
@@ -47,62 +73,132 @@ mv_status validate_and_fill_omega(const mv_trajectory* trajs, int32_t n_traj, in
         return bad(MV_ERR_BAD_RECORD, os.str());
       }
       last_j = e.junction;
-      if (e.n_evict < 0 || (e.n_evict > 0 && e.evict == nullptr))
-        return bad(MV_ERR_INVALID_ARG, "edit evict: null pointer or negative count");
-      int32_t prev_end = tr.begin;
+      if (mv_status st = check_spans(t, k, "evict", e.evict, e.n_evict, tr.begin, e.junction);
+          st != MV_OK)
+        return st;
+      if (mv_status st =
+              check_spans(t, k, "restore", e.restore, e.n_restore, tr.begin, e.junction);
+          st != MV_OK)
+        return st;
       for (int32_t s = 0; s < e.n_evict; ++s) {
         const mv_span sp = e.evict[s];
-        if (sp.begin < prev_end || sp.end <= sp.begin || sp.end > e.junction) {
-          std::ostringstream os;
-          os << "trajectory " << t << " edit " << k << " span " << s << " [" << sp.begin
-             << ", " << sp.end << ") must be non-empty, sorted, disjoint and inside ["
-             << tr.begin << ", " << e.junction << ")";
-          return bad(MV_ERR_BAD_RECORD, os.str());
-        }
-        prev_end = sp.end;
         for (int32_t j = sp.begin; j < sp.end; ++j) {
-          if (omega[j] != tr.end) {
+          if (open_at[j] < 0) {
             std::ostringstream os;
-            os << "token " << j << " is evicted at row " << e.junction
-               << " but already left the view at row " << omega[j];
+            os << "token " << j << " is evicted at row " << e.junction << " but is not live";
             return bad(MV_ERR_BAD_RECORD, os.str());
           }
-          omega[j] = e.junction;
+          if (!first_closed[j]) {
+            omega[j] = e.junction;
+            first_closed[j] = 1;
+          } else {
+            extra.push_back({j, open_at[j], e.junction});
+          }
+          open_at[j] = -1;
         }
         if (e.summary.begin < e.summary.end &&
             std::max(sp.begin, e.summary.begin) < std::min(sp.end, e.summary.end))
           return bad(MV_ERR_BAD_RECORD, "summary block intersects its own eviction set");
       }
+      for (int32_t s = 0; s < e.n_restore; ++s) {
+        const mv_span sp = e.restore[s];
+        for (int32_t j = sp.begin; j < sp.end; ++j) {
+          if (open_at[j] >= 0 || open_at[j] == -2) {
+            std::ostringstream os;
+            os << "token " << j << " is restored at row " << e.junction
+               << " but is live (or evicted by the same edit)";
+            return bad(MV_ERR_BAD_RECORD, os.str());
+          }
+        }
+      }
+      // a token evicted by this edit cannot come back in the same edit
+      for (int32_t s = 0; s < e.n_evict; ++s)
+        for (int32_t j = e.evict[s].begin; j < e.evict[s].end; ++j) open_at[j] = -2;
+      for (int32_t s = 0; s < e.n_restore; ++s)
+        for (int32_t j = e.restore[s].begin; j < e.restore[s].end; ++j) {
+          if (open_at[j] == -2) {
+            std::ostringstream os;
+            os << "token " << j << " is evicted and restored by the same edit at row "
+               << e.junction;
+            return bad(MV_ERR_BAD_RECORD, os.str());
+          }
+          open_at[j] = e.junction;
+        }
+      for (int32_t s = 0; s < e.n_evict; ++s)
+        for (int32_t j = e.evict[s].begin; j < e.evict[s].end; ++j) open_at[j] = -1;
       if (e.summary.begin != e.summary.end &&
           (e.summary.begin > e.summary.end || e.summary.begin < tr.begin || e.summary.end > tr.end))
         return bad(MV_ERR_BAD_RECORD, "summary block outside its trajectory");
     }
+    for (int32_t j = tr.begin; j < tr.end; ++j) {
+      if (open_at[j] < 0) continue;
+      if (!first_closed[j]) {
+        omega[j] = tr.end;
+        first_closed[j] = 1;
+      } else {
+        extra.push_back({j, open_at[j], tr.end});
+      }
+    }
     pos = tr.end;
   }
   if (pos != T) return bad(MV_ERR_BAD_RECORD, "trajectories do not cover [0, total_tokens)");
+  // per-key lists of further intervals, in order
+  std::stable_sort(extra.begin(), extra.end(),
+                   [](const auto& a, const auto& b) { return a[0] < b[0]; });
+  iv_ptr.assign(T + 1, 0);
+  iv.clear();
+  iv.reserve(2 * extra.size());
+  for (const auto& x : extra) {
+    ++iv_ptr[x[0] + 1];
+    iv.push_back(x[1]);
+    iv.push_back(x[2]);
+  }
+  for (int32_t j = 0; j < T; ++j) iv_ptr[j + 1] += iv_ptr[j];
+  for (int32_t j = 0; j < T; ++j)
+    if (iv_ptr[j + 1] > iv_ptr[j]) omega[j] |= int32_t(0x80000000u);
   return MV_OK;
 }
 
 // Diverging leaves (Definition "trajectory tree", Appendix B.1; Section 5.1):
-// a token t that survives every edit is scored under the live view of row t-1
-// and, on the final compressed walk, under the row of the last surviving
-// token before t.  The two conditioning sets differ iff some key before t is
-// evicted by an edit that fires at row t or later, i.e. iff the largest
-// death row among evicted keys j < t is >= t.  Computed from the live omega.
+// a token t of the final compressed walk is scored under the live view of
+// row t-1 and, on the final walk, under the row of the last surviving token
+// before t.  The two conditioning sets differ iff some key j < t is live at
+// row t-1 but not in the final walk, or (a key that re-entered) in the final
+// walk but not live at row t-1.  A difference array over t counts those keys
+// for every t at once from the keys' intervals.
 void build_leaves(mv_view_mask& m, const mv_trajectory* trajs, int32_t n_traj) {
   m.leaf_token.clear();
   m.leaf_teacher.clear();
   m.leaf_student.clear();
   for (int32_t k = 0; k < n_traj; ++k) {
     const int32_t b = trajs[k].begin, e = trajs[k].end;
-    int32_t latest_death = -1, last_survivor = -1;
+    // diff over t in [b, e]: key j counts at t iff (t-1 live) != (j final)
+    std::vector<int32_t> diff(e - b + 2, 0);
+    auto add = [&](int32_t t0, int32_t t1, int32_t v) {  // t in [t0, t1)
+      if (t0 >= t1) return;
+      diff[t0 - b] += v;
+      diff[t1 - b] -= v;
+    };
+    for (int32_t j = b; j < e; ++j) {
+      const bool final = m.last_end(j) == e;
+      // live at row t-1 for t-1 in an interval [lo, hi): t in [lo+1, hi+1),
+      // restricted to t > j
+      std::vector<std::pair<int32_t, int32_t>> ivs{{j, m.first_end(j)}};
+      for (int32_t q = m.iv_ptr[j]; q < m.iv_ptr[j + 1]; ++q)
+        ivs.push_back({m.iv[2 * q], m.iv[2 * q + 1]});
+      if (final) {
+        // counts where not live: t in (j, e] minus the live ranges
+        add(j + 1, e + 1, 1);
+        for (const auto& iv : ivs) add(iv.first + 1, iv.second + 1, -1);
+      } else {
+        for (const auto& iv : ivs) add(iv.first + 1, iv.second + 1, 1);
+      }
+    }
+    int32_t run = 0, last_survivor = -1;
     for (int32_t t = b + 1; t < e; ++t) {
-      const int32_t j = t - 1;
-      if (m.omega[j] < e)
-        latest_death = std::max(latest_death, m.omega[j]);
-      else
-        last_survivor = j;
-      if (m.omega[t] == e && latest_death >= t && last_survivor >= 0) {
+      run += diff[t - b];
+      if (m.last_end(t - 1) == e) last_survivor = t - 1;
+      if (m.last_end(t) == e && run > 0 && last_survivor >= 0) {
         m.leaf_token.push_back(t);
         m.leaf_teacher.push_back(t - 1);
         m.leaf_student.push_back(last_survivor);
@@ -118,9 +214,14 @@ void build_stats(mv_view_mask& m) {
   std::vector<int32_t> diff(T + 1, 0);
   int32_t segs = 0;
   for (int32_t j = 0; j < T; ++j) {
-    pairs += m.omega[j] - j;
+    pairs += m.first_end(j) - j;
     diff[j] += 1;
-    diff[m.omega[j]] -= 1;
+    diff[m.first_end(j)] -= 1;
+    for (int32_t q = m.iv_ptr[j]; q < m.iv_ptr[j + 1]; ++q) {
+      pairs += m.iv[2 * q + 1] - m.iv[2 * q];
+      diff[m.iv[2 * q]] += 1;
+      diff[m.iv[2 * q + 1]] -= 1;
+    }
     if (j == 0 || m.omega[j] != m.omega[j - 1]) ++segs;
   }
   int32_t run = 0, mx = 0;
@@ -140,10 +241,13 @@ void build_fwd_schedule(mv_view_mask& m) {
   m.n_qt = (T + BQ - 1) / BQ;
   m.kt_minmax.resize(2 * size_t(m.n_kt64));
   for (int32_t kt = 0; kt < m.n_kt64; ++kt) {
+    // lo: the first row some key of the tile is not live at (full tiles end
+    // there); hi: the end of the last live interval of any key (no row from
+    // there on sees the tile)
     int32_t lo = INT32_MAX, hi = 0;
     for (int32_t j = kt * BK; j < std::min(T, (kt + 1) * BK); ++j) {
-      lo = std::min(lo, m.omega[j]);
-      hi = std::max(hi, m.omega[j]);
+      lo = std::min(lo, m.first_end(j));
+      hi = std::max(hi, m.last_end(j));
     }
     m.kt_minmax[2 * kt] = lo;
     m.kt_minmax[2 * kt + 1] = hi;
@@ -198,8 +302,8 @@ void build_bwd_schedule(mv_view_mask& m) {
     const int32_t j0 = kt * BK, j1 = std::min(T, j0 + BK);
     int32_t lo = INT32_MAX, hi = 0;
     for (int32_t j = j0; j < j1; ++j) {
-      lo = std::min(lo, m.omega[j]);
-      hi = std::max(hi, m.omega[j]);
+      lo = std::min(lo, m.first_end(j));
+      hi = std::max(hi, m.last_end(j));
     }
     // rows seeing some key of the tile form the contiguous range [j0, hi)
     const int32_t qb0 = j0 / BQ, qb1 = (hi + BQ - 1) / BQ;
@@ -230,10 +334,11 @@ void build_bwd_schedule(mv_view_mask& m) {
 }
 
 void layout_device(mv_view_mask& m) {
-  const std::vector<int32_t>* arrs[8] = {&m.omega,  &m.kt_minmax, &m.q_ptr,     &m.k_list,
-                                         &m.qt_order, &m.bwd_items, &m.bwd_tiles, &m.bwd_red};
+  const std::vector<int32_t>* arrs[10] = {&m.omega,     &m.kt_minmax, &m.q_ptr,    &m.k_list,
+                                          &m.qt_order,  &m.bwd_items, &m.bwd_tiles, &m.bwd_red,
+                                          &m.iv_ptr,    &m.iv};
   size_t off = 0;
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < 10; ++i) {
     m.off[i] = off;
     off = align256(off + std::max<size_t>(1, arrs[i]->size()) * sizeof(int32_t));
   }
@@ -257,18 +362,21 @@ mv_status mv_build_view_mask_kind(const mv_trajectory* trajs, int32_t n_traj,
     auto* m = new mv_view_mask();
     m->T = total_tokens;
     m->kind = kind;
-    mv_status s = validate_and_fill_omega(trajs, n_traj, total_tokens, m->omega);
+    mv_status s =
+        validate_and_fill_lifetimes(trajs, n_traj, total_tokens, m->omega, m->iv_ptr, m->iv);
     if (s != MV_OK) {
       delete m;
       return s;
     }
     build_leaves(*m, trajs, n_traj);
     if (kind == MV_VIEW_FINAL) {
-      // the final compressed walk applies every edit: an evicted key is seen
-      // by its own row only
+      // the final compressed walk applies every edit: a key of the final walk
+      // is seen by every later row, any other key by its own row only
       for (int32_t t = 0; t < n_traj; ++t)
         for (int32_t j = trajs[t].begin; j < trajs[t].end; ++j)
-          if (m->omega[j] < trajs[t].end) m->omega[j] = j + 1;
+          m->omega[j] = m->last_end(j) == trajs[t].end ? trajs[t].end : j + 1;
+      std::fill(m->iv_ptr.begin(), m->iv_ptr.end(), 0);
+      m->iv.clear();
     }
     build_stats(*m);
     build_fwd_schedule(*m);
@@ -317,11 +425,12 @@ mv_status mv_view_mask_upload(mv_view_mask* m, void* dev_buf, size_t bytes, hipS
     os << "mask buffer has " << bytes << " bytes, needs " << m->bytes;
     return bad(MV_ERR_WORKSPACE, os.str());
   }
-  const std::vector<int32_t>* arrs[8] = {&m->omega,    &m->kt_minmax, &m->q_ptr,
-                                         &m->k_list,   &m->qt_order,  &m->bwd_items,
-                                         &m->bwd_tiles, &m->bwd_red};
+  const std::vector<int32_t>* arrs[10] = {&m->omega,     &m->kt_minmax, &m->q_ptr,
+                                          &m->k_list,    &m->qt_order,  &m->bwd_items,
+                                          &m->bwd_tiles, &m->bwd_red,   &m->iv_ptr,
+                                          &m->iv};
   char* base = static_cast<char*>(dev_buf);
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < 10; ++i) {
     if (arrs[i]->empty()) continue;
     hipError_t e = hipMemcpyAsync(base + m->off[i], arrs[i]->data(),
                                   arrs[i]->size() * sizeof(int32_t), hipMemcpyHostToDevice, stream);
@@ -332,7 +441,7 @@ mv_status mv_view_mask_upload(mv_view_mask* m, void* dev_buf, size_t bytes, hipS
   m->dev = dev_buf;
   m->device = dev;
   auto at = [&](int i) { return reinterpret_cast<const int32_t*>(base + m->off[i]); };
-  m->d = mv_mask_dev{at(0), at(1), at(2), at(3), at(4), at(5), at(6), at(7)};
+  m->d = mv_mask_dev{at(0), at(1), at(2), at(3), at(4), at(5), at(6), at(7), at(8), at(9)};
   return MV_OK;
 }
 
@@ -344,7 +453,19 @@ mv_status mv_view_mask_stats(const mv_view_mask* m, mv_mask_stats* out) {
 
 mv_status mv_view_mask_death(const mv_view_mask* m, int32_t* host_out) {
   if (m == nullptr || host_out == nullptr) return bad(MV_ERR_INVALID_ARG, "null argument");
-  std::memcpy(host_out, m->omega.data(), m->omega.size() * sizeof(int32_t));
+  for (int32_t j = 0; j < m->T; ++j) host_out[j] = m->first_end(j);
+  return MV_OK;
+}
+
+mv_status mv_view_mask_intervals(const mv_view_mask* m, int32_t* iv_ptr, int32_t* iv,
+                                 int32_t capacity, int32_t* n_out) {
+  if (m == nullptr || n_out == nullptr) return bad(MV_ERR_INVALID_ARG, "null argument");
+  const int32_t n = int32_t(m->iv.size() / 2);
+  *n_out = n;
+  if (iv_ptr != nullptr) std::copy(m->iv_ptr.begin(), m->iv_ptr.end(), iv_ptr);
+  if (iv == nullptr) return MV_OK;
+  if (capacity < n) return bad(MV_ERR_WORKSPACE, "interval array smaller than the interval count");
+  std::copy(m->iv.begin(), m->iv.end(), iv);
   return MV_OK;
 }
 
@@ -362,7 +483,7 @@ mv_status mv_view_mask_materialize_host(const mv_view_mask* m, int32_t row_begin
       const int32_t kt = m->k_list[e] >> 1;
       const bool full = m->k_list[e] & 1;
       for (int32_t j = kt * mv::kFwdTileK; j < std::min(T, (kt + 1) * mv::kFwdTileK); ++j)
-        if (full || mv_visible(i, j, m->omega[j])) row[j >> 5] |= 1u << (j & 31);
+        if (full || m->visible(i, j)) row[j >> 5] |= 1u << (j & 31);
     }
   }
   return MV_OK;
@@ -371,3 +492,7 @@ mv_status mv_view_mask_materialize_host(const mv_view_mask* m, int32_t row_begin
 void mv_view_mask_free(mv_view_mask* m) { delete m; }
 
 }  // extern "C"
+
+bool mv_view_mask::visible(int32_t i, int32_t j) const {
+  return mv_visible_iv(i, j, omega[j], iv_ptr.data(), iv.data());
+}

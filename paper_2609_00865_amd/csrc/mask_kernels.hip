@@ -35,7 +35,7 @@ __global__ void materialize_kernel(mv_mask_dev mk, int T, int row_begin, int row
     for (int b = 0; b < 32; ++b) {
       const int j = w * 32 + b;
       if (j >= T) break;
-      if (full || mv_visible(i, j, mk.omega[j])) out |= 1u << b;
+      if (full || mv_visible_iv(i, j, mk.omega[j], mk.iv_ptr, mk.iv)) out |= 1u << b;
     }
   }
   bits[gid] = out;

@@ -52,6 +52,8 @@ struct mv_mask_dev {
   const int32_t* bwd_items;  // [n_items * 4] (kt128, qb_begin, qb_end, slot)
   const int32_t* bwd_tiles;  // [n_kt128 * 4] (min omega, max omega, first slot, n slots)
   const int32_t* bwd_red;    // [n_red] key tiles whose partials are reduced
+  const int32_t* iv_ptr;     // [T + 1] per-key ranges of further live intervals
+  const int32_t* iv;         // [2 * n_iv] (begin, end) of those intervals
 };
 
 struct mv_view_mask {
@@ -59,16 +61,23 @@ struct mv_view_mask {
   int32_t n_qt = 0, n_kt64 = 0, n_kt128 = 0;
   std::vector<int32_t> omega, kt_minmax, q_ptr, k_list, qt_order;
   std::vector<int32_t> bwd_items, bwd_tiles, bwd_red;
+  std::vector<int32_t> iv_ptr, iv;  // further live intervals of restored keys
   int32_t n_slots = 0;
   int32_t kind = MV_VIEW_LIVE;
   std::vector<int32_t> leaf_token, leaf_teacher, leaf_student;  // diverging leaves
   mv_mask_stats stats{};
   // device copy
-  size_t off[8] = {0};
+  size_t off[10] = {0};
   size_t bytes = 0;
   void* dev = nullptr;
   int device = -1;
   mv_mask_dev d{};
+  int32_t first_end(int32_t j) const { return omega[j] & 0x7fffffff; }
+  // end of the key's last live interval
+  int32_t last_end(int32_t j) const {
+    return iv_ptr[j + 1] > iv_ptr[j] ? iv[2 * (iv_ptr[j + 1] - 1) + 1] : first_end(j);
+  }
+  bool visible(int32_t i, int32_t j) const;
 };
 
 struct mv_branch_pack {

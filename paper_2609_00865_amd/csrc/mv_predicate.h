@@ -13,3 +13,18 @@
 #endif
 
 MV_HD bool mv_visible(int i, int j, int omega_j) { return j <= i && i < omega_j; }
+
+// A key that a later edit restores has further live intervals.  Such a key is
+// stored with the sign bit of omega set (the low 31 bits keep the end of its
+// first interval) and its other intervals [b, e) in a per-key list: iv[2k],
+// iv[2k + 1] for k in [iv_ptr[j], iv_ptr[j + 1]).  For every other key this is
+// the single-interval test above.
+MV_HD int mv_first_end(int omega_j) { return omega_j & 0x7fffffff; }
+
+MV_HD bool mv_visible_iv(int i, int j, int omega_j, const int* iv_ptr, const int* iv) {
+  if (omega_j >= 0) return j <= i && i < omega_j;
+  if (j <= i && i < mv_first_end(omega_j)) return true;
+  for (int k = iv_ptr[j]; k < iv_ptr[j + 1]; ++k)
+    if (iv[2 * k] <= i && i < iv[2 * k + 1]) return true;
+  return false;
+}

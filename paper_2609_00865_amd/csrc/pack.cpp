@@ -1,9 +1,10 @@
 // Host construction of the branch-replicated packing (Appendix G): one
 // segment per branch layer (Appendix B.1), holding the keys live just before
 // the layer's first row and then the layer's rows, with position ids that
-// restart per segment.  The live keys before row J are those j < J whose
-// lifetime omega(j) (Eq. "4d-mask-def") extends past J; no edit fires inside
-// a layer, so causal attention over the segment reproduces every row's view.
+// restart per segment.  The live keys before row J are the keys j < J whose
+// lifetime (Eq. "4d-mask-def"; several intervals for a key that an edit
+// restores) holds row J; no edit fires inside a layer, so causal attention
+// over the segment reproduces every row's view.
 #include <algorithm>
 #include <sstream>
 
@@ -48,7 +49,6 @@ mv_status mv_build_branch_pack(const mv_trajectory* trajs, int32_t n_traj, int32
     return st;
   try {
     auto* p = new mv_branch_pack();
-    const std::vector<int32_t>& omega = live->omega;
     p->T = total_tokens;
     p->seg_begin.push_back(0);
     int64_t pairs = 0;
@@ -61,7 +61,7 @@ mv_status mv_build_branch_pack(const mv_trajectory* trajs, int32_t n_traj, int32
         const int32_t first = bounds[k], end = bounds[k + 1];
         int32_t p_in_seg = 0;
         for (int32_t j = tr.begin; j < first; ++j) {
-          if (omega[j] <= first) continue;  // evicted by row `first`
+          if (!live->visible(first, j)) continue;  // not in row `first`'s view
           p->src.push_back(j);
           p->pos.push_back(p_in_seg++);
           p->owner.push_back(0);

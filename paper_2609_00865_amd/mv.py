@@ -41,7 +41,8 @@ class Span(ctypes.Structure):
 
 class EditC(ctypes.Structure):
     _fields_ = [("junction", ctypes.c_int32), ("n_evict", ctypes.c_int32),
-                ("evict", ctypes.POINTER(Span)), ("summary", Span)]
+                ("evict", ctypes.POINTER(Span)), ("summary", Span),
+                ("n_restore", ctypes.c_int32), ("restore", ctypes.POINTER(Span))]
 
 
 class TrajectoryC(ctypes.Structure):
@@ -117,6 +118,8 @@ mv_build_view_mask_kind = _sig("mv_build_view_mask_kind", ctypes.c_int, _P(Traje
                                _i32, _i32, _P(_vp))
 mv_view_mask_leaves = _sig("mv_view_mask_leaves", ctypes.c_int, _vp, _vp, _vp, _vp, _i32,
                            _P(_i32))
+mv_view_mask_intervals = _sig("mv_view_mask_intervals", ctypes.c_int, _vp, _vp, _vp, _i32,
+                              _P(_i32))
 mv_view_mask_device_bytes = _sig("mv_view_mask_device_bytes", _sz, _vp)
 mv_view_mask_upload = _sig("mv_view_mask_upload", ctypes.c_int, _vp, _vp, _sz, _vp)
 mv_view_mask_stats = _sig("mv_view_mask_stats", ctypes.c_int, _vp, _P(MaskStats))
@@ -181,6 +184,7 @@ EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_ma
             "mv_branch_pack_stats", "mv_branch_pack_layout", "mv_branch_pack_mask",
             "mv_branch_pack_device_bytes", "mv_branch_pack_upload", "mv_branch_pack_free",
             "mv_pack_rows", "mv_unpack_rows_sum", "mv_rope", "mv_token_logprob_dweight",
+            "mv_view_mask_intervals",
             "mv_profile_enable", "mv_profile_read"]
 
 VIEW_LIVE, VIEW_FINAL = 0, 1
@@ -222,9 +226,14 @@ def _trajectories_c(trajectories: Sequence):
             for si, (b, x) in enumerate(e.evict):
                 spans[si] = Span(int(b), int(x))
             keep.append(spans)
+            rest = tuple(getattr(e, "restore", ()))
+            rspans = (Span * max(1, len(rest)))()
+            for si, (b, x) in enumerate(rest):
+                rspans[si] = Span(int(b), int(x))
+            keep.append(rspans)
             summ = getattr(e, "summary", (0, 0))
             edits[ei] = EditC(int(e.junction), len(e.evict), spans,
-                              Span(int(summ[0]), int(summ[1])))
+                              Span(int(summ[0]), int(summ[1])), len(rest), rspans)
         keep.append(edits)
         trajs[ti] = TrajectoryC(int(t.begin), int(t.end), len(t.edits), edits)
     return trajs, keep
@@ -283,6 +292,15 @@ class ViewMask:
         check(mv_view_mask_leaves(self._h, _ptr(out[0]), _ptr(out[1]), _ptr(out[2]), n.value,
                                   ctypes.byref(n)))
         return tuple(out)
+
+    def intervals(self):
+        """(iv_ptr [T + 1], iv [n, 2]): further live intervals of restored keys."""
+        n = ctypes.c_int32()
+        ptr = torch.empty(self.total_tokens + 1, dtype=torch.int32)
+        check(mv_view_mask_intervals(self._h, _ptr(ptr), None, 0, ctypes.byref(n)))
+        iv = torch.empty(max(1, 2 * n.value), dtype=torch.int32)
+        check(mv_view_mask_intervals(self._h, None, _ptr(iv), n.value, ctypes.byref(n)))
+        return ptr, iv[:2 * n.value].view(-1, 2)
 
     def device_bytes(self) -> int:
         return int(mv_view_mask_device_bytes(self._h))

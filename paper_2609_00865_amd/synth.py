@@ -48,6 +48,7 @@ class Edit:
     junction: int                 # J_k: first row evaluated under the post-edit view
     evict: Tuple[Span, ...]       # E_k as disjoint, sorted, half-open physical spans
     summary: Span = (0, 0)        # metadata only; (b, b) means none
+    restore: Tuple[Span, ...] = ()  # earlier-evicted spans live again from J_k on
 
 
 @dataclass(frozen=True)
@@ -146,6 +147,15 @@ class _LiveTracker:
         for p in positions:
             assert self.alive[p - self.begin]
             self.alive[p - self.begin] = False
+
+    def dead_before(self, junction: int) -> np.ndarray:
+        idx = np.nonzero(~self.alive[: junction - self.begin])[0]
+        return idx + self.begin
+
+    def revive(self, positions: Sequence[int]) -> None:
+        for p in positions:
+            assert not self.alive[p - self.begin]
+            self.alive[p - self.begin] = True
 
     def protect(self, b: int, e: int) -> None:
         self.protected[b - self.begin: e - self.begin] = True
@@ -254,8 +264,12 @@ def make_trajectories(workload: str, seed: int = 0) -> List[Trajectory]:
 
 def random_trajectories(rng: np.random.Generator, lengths: Sequence[int],
                         max_edits: int = 4, max_span: int = 6,
-                        summary_max: int = 3) -> List[Trajectory]:
-    """Small random trajectories for property tests (any valid record)."""
+                        summary_max: int = 3, restore_max: int = 0) -> List[Trajectory]:
+    """Small random trajectories for property tests (any valid record).
+
+    With restore_max > 0 an edit may also bring back up to that many tokens
+    evicted by earlier edits (offload / retrieve, keys with several live
+    intervals); a token is never evicted and restored by the same edit."""
     out, b = [], 0
     for n in lengths:
         tr = _LiveTracker(b, b + n)
@@ -263,12 +277,16 @@ def random_trajectories(rng: np.random.Generator, lengths: Sequence[int],
         js = sorted(set(int(x) for x in rng.integers(b + 1, b + n, size=k))) if k else []
         edits = []
         for J in js:
+            dead = tr.dead_before(J)
+            n_rs = int(rng.integers(0, min(restore_max, len(dead)) + 1)) if restore_max else 0
+            rs = sorted(rng.choice(dead, size=n_rs, replace=False).tolist()) if n_rs else []
             view = tr.live_before(J)
             n_ev = int(rng.integers(0, min(max_span, len(view)) + 1))
             ev = sorted(rng.choice(view, size=n_ev, replace=False).tolist()) if n_ev else []
             tr.kill(ev)
+            tr.revive(rs)
             s = int(rng.integers(0, summary_max + 1))
-            edits.append(Edit(J, _to_spans(ev), (J, min(J + s, b + n))))
+            edits.append(Edit(J, _to_spans(ev), (J, min(J + s, b + n)), _to_spans(rs)))
         out.append(Trajectory(b, b + n, tuple(edits)))
         b += n
     return out

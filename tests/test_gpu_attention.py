@@ -89,6 +89,25 @@ def test_ragged_packed(d, hq, hkv, lens, seed):
     _check_full(trajs, q, k, v, do, f"ragged{lens}/d{d}")
 
 
+@pytest.mark.parametrize("d,lens,seed", [(128, [700, 450, 301], 31), (64, [1200, 257], 32)])
+def test_keys_that_re_enter(d, lens, seed):
+    """Offload / retrieve records: evicted keys restored by later edits have
+    several live intervals; every row must still attend exactly its view.
+    The device mask bits are checked too (kernels share the predicate)."""
+    rng = np.random.default_rng(seed)
+    trajs = synth.random_trajectories(rng, lens, max_edits=10, max_span=80, summary_max=20,
+                                      restore_max=60)
+    assert any(e.restore for t in trajs for e in t.edits)
+    T = trajs[-1].end
+    gen = torch.Generator().manual_seed(seed)
+    q, do = (torch.randn(T, 4, d, generator=gen).to(torch.bfloat16) for _ in range(2))
+    k, v = (torch.randn(T, 2, d, generator=gen).to(torch.bfloat16) for _ in range(2))
+    _check_full(trajs, q, k, v, do, f"restores{lens}/d{d}")
+    m = mv.ViewMask(trajs).upload()
+    dev = mv.unpack_bits(m.materialize(0, T).cpu(), T)
+    assert torch.equal(dev, OA.visibility(trajs))
+
+
 def test_no_compression_is_causal():
     T, hq, hkv, d = 700, 4, 1, 128
     gen = torch.Generator().manual_seed(11)

@@ -105,6 +105,28 @@ def test_packed_attention_forward_backward():
     assert_bf16_close(dV, rdV, "packed dV summed over copies")
 
 
+def test_packed_attention_with_re_entering_keys():
+    """Packing a record whose keys leave and re-enter: every layer's segment
+    copies the keys live at its start (restored ones at their own slots)."""
+    rng = np.random.default_rng(41)
+    trajs = synth.random_trajectories(rng, [600, 333], max_edits=8, max_span=60,
+                                      summary_max=10, restore_max=50)
+    T = trajs[-1].end
+    gen = torch.Generator().manual_seed(41)
+    q = torch.randn(T, 2, 64, generator=gen).to(BF)
+    k, v = (torch.randn(T, 1, 64, generator=gen).to(BF) for _ in range(2))
+    pk = mv.BranchPack(trajs).upload()
+    lay = pk.layout()
+    own = lay["owner"].bool()
+    print(f"[gpu] packed attention with restores T={T} N={pk.n_packed}", flush=True)
+    o, _ = mv.attn_fwd(pk.mask, *(mv.pack_rows(pk, x.cuda()) for x in (q, k, v)))
+    torch.cuda.synchronize()
+    O, _ = OA.logittree(trajs, q.to(F64), k.to(F64), v.to(F64))
+    got = torch.zeros_like(O)
+    got[lay["src"].long()[own]] = o.cpu()[own].double()
+    assert_bf16_close(got, O, "packed O with restores")
+
+
 def _bf(x):
     return x.to(BF)
 

@@ -122,7 +122,15 @@ def test_record_errors():
     assert _err([Tr(0, 5)], T=6).name == "MV_ERR_BAD_RECORD"                           # does not cover T
     assert _err([Tr(0, 10, (E(8, ((1, 1),)),))]).name == "MV_ERR_BAD_RECORD"           # empty span
     msg = str(_err([Tr(0, 10, (E(4, ((1, 2),)), E(6, ((1, 2),))))]))
-    assert "already left the view" in msg
+    assert "not live" in msg
+    # restores: only a token that is out of the view may come back, not in the
+    # edit that evicts it, and only from before the junction
+    assert _err([Tr(0, 10, (E(4, (), restore=((1, 2),)),))]).name == "MV_ERR_BAD_RECORD"
+    assert _err([Tr(0, 10, (E(4, ((1, 2),), restore=((1, 2),)),))]).name == "MV_ERR_BAD_RECORD"
+    assert _err([Tr(0, 10, (E(4, ((1, 2),)), E(6, (), restore=((1, 3),))))]).name == "MV_ERR_BAD_RECORD"
+    assert _err([Tr(0, 10, (E(4, ((1, 2),)), E(6, (), restore=((7, 8),))))]).name == "MV_ERR_BAD_RECORD"
+    assert _err([Tr(0, 10, (E(4, ((1, 2),)), E(6, (), restore=((1, 2),)),
+                            E(8, (), restore=((1, 2),))))]).name == "MV_ERR_BAD_RECORD"
 
 
 def test_empty_edit_and_summary_only_edits():
@@ -155,3 +163,38 @@ def test_ragged_tail_tiles_are_never_full(T):
     assert st["tiles_full"] == full
     assert st["tiles_full"] + st["tiles_partial"] == causal
     assert _bits_ok(m, [synth.Trajectory(0, T, ())])
+
+
+def test_restore_hand_example():
+    """y1, y2 evicted at row 4; y1 restored at row 7: rows 4-6 see neither,
+    rows 7-9 see y1 again (at its own position), y2 never comes back."""
+    E, Tr = synth.Edit, synth.Trajectory
+    trajs = [Tr(0, 10, (E(4, ((1, 3),)), E(7, (), restore=((1, 2),))))]
+    m = mv.ViewMask(trajs)
+    assert m.death().tolist() == [10, 4, 4] + [10] * 7
+    ptr, iv = m.intervals()
+    assert ptr.tolist() == [0, 0, 1] + [1] * 8 and iv.tolist() == [[7, 10]]
+    assert V.lifetimes(trajs[0])[1] == [(1, 4), (7, 10)]
+    assert _bits_ok(m, trajs)
+    views = V.views(trajs[0])
+    assert views[5] == frozenset({0, 3, 4, 5}) and views[8] == frozenset({0, 1, 3, 4, 5, 6, 7, 8})
+    assert m.stats()["visible_pairs"] == sum(len(v) for v in views)
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_random_records_with_restores(seed):
+    rng = np.random.default_rng(7000 + seed)
+    lens = [int(x) for x in rng.integers(2, 300, size=int(rng.integers(1, 4)))]
+    trajs = synth.random_trajectories(rng, lens, max_edits=10, max_span=40, summary_max=10,
+                                      restore_max=30)
+    m = mv.ViewMask(trajs)
+    assert torch.equal(m.death(), _oracle_death(trajs))
+    ptr, iv = m.intervals()
+    want = [ivs[1:] for tr in trajs for ivs in V.lifetimes(tr)]
+    got = [iv[ptr[j]:ptr[j + 1]].tolist() for j in range(trajs[-1].end)]
+    assert got == [[list(x) for x in w] for w in want]
+    assert _bits_ok(m, trajs)
+    sizes = [s for t in trajs for s in V.view_sizes(t)]
+    st = m.stats()
+    assert st["visible_pairs"] == sum(sizes) and st["max_view"] == max(sizes)
+

@@ -101,6 +101,19 @@ def test_logittree_equals_dense_union(seed):
         assert torch.allclose(x, y, atol=1e-12, rtol=0)
 
 
+@pytest.mark.parametrize("seed", range(4))
+def test_logittree_equals_dense_union_with_restores(seed):
+    """Keys that leave and re-enter: the per-branch forwards and the masked
+    union still agree (each row attends exactly to its view)."""
+    trajs = _random_trajs(60 + seed, [90, 70], max_edits=6, max_span=15, restore_max=10)
+    T = trajs[-1].end
+    q, k, v, do = _rand(T, 2, 1, 8, seed)
+    a = A.logittree(trajs, q, k, v, dout=do)
+    b = A.dense(trajs, q, k, v, dout=do)
+    for x, y in zip(a, b):
+        assert torch.allclose(x, y, atol=1e-12, rtol=0)
+
+
 def test_logittree_row_chunking_and_heads():
     trajs = synth.make_trajectories("tiny", 1)
     q, k, v, do = _rand(512, 2, 1, 8, 5)

@@ -207,3 +207,26 @@ def test_lambda_schedule():
         for total in [1, 10, 1000]:
             assert abs(mv.sdcc_lambda(step, total) - OS.kl_weight(step, total)) < 1e-6
     assert mv.sdcc_lambda(5, 10, 0.1, 0.0) == pytest.approx(0.1)
+
+
+@pytest.mark.parametrize("seed", range(15))
+def test_library_leaves_and_final_walk_with_restores(seed):
+    """With keys that leave and re-enter (offload / retrieve), a surviving
+    token diverges when its live prefix and its final-walk prefix differ in
+    either direction; the final-walk mask keeps exactly the final walk."""
+    rng = np.random.default_rng(2600 + seed)
+    lens = [int(x) for x in rng.integers(2, 300, size=int(rng.integers(1, 4)))]
+    trajs = synth.random_trajectories(rng, lens, max_edits=10, max_span=40, summary_max=8,
+                                      restore_max=30)
+    want = OS.packed_leaves(trajs)
+    m = mv.ViewMask(trajs, kind=mv.VIEW_FINAL)
+    tok, tea, stu = m.leaves()
+    assert list(zip(tok.tolist(), tea.tolist(), stu.tolist())) == want
+    T = trajs[-1].end
+    bits = mv.unpack_bits(m.materialize_host(0, T), T)
+    ref = torch.zeros(T, T, dtype=torch.bool)
+    for tr in trajs:
+        for r, vis in zip(range(tr.begin, tr.end), V.naive_views(tr, "compressed")):
+            ref[r, list(vis)] = True
+    assert torch.equal(bits, ref)
+

@@ -89,9 +89,12 @@ def _check_against_definition(trajs):
             d = V.view_by_definition(t, r)
             assert vs[r - t.begin] == d
             assert len(d) == V.view_sizes(t)[r - t.begin]
+        life = V.lifetimes(t)
         for j in range(t.begin, t.end):
             seen = [r for r in range(t.begin, t.end) if j in vs[r - t.begin]]
-            assert seen == list(range(j, death[j - t.begin]))
+            ivs = life[j - t.begin]
+            assert seen == [r for b, e in ivs for r in range(b, e)]
+            assert ivs[0][0] == j and death[j - t.begin] == ivs[0][1]
 
 
 @pytest.mark.parametrize("seed", range(20))
@@ -106,6 +109,29 @@ def test_replay_matches_definition(seed):
 def test_replay_matches_definition_hypothesis(seed, lengths):
     rng = np.random.default_rng(seed)
     _check_against_definition(synth.random_trajectories(rng, lengths, max_edits=5))
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_replay_matches_definition_with_restores(seed):
+    rng = np.random.default_rng(100 + seed)
+    trajs = synth.random_trajectories(rng, [int(x) for x in rng.integers(3, 60, size=3)],
+                                      max_edits=8, max_span=10, restore_max=8)
+    _check_against_definition(trajs)
+    for t in trajs:
+        live = V.views(t)
+        for j, ivs in zip(range(t.begin, t.end), V.lifetimes(t)):
+            rows = {r for r in range(t.begin, t.end) if j in live[r - t.begin]}
+            assert rows == {r for b, e in ivs for r in range(b, e)}
+            assert all(e < b2 for (_, e), (b2, _) in zip(ivs, ivs[1:]))   # disjoint, gaps
+
+
+def test_restore_re_enters_in_physical_order():
+    t = synth.Trajectory(0, 9, (synth.Edit(3, ((0, 2),)), synth.Edit(6, (), restore=((1, 2),))))
+    rows = {r: list(lv) for r, lv in V.replay(t)}
+    assert rows[5] == [2, 3, 4, 5]
+    assert rows[6] == [1, 2, 3, 4, 5, 6]          # y1 back at its own slot
+    with pytest.raises(V.BadRecord):
+        list(V.replay(synth.Trajectory(0, 9, (synth.Edit(3, (), restore=((1, 2),)),))))
 
 
 def _budget(t):

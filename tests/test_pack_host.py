@@ -43,6 +43,14 @@ def test_random_records(seed):
     _check(synth.random_trajectories(rng, lens, max_edits=8, max_span=40, summary_max=10))
 
 
+@pytest.mark.parametrize("seed", range(10))
+def test_random_records_with_restores(seed):
+    rng = np.random.default_rng(5000 + seed)
+    lens = [int(x) for x in rng.integers(2, 300, size=int(rng.integers(1, 4)))]
+    _check(synth.random_trajectories(rng, lens, max_edits=8, max_span=40, summary_max=8,
+                                     restore_max=25))
+
+
 def test_no_edits_is_the_identity_layout():
     trajs = [synth.Trajectory(0, 50, ()), synth.Trajectory(50, 51, ())]
     pk = _check(trajs)
