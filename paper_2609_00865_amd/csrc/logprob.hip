@@ -1,26 +1,33 @@
 // Fused LM-head token log-prob, ratio and clip on gfx950.
 //
 // Forward: z = W h is produced 256 vocab rows x 256 tokens at a time by a bf16
-// MFMA tile engine and reduced in registers to a per-token (max, sum of
-// exp) over each wave's 128 vocab rows; the target logit is captured by the
-// one lane that owns it.  The full logits are never stored.  A combine pass
-// merges the partials into logsumexp and writes logp, ratio and the clipped
-// ratio (the GRPO ratio of Appendix C, "Pitfall A, RL view").
+// MFMA tile engine and reduced in registers to a per-token (max, sum of exp)
+// over each wave's 128 vocab rows; the full logits are never stored.  The
+// target logit z_{t,y_t} comes from a per-token fp32 dot product, and a
+// combine pass merges the partials into logsumexp and writes logp, ratio and
+// the clipped ratio (the GRPO ratio of Appendix C, "Pitfall A, RL view").
 //
 // Backward: the logits tile is recomputed and turned into
-// G_tv = g_t (onehot(y_t)_v - softmax(z_t)_v), stored once in bf16, and a
-// second pass of the same engine computes dH = G W (contraction over the
-// vocabulary).
+// G_tv = g_t (onehot(y_t)_v - softmax(z_t)_v), stored once in bf16 (the tile
+// writes -g_t softmax(z_t)_v everywhere, the per-token pass then rewrites the
+// target entry), and a second pass of the same engine computes dH = G W from
+// a transposed copy of W, so that both operands run along the vocabulary.
+// dW = G^T H contracts over tokens, along which neither operand is
+// contiguous: it has an engine of its own that stages both operands k-major
+// and reads them with the transposing LDS read.
 //
-// Tile engine: 512 threads = 8 waves (two per SIMD) in a 2 x 4 grid over a
-// 256 A-row x 256 token tile; each wave owns 128 A-rows x 64 tokens (tokens on
-// lanes), MFMA 32x32x16 (the dH pass reads its W^T operand from a row-major W
-// slice with the transposing LDS read).  The 64-wide k slices are double-buffered in LDS with
-// one barrier per slice: while a slice is multiplied, the next one is written
-// from registers into the other buffer and the one after is loaded from HBM.
-// Tiles are ordered so that the blocks resident on one XCD at a time form a
-// compact 2-D patch (a few token tiles x several A tiles) and share operand
-// slices in that XCD's L2.
+// Tile engine (logits, G, the KL passes, dH): 512 threads = 8 waves (two per
+// SIMD) in a 2 x 4 grid over a 256 A-row x 256 token tile; each wave owns 128
+// A rows x 64 tokens and runs MFMA 16x16x32.  64-wide k slices go from HBM
+// straight into LDS (global_load_lds: no register staging and no LDS store
+// instructions), two slices in flight, one barrier per slice; the next k
+// step's operand fragments are read while the current step's MFMAs run.  An
+// operand slice sits in LDS as [256 rows][64] bf16 without padding, with
+// 16-byte chunk c of row r at chunk position c ^ (r & 7): the fragment reads
+// (16 lanes = 16 consecutive rows at one chunk) hit distinct banks.  Tiles are
+// ordered so that the blocks resident on one XCD at a time form a compact 2-D
+// patch (a few token tiles x several A tiles) and share operand slices in that
+// XCD's L2.
 #include <algorithm>
 
 #include "mv_device.h"
@@ -29,34 +36,37 @@ namespace mv {
 
 namespace {
 constexpr int BA = 256, BT = 256, BKK = 64;
-constexpr int PAD = BKK + 8;               // LDS row stride (bf16), conflict-free operand reads
-// row stride of the row-major W slice of the dH pass: 576 bytes, so the four
-// rows one transposing read touches start 16 banks apart
-constexpr int WPAD = BA + 32;
-constexpr int STAGE = (BA + BT) * PAD;     // one k slice of both operands
-static_assert(BKK * WPAD <= BA * PAD, "dH pass W slice must fit the A region");
-static_assert(BKK * WPAD <= BT * PAD, "dW pass hidden slice must fit the token region");
-constexpr int NWAVES = 8;                 // waves per tile (2 x NWAVES/2 grid)
+constexpr int NWAVES = 8;                  // waves per tile (2 x 4 grid)
 constexpr int GROUP_T = 4;                 // token tiles per raster group
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
+// tile engine
+constexpr int SLICE_B = 256 * BKK * 2;             // bytes of one operand's k slice
+constexpr int NLD = SLICE_B / 1024 / NWAVES;       // direct loads per operand, thread and slice
+constexpr int FA = 8, FB = 4;                      // 16-row MFMA blocks per wave: A rows, tokens
+static_assert(NLD * NWAVES * 1024 == SLICE_B, "slice split over the waves");
+// dW engine: k-major slices [64 tokens][256 (+32 pad)] of both operands; the
+// 576-byte row stride puts the four rows one transposing read touches 16 banks apart
+constexpr int WPAD = BA + 32;
+constexpr int DW_STAGE = 2 * BKK * WPAD;           // u16 per stage (both operands)
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int vocab_pad(int V) { return (V + BA - 1) / BA * BA; }
 }  // namespace
 
-enum { kModeLogits = 0, kModeGrad = 1, kModeDh = 2, kModeKL = 3, kModeKLGrad = 4, kModeDw = 5 };
+enum { kModeLogits = 0, kModeGrad = 1, kModeDh = 2, kModeKL = 3, kModeKLGrad = 4 };
 
 struct LmArgs {
   const u16* h;       // [T, H]
   const u16* w;       // [V, H]
+  const u16* wT;      // [H, Vp] (dH mode: W transposed, zero past V)
   const int32_t* tgt; // [T]
   const float* lse;   // [T] (grad mode)
   const float* g;     // [T] upstream dlogp (grad mode)
-  const u16* G;       // [T, Vp] (dH mode)
-  u16* Gout;          // [T, Vp] (grad mode)
+  const u16* G;       // [T, Vp] (dH and dW modes)
+  u16* Gout;          // [T, Vp] (grad modes)
   u16* dh;            // [T, H] (dH mode)
   float2* part;       // [T, n_chunks] (logits mode)
-  float* tlogit;      // [T] (logits mode)
+  float* tlogit;      // [T] (target pass)
   // KL modes: token row 2i is leaf i's teacher row, 2i + 1 its student row
   const u16* zero_row; // [H] zeros: the row read for an out-of-range leaf row index
   const u16* hT;      // teacher hidden states [*, H]
@@ -76,53 +86,318 @@ struct LmArgs {
   // writes fp32 partials dh_part[s][t][H], summed in order by dh_reduce_kernel
   int k_split, nk_split;
   float* dh_part;
-  float* dw;          // [V, H] fp32 (dW mode)
+  float* dw;          // [V, H] fp32 (dW)
 };
 
-template <int MODE, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
-  constexpr int NT = NW * 64;              // threads
-  constexpr int WTOK = BT / (NW / 2);      // tokens per wave (2 waves along the A side)
-  constexpr int NJ = WTOK / 32;            // 32-token MFMA blocks per wave
-  constexpr int LDA = (BA * BKK / 8) / NT; // 16-byte loads per thread, A slice
-  constexpr int LDB = (BT * BKK / 8) / NT; // 16-byte loads per thread, token slice
-  __shared__ __align__(16) u16 smem[2 * STAGE];
-
-  // Blocks are dealt to XCDs round-robin; give each XCD a contiguous range of
-  // the rasterised tile order (groups of GROUP_T token tiles x all A tiles).
+// Output tile (a0, t0) and k split of this block.  Blocks are dealt to XCDs
+// round-robin; each XCD gets a contiguous range of the rasterised tile order
+// (groups of GROUP_T token tiles x all A tiles).  False: no tile (grid tail).
+__device__ __forceinline__ bool tile_of(const LmArgs& a, int n_splits, int& a0, int& t0,
+                                        int& split) {
   const int n_out = a.nA * a.nT;
-  const int n_tiles = n_out * (MODE == kModeDh ? a.k_split : 1);
+  const int n_tiles = n_out * n_splits;
   const int per_xcd = (n_tiles + kNumXcd - 1) / kNumXcd;
   int xcd, local;
   xcd_split(xcd, local);
   const int Lx = xcd * per_xcd + local;
-  if (local >= per_xcd || Lx >= n_tiles) return;
-  const int split = Lx / n_out;            // 0 unless the dH product is split
+  if (local >= per_xcd || Lx >= n_tiles) return false;
+  split = Lx / n_out;
   const int L = Lx % n_out;
   const int grp = L / (GROUP_T * a.nA);
   const int rem = L % (GROUP_T * a.nA);
   const int t_in = min(GROUP_T, a.nT - grp * GROUP_T);
-  const int tt = grp * GROUP_T + rem % t_in;
-  const int at = rem / t_in;
-  const int a0 = at * BA, t0 = tt * BT;
+  a0 = (rem / t_in) * BA;
+  t0 = (grp * GROUP_T + rem % t_in) * BT;
+  return true;
+}
 
+template <int MODE>
+__global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
+  __shared__ __align__(1024) u16 smem[2 * 2 * SLICE_B / 2];   // 2 slices x 2 operands
+
+  int a0, t0, split;
+  if (!tile_of(a, MODE == kModeDh ? a.k_split : 1, a0, t0, split)) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wa = wave >> 2, wt = wave & 3;
+
+  // A [a_rows][K] and B [T][K], both contiguous along k
+  const int K = (MODE == kModeDh) ? a.Vp : a.H;
+  const int a_rows = (MODE == kModeDh) ? a.H : a.V;
+  const u16* A = (MODE == kModeDh) ? a.wT : a.w;
+  const int kbeg = (MODE == kModeDh) ? split * a.nk_split : 0;
+  const int nk = (MODE == kModeDh) ? min(K / BKK - kbeg, a.nk_split) : K / BKK;
+
+  // Load i of this wave fills 16-byte slots (i * NWAVES + wave) * 64 + lane of
+  // each operand's slice: row s / 8, k chunk (s % 8) ^ (row & 7).  Rows past
+  // the operands are read from clamped (valid) rows; their products land in
+  // output rows or columns that the epilogues skip.
+  const u16* srcA[NLD];
+  const u16* srcB[NLD];
+#pragma unroll
+  for (int i = 0; i < NLD; ++i) {
+    const int s = (i * NWAVES + wave) * 64 + lane;
+    const int row = s >> 3, kc = (s & 7) ^ (row & 7);
+    const size_t koff = size_t(kbeg) * BKK + kc * 8;
+    srcA[i] = A + size_t(min(a0 + row, a_rows - 1)) * K + koff;
+    const int t = min(t0 + row, a.T - 1);
+    const u16* brow;
+    if (MODE == kModeDh) {
+      brow = a.G + size_t(t) * a.Vp;
+    } else if (MODE == kModeKL || MODE == kModeKLGrad) {
+      // a row index outside its matrix reads as a zero hidden state
+      const int r = (t & 1) ? a.rowsS[t >> 1] : a.rowsT[t >> 1];
+      const int n_rows = (t & 1) ? a.n_rows_S : a.n_rows_T;
+      brow = (r >= 0 && r < n_rows) ? ((t & 1) ? a.hS : a.hT) + size_t(r) * a.H : a.zero_row;
+    } else {
+      brow = a.h + size_t(t) * a.H;
+    }
+    srcB[i] = brow + koff;
+  }
+  typedef __attribute__((address_space(3))) u16 lds_u16;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u16*)smem;   // LDS byte address
+  auto issue = [&](int kk) {
+    const uint32_t st = lds0 + (kk & 1) * (2 * SLICE_B) + wave * 1024;
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      lds_load16(srcA[i] + size_t(kk) * BKK, st + i * NWAVES * 1024);
+      lds_load16(srcB[i] + size_t(kk) * BKK, st + SLICE_B + i * NWAVES * 1024);
+    }
+  };
+
+  const char* lds = reinterpret_cast<const char*>(smem);
+  const int frow = lane & 15, fk = lane >> 4;
+  bf16x8 fa[2][FA], fb[2][FB];
+  // operand fragments of k step ks (0 or 1) of slice kk into register set buf
+  auto read_frags = [&](int buf, int kk, int ks) {
+    const char* sA = lds + (kk & 1) * (2 * SLICE_B);
+    const char* sB = sA + SLICE_B;
+    const int kc = ks * 4 + fk;
+#pragma unroll
+    for (int i = 0; i < FA; ++i) {
+      const int row = wa * 128 + i * 16 + frow;
+      fa[buf][i] = as_bf16x8(ld16(sA + (row * 8 + (kc ^ (row & 7))) * 16));
+    }
+#pragma unroll
+    for (int j = 0; j < FB; ++j) {
+      const int row = wt * 64 + j * 16 + frow;
+      fb[buf][j] = as_bf16x8(ld16(sB + (row * 8 + (kc ^ (row & 7))) * 16));
+    }
+  };
+
+  f32x4 acc[FA][FB];
+#pragma unroll
+  for (int i = 0; i < FA; ++i)
+#pragma unroll
+    for (int j = 0; j < FB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto mma = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < FA; ++i)
+#pragma unroll
+      for (int j = 0; j < FB; ++j) acc[i][j] = mfma16(fa[buf][i], fb[buf][j], acc[i][j]);
+  };
+
+  issue(0);
+  if (nk > 1) {
+    issue(1);
+    wait_vmcnt<2 * NLD>();   // slice 0 landed, slice 1 may still be in flight
+  } else {
+    wait_vmcnt<0>();
+  }
+  __syncthreads();
+  read_frags(0, 0, 0);
+  for (int kk = 0; kk < nk; ++kk) {
+    read_frags(1, kk, 1);
+    mma(0);
+    if (kk + 1 < nk) {
+      // slice kk + 1 is the only one in flight; after the barrier it is
+      // visible to every wave and every wave has read all of slice kk, whose
+      // buffer then takes slice kk + 2
+      wait_vmcnt<0>();
+      __syncthreads();
+      if (kk + 2 < nk) issue(kk + 2);
+      read_frags(0, kk + 1, 0);
+    }
+    mma(1);
+  }
+
+  // acc[i][j][r]: A row rb + i*16 + r, token tb + j*16
+  const int rb = a0 + wa * 128 + (lane >> 4) * 4;
+  const int tb = t0 + wt * 64 + (lane & 15);
+  const bool full_v = a0 + BA <= a.V;  // block-uniform: no vocabulary padding in this tile
+  const int chunk = (a0 + wa * 128) / 128;
+  if (MODE == kModeLogits) {
+#pragma unroll
+    for (int j = 0; j < FB; ++j) {
+      const int t = tb + j * 16;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < FA; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (!full_v && rb + i * 16 + r >= a.V) acc[i][j][r] = -INFINITY;
+          mx = fmaxf(mx, acc[i][j][r]);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m2 = mx * kLog2e;                // -inf for a chunk of padding only
+      const float mu = mx == -INFINITY ? 0.f : m2;
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < FA; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) s += fast_exp2(fmaf(acc[i][j][r], kLog2e, -mu));
+      s += __shfl_xor(s, 16);
+      s += __shfl_xor(s, 32);
+      if (lane < 16 && t < a.T) a.part[size_t(t) * a.n_chunks + chunk] = make_float2(m2, s);
+    }
+  } else if (MODE == kModeGrad) {
+    // -g_t softmax(z_t)_v everywhere (zero in the vocabulary padding); the
+    // target entry gets its one-hot term from lm_target_kernel afterwards
+#pragma unroll
+    for (int j = 0; j < FB; ++j) {
+      const int t = tb + j * 16;
+      if (t >= a.T) continue;
+      const int y = a.tgt[t];
+      const float ng = y >= 0 ? -a.g[t] : 0.f;
+      const float l2 = a.lse[t] * kLog2e;
+      u16* out = a.Gout + size_t(t) * a.Vp + rb;
+#pragma unroll
+      for (int i = 0; i < FA; ++i) {
+        float vals[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          vals[r] = ng * fast_exp2(fmaf(acc[i][j][r], kLog2e, -l2));
+          if (!full_v && rb + i * 16 + r >= a.V) vals[r] = 0.f;
+        }
+        uint2 wv;
+        wv.x = pack2(vals[0], vals[1]);
+        wv.y = pack2(vals[2], vals[3]);
+        *reinterpret_cast<uint2*>(out + i * 16) = wv;
+      }
+    }
+  } else if (MODE == kModeKL) {
+    // lanes c (even, teacher) and c ^ 1 (student) hold the same vocabulary
+    // rows of one leaf; each lane keeps its own (max, sum of exp) and the
+    // teacher also accumulates sum exp(zT - mT) * (zT - zS)
+#pragma unroll
+    for (int j = 0; j < FB; ++j) {
+      const int t = tb + j * 16;
+      const int leaf = t >> 1;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < FA; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (full_v || rb + i * 16 + r < a.V) mx = fmaxf(mx, acc[i][j][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m2 = mx * kLog2e;
+      const float mu = mx == -INFINITY ? 0.f : m2;
+      float sm = 0.f, cross = 0.f;
+#pragma unroll
+      for (int i = 0; i < FA; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float z = acc[i][j][r];
+          const float zo = __shfl_xor(z, 1);  // the partner row's logit
+          const bool ok = full_v || rb + i * 16 + r < a.V;
+          const float e = ok ? fast_exp2(fmaf(z, kLog2e, -mu)) : 0.f;
+          sm += e;
+          cross += e * (z - zo);
+        }
+      sm += __shfl_xor(sm, 16);
+      sm += __shfl_xor(sm, 32);
+      cross += __shfl_xor(cross, 16);
+      cross += __shfl_xor(cross, 32);
+      if (lane < 16 && leaf < a.n_leaves) {
+        const size_t o = size_t(leaf) * a.n_chunks + chunk;
+        if (t & 1)
+          a.partS[o] = make_float2(m2, sm);
+        else
+          a.partT[o] = make_float4(m2, sm, cross, 0.f);
+      }
+    }
+  } else if (MODE == kModeKLGrad) {
+    // student lanes write G = dkl * (q - p) for their leaf
+#pragma unroll
+    for (int j = 0; j < FB; ++j) {
+      const int t = tb + j * 16;
+      const int leaf = t >> 1;
+      const bool student = (t & 1) && leaf < a.n_leaves;
+      const int lc = leaf < a.n_leaves ? leaf : 0;
+      const float gl = a.dkl[lc];
+      const float lS = a.lseS[lc] * kLog2e, lT = a.lseT[lc] * kLog2e;
+      u16* out = a.Gout + size_t(lc) * a.Vp + rb;
+#pragma unroll
+      for (int i = 0; i < FA; ++i) {
+        float vals[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float zS = acc[i][j][r];
+          const float zT = __shfl_xor(zS, 1);
+          const float q = fast_exp2(fmaf(zS, kLog2e, -lS));
+          const float pt = fast_exp2(fmaf(zT, kLog2e, -lT));
+          vals[r] = (full_v || rb + i * 16 + r < a.V) ? gl * (q - pt) : 0.f;
+        }
+        if (student) {
+          uint2 wv;
+          wv.x = pack2(vals[0], vals[1]);
+          wv.y = pack2(vals[2], vals[3]);
+          *reinterpret_cast<uint2*>(out + i * 16) = wv;
+        }
+      }
+    }
+  } else {  // kModeDh: A rows are hidden columns
+#pragma unroll
+    for (int j = 0; j < FB; ++j) {
+      const int t = tb + j * 16;
+      if (t >= a.T) continue;
+      if (a.k_split > 1) {
+        float* out = a.dh_part + (size_t(split) * a.T + t) * a.H;
+#pragma unroll
+        for (int i = 0; i < FA; ++i) {
+          const int hcol = rb + i * 16;
+          if (hcol < a.H)
+            *reinterpret_cast<float4*>(out + hcol) =
+                make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+        }
+      } else {
+        u16* out = a.dh + size_t(t) * a.H;
+#pragma unroll
+        for (int i = 0; i < FA; ++i) {
+          const int hcol = rb + i * 16;
+          if (hcol < a.H) {
+            uint2 wv;
+            wv.x = pack2(acc[i][j][0], acc[i][j][1]);
+            wv.y = pack2(acc[i][j][2], acc[i][j][3]);
+            *reinterpret_cast<uint2*>(out + hcol) = wv;
+          }
+        }
+      }
+    }
+  }
+}
+
+// dW[v][c] = sum_t G[t][v] H[t][c] (fp32 out).  Same tile shape as the tile
+// engine (256 vocabulary rows x 256 hidden columns, 8 waves of 128 x 64) with
+// MFMA 32x32x16; k = tokens.  Both operands are staged k-major
+// ([64 tokens][256]) through registers into padded LDS rows and read with the
+// transposing LDS read; the token rows past T of the last slice are zeroed.
+__global__ __launch_bounds__(NWAVES * 64, 1) void lm_dw_kernel(LmArgs a) {
+  constexpr int NT = NWAVES * 64;
+  constexpr int WC = BT / (NWAVES / 2);    // hidden columns per wave (64)
+  constexpr int NJ = WC / 32;
+  constexpr int LDA = (BA * BKK / 8) / NT; // 16-byte loads per thread, G slice
+  constexpr int LDB = (BT * BKK / 8) / NT; // 16-byte loads per thread, H slice
+  __shared__ __align__(16) u16 smem[2 * DW_STAGE];
+
+  int a0, t0, split;
+  if (!tile_of(a, 1, a0, t0, split)) return;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int c = lane & 31, g = lane >> 5;
-  const int wa = wave / (NW / 2), wt = wave % (NW / 2);
-
-  // dW mode: A rows = vocabulary, B "tokens" = hidden columns, k = tokens
-  constexpr bool kT = (MODE == kModeDh || MODE == kModeDw);  // both stages k-major
-  const int K = (MODE == kModeDh) ? a.Vp : (MODE == kModeDw ? a.T : a.H);
-  const int a_rows = (MODE == kModeDh) ? a.H : a.V;
-  const int b_rows = (MODE == kModeDw) ? a.H : a.T;
-  const int kbeg = (MODE == kModeDh) ? split * a.nk_split : 0;
-  const int nk = (MODE == kModeDh) ? min(K / BKK - kbeg, a.nk_split) : (K + BKK - 1) / BKK;
-  // Out-of-range operand rows and columns are read from clamped (valid)
-  // addresses instead of being masked, so loads never wait on a select: the
-  // products they feed land in output rows, columns or vocabulary padding that
-  // the epilogues skip or zero (and padding columns of G are stored as zero).
-  // Tiles wholly inside the operands skip even the clamping.
-  const bool interior = (t0 + BT <= b_rows) && (MODE == kModeDh ? (a0 + BA <= a.H) : (a0 + BA <= a_rows));
+  const int wa = wave / (NWAVES / 2), wt = wave % (NWAVES / 2);
+  const int nk = (a.T + BKK - 1) / BKK;
 
   f32x16 acc[4][NJ];
 #pragma unroll
@@ -132,135 +407,69 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // each thread's token rows are fixed across k slices: resolve them once
-  const u16* brow[LDB];
-#pragma unroll
-  for (int r = 0; r < LDB; ++r) {
-    const int t = t0 + (tid + r * NT) / (BKK / 8);
-    const int tc = (interior || t < a.T) ? t : 0;
-    if (MODE == kModeDw) {
-      brow[r] = nullptr;  // the dW stages are addressed per k slice
-    } else if (MODE == kModeDh) {
-      brow[r] = a.G + size_t(tc) * a.Vp;
-    } else if (MODE == kModeKL || MODE == kModeKLGrad) {
-      // a row index outside its matrix reads as a zero hidden state
-      const int row = (tc & 1) ? a.rowsS[tc >> 1] : a.rowsT[tc >> 1];
-      const int n_rows = (tc & 1) ? a.n_rows_S : a.n_rows_T;
-      const bool row_ok = row >= 0 && row < n_rows;
-      brow[r] = row_ok ? ((tc & 1) ? a.hS : a.hT) + size_t(row) * a.H : a.zero_row;
-    } else {
-      brow[r] = a.h + size_t(tc) * a.H;
-    }
-  }
-
   uint4 ra[LDA], rb[LDB];
   auto load = [&](int k0) {
-    if (MODE == kModeDw) {
-      // G slice [64 tokens][256 vocabulary] and H slice [64 tokens][256
-      // hidden], both staged k-major and read with the transposing LDS read.
-      // Token rows past T must add nothing (k is summed): the tail slice
-      // zeroes them (a block-uniform branch, taken once per tile).
-      auto stage = [&](bool tail) {
+    // G slice [64 tokens][256 vocabulary] and H slice [64 tokens][256
+    // hidden]; token rows past T must add nothing (k is summed): the tail
+    // slice zeroes them (a block-uniform branch, taken once per tile)
+    auto stage = [&](bool tail) {
 #pragma unroll
-        for (int r = 0; r < LDA; ++r) {
-          const int idx = tid + r * NT;
-          const int row = idx / (BA / 8), cc = (idx % (BA / 8)) * 8;
-          const int t = k0 + row;
-          ra[r] = ld16(a.G + size_t(min(t, a.T - 1)) * a.Vp + a0 + cc);
-          if (tail && t >= a.T) ra[r] = make_uint4(0, 0, 0, 0);
-        }
-#pragma unroll
-        for (int r = 0; r < LDB; ++r) {
-          const int idx = tid + r * NT;
-          const int row = idx / (BT / 8), cc = (idx % (BT / 8)) * 8;
-          const int t = k0 + row;
-          rb[r] = ld16(a.h + size_t(min(t, a.T - 1)) * a.H + min(t0 + cc, a.H - 8));
-          if (tail && t >= a.T) rb[r] = make_uint4(0, 0, 0, 0);
-        }
-      };
-      if (k0 + BKK > a.T)
-        stage(true);
-      else
-        stage(false);
-      return;
-    }
-#pragma unroll
-    for (int r = 0; r < LDA; ++r) {
-      const int idx = tid + r * NT;
-      if (MODE == kModeDh) {
-        // W slice [64 vocab rows][256 hidden], staged row-major; the A = W^T
-        // operand is read across its rows with the transposing LDS read
+      for (int r = 0; r < LDA; ++r) {
+        const int idx = tid + r * NT;
         const int row = idx / (BA / 8), cc = (idx % (BA / 8)) * 8;
-        const int v = k0 + row;
-        const u16* p = a.w + size_t(min(v, a.V - 1)) * a.H + min(a0 + cc, a.H - 8);
-        ra[r] = ld16(p);
-      } else {
-        const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
-        const int v = a0 + row;
-        const u16* p = a.w + size_t(min(v, a_rows - 1)) * a.H + k0 + cc;
-        ra[r] = ld16(p);
+        const int t = k0 + row;
+        ra[r] = ld16(a.G + size_t(min(t, a.T - 1)) * a.Vp + a0 + cc);
+        if (tail && t >= a.T) ra[r] = make_uint4(0, 0, 0, 0);
       }
-    }
 #pragma unroll
-    for (int r = 0; r < LDB; ++r) {
-      const int cc = ((tid + r * NT) % (BKK / 8)) * 8;
-      rb[r] = ld16(brow[r] + k0 + cc);
-    }
+      for (int r = 0; r < LDB; ++r) {
+        const int idx = tid + r * NT;
+        const int row = idx / (BT / 8), cc = (idx % (BT / 8)) * 8;
+        const int t = k0 + row;
+        rb[r] = ld16(a.h + size_t(min(t, a.T - 1)) * a.H + min(t0 + cc, a.H - 8));
+        if (tail && t >= a.T) rb[r] = make_uint4(0, 0, 0, 0);
+      }
+    };
+    if (k0 + BKK > a.T)
+      stage(true);
+    else
+      stage(false);
   };
   auto store = [&](u16* sA) {
-    u16* sB = sA + BA * PAD;
+    u16* sB = sA + BKK * WPAD;
 #pragma unroll
     for (int r = 0; r < LDA; ++r) {
       const int idx = tid + r * NT;
-      if (kT) {
-        const int row = idx / (BA / 8), cc = (idx % (BA / 8)) * 8;
-        st16(&sA[row * WPAD + cc], ra[r]);
-      } else {
-        const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
-        st16(&sA[row * PAD + cc], ra[r]);
-      }
+      st16(&sA[(idx / (BA / 8)) * WPAD + (idx % (BA / 8)) * 8], ra[r]);
     }
 #pragma unroll
     for (int r = 0; r < LDB; ++r) {
       const int idx = tid + r * NT;
-      if (MODE == kModeDw) {
-        const int row = idx / (BT / 8), cc = (idx % (BT / 8)) * 8;
-        st16(&sB[row * WPAD + cc], rb[r]);
-      } else {
-        const int row = idx / (BKK / 8), cc = (idx % (BKK / 8)) * 8;
-        st16(&sB[row * PAD + cc], rb[r]);
-      }
+      st16(&sB[(idx / (BT / 8)) * WPAD + (idx % (BT / 8)) * 8], rb[r]);
     }
   };
 
-  if (nk > 0) {  // block-uniform
-    load(kbeg * BKK);
-    store(smem);
-    if (nk > 1) load((kbeg + 1) * BKK);
-    __syncthreads();
-  }
+  load(0);
+  store(smem);
+  if (nk > 1) load(BKK);
+  __syncthreads();
   for (int kk = 0; kk < nk; ++kk) {
-    const u16* sA = smem + (kk & 1) * STAGE;
-    const u16* sB = sA + BA * PAD;
+    const u16* sA = smem + (kk & 1) * DW_STAGE;
+    const u16* sB = sA + BKK * WPAD;
     // The next slice goes to the other buffer first (every wave finished
     // reading it before the last barrier), then the slice after it is
     // requested from HBM, so both overlap this slice's MFMAs.
     if (kk + 1 < nk) {
-      store(smem + ((kk + 1) & 1) * STAGE);
-      if (kk + 2 < nk) load((kbeg + kk + 2) * BKK);
+      store(smem + ((kk + 1) & 1) * DW_STAGE);
+      if (kk + 2 < nk) load((kk + 2) * BKK);
     }
 #pragma unroll
     for (int ks = 0; ks < BKK / 16; ++ks) {
       bf16x8 af[4], bf[NJ];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[i] = kT ? ld_operand_tr<WPAD, true>(sA, ks * 16, wa * 128 + i * 32)
-                   : as_bf16x8(ld16(&sA[(wa * 128 + i * 32 + c) * PAD + ks * 16 + g * 8]));
+      for (int i = 0; i < 4; ++i) af[i] = ld_operand_tr<WPAD, true>(sA, ks * 16, wa * 128 + i * 32);
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
-        bf[j] = (MODE == kModeDw)
-                    ? ld_operand_tr<WPAD, true>(sB, ks * 16, wt * WTOK + j * 32)
-                    : as_bf16x8(ld16(&sB[(wt * WTOK + j * 32 + c) * PAD + ks * 16 + g * 8]));
+      for (int j = 0; j < NJ; ++j) bf[j] = ld_operand_tr<WPAD, true>(sB, ks * 16, wt * WC + j * 32);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -269,182 +478,83 @@ __global__ __launch_bounds__(NW * 64, 1) void lm_gemm_kernel(LmArgs a) {
     __syncthreads();
   }
 
-  // acc[i][j][r]: A-row a0 + wa*128 + i*32 + (r/4)*8 + g*4 + r%4,
-  //               token t0 + wt*WTOK + j*32 + c
+  // acc[i][j][r]: vocabulary row a0 + wa*128 + i*32 + (r/4)*8 + g*4 + r%4,
+  //               hidden column t0 + wt*WC + j*32 + c
   const int arow0 = a0 + wa * 128;
-  if (MODE == kModeLogits) {
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int t = t0 + wt * WTOK + j * 32 + c;
-      const int y = t < a.T ? a.tgt[t] : -1;
-      float mx = -INFINITY;
+  for (int j = 0; j < NJ; ++j) {
+    const int hcol = t0 + wt * WC + j * 32 + c;
+    if (hcol >= a.H) continue;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int v = arow0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-          float z = acc[i][j][r];
-          if (v == y) a.tlogit[t] = z;
-          z = v < a.V ? z * kLog2e : -INFINITY;
-          acc[i][j][r] = z;
-          mx = fmaxf(mx, z);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mu = mx == -INFINITY ? 0.f : mx;  // a chunk of vocabulary padding only
-      float s = 0.f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s += fast_exp2(acc[i][j][r] - mu);
-      s += __shfl_xor(s, 32);
-      if (g == 0 && t < a.T) a.part[size_t(t) * a.n_chunks + arow0 / 128] = make_float2(mx, s);
-    }
-  } else if (MODE == kModeGrad) {
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int t = t0 + wt * WTOK + j * 32 + c;
-      if (t >= a.T) continue;
-      const int y = a.tgt[t];
-      const float gt = y >= 0 ? a.g[t] : 0.f;
-      const float l2 = a.lse[t] * kLog2e;
-      u16* out = a.Gout + size_t(t) * a.Vp;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          float vals[4];
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int v = arow0 + i * 32 + q4 * 8 + g * 4 + u;
-            const float p = fast_exp2(acc[i][j][q4 * 4 + u] * kLog2e - l2);
-            vals[u] = v < a.V ? gt * ((v == y ? 1.f : 0.f) - p) : 0.f;
-          }
-          uint2 wv;
-          wv.x = pack2(vals[0], vals[1]);
-          wv.y = pack2(vals[2], vals[3]);
-          *reinterpret_cast<uint2*>(out + arow0 + i * 32 + q4 * 8 + g * 4) = wv;
-        }
-    }
-  } else if (MODE == kModeKL) {
-    // lanes c (even, teacher) and c + 1 (student) hold the same vocabulary
-    // rows of one leaf; each lane keeps its own (max, sum of exp) and the
-    // teacher also accumulates sum exp(zT - mT) * (zT - zS)
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int t = t0 + wt * WTOK + j * 32 + c;
-      const int leaf = t >> 1;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int v = arow0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-          if (v < a.V) mx = fmaxf(mx, acc[i][j][r] * kLog2e);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mu = mx == -INFINITY ? 0.f : mx;
-      float sm = 0.f, cross = 0.f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int v = arow0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-          const float z = acc[i][j][r];
-          const float zo = __shfl_xor(z, 1);  // the partner row's logit
-          const float e = v < a.V ? fast_exp2(z * kLog2e - mu) : 0.f;
-          sm += e;
-          cross += e * (z - zo);
-        }
-      sm += __shfl_xor(sm, 32);
-      cross += __shfl_xor(cross, 32);
-      if (g == 0 && leaf < a.n_leaves) {
-        const size_t o = size_t(leaf) * a.n_chunks + arow0 / 128;
-        if (t & 1)
-          a.partS[o] = make_float2(mx, sm);
-        else
-          a.partT[o] = make_float4(mx, sm, cross, 0.f);
+      for (int r = 0; r < 16; ++r) {
+        const int v = arow0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+        if (v < a.V) a.dw[size_t(v) * a.H + hcol] = acc[i][j][r];
       }
+  }
+}
+
+// Target logit z_{t,y_t} = h_t . W[y_t] in fp32, one wave per token.  Forward
+// (BWD = false): stored for the combine pass (0 for a token without loss).
+// Backward: rewrites G[t][y_t], which the grad tile left at -g_t p, to
+// g_t (1 - p) with p = softmax(z_t)_{y_t} from the forward's lse.
+template <bool BWD>
+__global__ __launch_bounds__(256) void lm_target_kernel(LmArgs a) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= a.T) return;
+  const int y = a.tgt[t];
+  if (y < 0) {
+    if (!BWD && lane == 0) a.tlogit[t] = 0.f;
+    return;
+  }
+  const u16* hp = a.h + size_t(t) * a.H;
+  const u16* wp = a.w + size_t(y) * a.H;
+  float s = 0.f;
+  for (int k = lane * 8; k < a.H; k += 512) {
+    const uint4 hv = ld16(hp + k), wv = ld16(wp + k);
+    const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w}, ww[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      s = fmaf(bf16_to_f32(u16(hw[u])), bf16_to_f32(u16(ww[u])), s);
+      s = fmaf(bf16_to_f32(u16(hw[u] >> 16)), bf16_to_f32(u16(ww[u] >> 16)), s);
     }
-  } else if (MODE == kModeKLGrad) {
-    // student lanes write G = dkl * (q - p) for their leaf
+  }
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int t = t0 + wt * WTOK + j * 32 + c;
-      const int leaf = t >> 1;
-      const bool student = (t & 1) && leaf < a.n_leaves;
-      const int lc = leaf < a.n_leaves ? leaf : 0;
-      const float gl = a.dkl[lc];
-      const float lS = a.lseS[lc] * kLog2e, lT = a.lseT[lc] * kLog2e;
-      u16* out = a.Gout + size_t(lc) * a.Vp;
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+  if (lane != 0) return;
+  if (!BWD) {
+    a.tlogit[t] = s;
+    return;
+  }
+  const float p = fast_exp2(fmaf(s, kLog2e, -a.lse[t] * kLog2e));
+  a.Gout[size_t(t) * a.Vp + y] = u16(bf16_bits(a.g[t] * (1.f - p)));
+}
+
+// wT[h][v] = w[v][h] for v < V and 0 for V <= v < Vp; 64 x 64 tiles through LDS.
+__global__ __launch_bounds__(256) void transpose_w_kernel(const u16* w, u16* wT, int V, int H,
+                                                          int Vp) {
+  __shared__ u16 tile[64][72];
+  const int v0 = blockIdx.x * 64, h0 = blockIdx.y * 64;
+  const int tid = threadIdx.x;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+  for (int q = 0; q < 2; ++q) {
+    const int idx = tid + q * 256;
+    const int r = idx >> 3, c = (idx & 7) * 8;
+    const uint4 val = v0 + r < V ? ld16(w + size_t(v0 + r) * H + h0 + c) : make_uint4(0, 0, 0, 0);
+    st16(&tile[r][c], val);
+  }
+  __syncthreads();
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          float vals[4];
+  for (int q = 0; q < 2; ++q) {
+    const int idx = tid + q * 256;
+    const int r = idx >> 3, c = (idx & 7) * 8;   // wT row h0 + r, columns v0 + c .. + 8
+    uint32_t e[4];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int v = arow0 + i * 32 + q4 * 8 + g * 4 + u;
-            const float zS = acc[i][j][q4 * 4 + u];
-            const float zT = __shfl_xor(zS, 1);
-            const float q = fast_exp2(zS * kLog2e - lS), pt = fast_exp2(zT * kLog2e - lT);
-            vals[u] = v < a.V ? gl * (q - pt) : 0.f;
-          }
-          if (student) {
-            uint2 wv;
-            wv.x = pack2(vals[0], vals[1]);
-            wv.y = pack2(vals[2], vals[3]);
-            *reinterpret_cast<uint2*>(out + arow0 + i * 32 + q4 * 8 + g * 4) = wv;
-          }
-        }
-    }
-  } else if (MODE == kModeDw) {
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int hcol = t0 + wt * WTOK + j * 32 + c;
-      if (hcol >= a.H) continue;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int v = arow0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-          if (v < a.V) a.dw[size_t(v) * a.H + hcol] = acc[i][j][r];
-        }
-    }
-  } else if (a.k_split > 1) {
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int t = t0 + wt * WTOK + j * 32 + c;
-      if (t >= a.T) continue;
-      float* out = a.dh_part + (size_t(split) * a.T + t) * a.H;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const int hcol = arow0 + i * 32 + q4 * 8 + g * 4;
-          if (hcol >= a.H) continue;
-          *reinterpret_cast<float4*>(out + hcol) =
-              make_float4(acc[i][j][q4 * 4 + 0], acc[i][j][q4 * 4 + 1], acc[i][j][q4 * 4 + 2],
-                          acc[i][j][q4 * 4 + 3]);
-        }
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int t = t0 + wt * WTOK + j * 32 + c;
-      if (t >= a.T) continue;
-      u16* out = a.dh + size_t(t) * a.H;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const int hcol = arow0 + i * 32 + q4 * 8 + g * 4;
-          if (hcol >= a.H) continue;
-          uint2 wv;
-          wv.x = pack2(acc[i][j][q4 * 4 + 0], acc[i][j][q4 * 4 + 1]);
-          wv.y = pack2(acc[i][j][q4 * 4 + 2], acc[i][j][q4 * 4 + 3]);
-          *reinterpret_cast<uint2*>(out + hcol) = wv;
-        }
-    }
+    for (int u = 0; u < 4; ++u)
+      e[u] = uint32_t(tile[c + 2 * u][r]) | (uint32_t(tile[c + 2 * u + 1][r]) << 16);
+    st16(wT + size_t(h0 + r) * Vp + v0 + c, make_uint4(e[0], e[1], e[2], e[3]));
   }
 }
 
@@ -543,6 +653,8 @@ static size_t dh_part_bytes(int T, int H) {
   return splits > 1 ? align256(size_t(splits) * T * H * sizeof(float)) : 0;
 }
 
+static size_t wT_bytes(int H, int V) { return align256(size_t(H) * vocab_pad(V) * sizeof(u16)); }
+
 size_t kl_fwd_ws_bytes(int n, int H, int V) {
   const int n_chunks = vocab_pad(V) / 128;
   return align256(size_t(n) * n_chunks * sizeof(float4)) +
@@ -550,9 +662,10 @@ size_t kl_fwd_ws_bytes(int n, int H, int V) {
          256;
 }
 
+// G [n, Vp] | dH partials | zero row [H] | W^T [H, Vp]
 size_t kl_bwd_ws_bytes(int n, int H, int V) {
   return align256(size_t(n) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(n, H) +
-         align256(size_t(H) * sizeof(u16)) + 256;
+         align256(size_t(H) * sizeof(u16)) + wT_bytes(H, V) + 256;
 }
 
 __global__ __launch_bounds__(256) void zero_u16_kernel(u16* p, int n) {
@@ -572,19 +685,28 @@ size_t logprob_fwd_ws_bytes(int T, int H, int V) {
          256;
 }
 
+// G [T, Vp] | dH partials | W^T [H, Vp]
 size_t logprob_bwd_ws_bytes(int T, int H, int V) {
-  return align256(size_t(T) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(T, H) + 256;
+  return align256(size_t(T) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(T, H) +
+         wT_bytes(H, V) + 256;
 }
 
 static char* align_ptr(void* p) {
   return reinterpret_cast<char*>((reinterpret_cast<uintptr_t>(p) + 255) & ~uintptr_t(255));
 }
 
-
 static dim3 gemm_grid(const LmArgs& a) {
   const int splits = a.k_split > 1 ? a.k_split : 1;
   const int per_xcd = (a.nA * a.nT * splits + kNumXcd - 1) / kNumXcd;
   return dim3(per_xcd * kNumXcd);
+}
+
+static hipError_t transpose_w(const u16* w, u16* wT, int V, int H, const char* name,
+                              hipStream_t stream) {
+  ProfScope p(name, stream);
+  hipLaunchKernelGGL(transpose_w_kernel, dim3(vocab_pad(V) / 64, H / 64), dim3(256), 0, stream, w,
+                     wT, V, H, vocab_pad(V));
+  return hipGetLastError();
 }
 
 // dH[t][h] = sum over splits of the fp32 partials, in split order (the
@@ -608,11 +730,9 @@ __global__ __launch_bounds__(256) void dh_reduce_kernel(const float* part, u16* 
   reinterpret_cast<uint2*>(dh)[i] = w;
 }
 
-
-
-// dh[T, H] = G[T, Vp] W[Vp, H] (bf16 out), split over the vocabulary when the
-// output alone would leave CUs idle; `part` is the fp32 partial area of the
-// workspace (dh_part_bytes).
+// dh[T, H] = G[T, Vp] W[Vp, H] (bf16 out) with b.wT = W^T [H, Vp], split over
+// the vocabulary when the output alone would leave CUs idle; `part` is the
+// fp32 partial area of the workspace (dh_part_bytes).
 static hipError_t launch_dh(LmArgs b, float* part, const char* name, hipStream_t stream) {
   const int nk_total = b.Vp / BKK;
   int splits = std::min(dh_splits(b.T, b.H), nk_total);
@@ -624,8 +744,7 @@ static hipError_t launch_dh(LmArgs b, float* part, const char* name, hipStream_t
   b.nT = (b.T + BT - 1) / BT;
   {
     ProfScope p(name, stream);
-    hipLaunchKernelGGL((lm_gemm_kernel<kModeDh, NWAVES>), gemm_grid(b), dim3(NWAVES * 64), 0,
-                       stream, b);
+    hipLaunchKernelGGL(lm_tile_kernel<kModeDh>, gemm_grid(b), dim3(NWAVES * 64), 0, stream, b);
     if (splits > 1) {
       const size_t n4 = size_t(b.T) * b.H / 4;
       hipLaunchKernelGGL(dh_reduce_kernel, dim3(unsigned((n4 + 255) / 256)), dim3(256), 0, stream,
@@ -655,8 +774,11 @@ hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, c
   a.nT = (T + BT - 1) / BT;
   {
     ProfScope p("lm_logits", stream);
-    hipLaunchKernelGGL((lm_gemm_kernel<kModeLogits, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
-                       stream, a);
+    hipLaunchKernelGGL(lm_tile_kernel<kModeLogits>, gemm_grid(a), dim3(NWAVES * 64), 0, stream, a);
+  }
+  {
+    ProfScope p("lm_target", stream);
+    hipLaunchKernelGGL(lm_target_kernel<false>, dim3((T + 3) / 4), dim3(256), 0, stream, a);
   }
   {
     ProfScope p("lm_combine", stream);
@@ -679,20 +801,26 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
   a.H = H;
   a.V = V;
   a.Vp = vocab_pad(V);
-  u16* G = reinterpret_cast<u16*>(align_ptr(ws));
+  char* base = align_ptr(ws);
+  u16* G = reinterpret_cast<u16*>(base);
+  float* part = reinterpret_cast<float*>(base + align256(size_t(T) * a.Vp * sizeof(u16)));
+  u16* wT = reinterpret_cast<u16*>(reinterpret_cast<char*>(part) + dh_part_bytes(T, H));
   a.Gout = G;
   a.G = G;
+  a.wT = wT;
   a.dh = static_cast<u16*>(dhidden);
   a.nA = a.Vp / BA;
   a.nT = (T + BT - 1) / BT;
+  if (hipError_t e = transpose_w(a.w, wT, V, H, "lm_wt", stream); e != hipSuccess) return e;
   {
     ProfScope p("lm_grad", stream);
-    hipLaunchKernelGGL((lm_gemm_kernel<kModeGrad, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
-                       stream, a);
+    hipLaunchKernelGGL(lm_tile_kernel<kModeGrad>, gemm_grid(a), dim3(NWAVES * 64), 0, stream, a);
+  }
+  {
+    ProfScope p("lm_target", stream);
+    hipLaunchKernelGGL(lm_target_kernel<true>, dim3((T + 3) / 4), dim3(256), 0, stream, a);
   }
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
-  float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(G) +
-                                         align256(size_t(T) * a.Vp * sizeof(u16)));
   return launch_dh(a, part, "lm_dh", stream);
 }
 
@@ -710,8 +838,7 @@ hipError_t launch_logprob_dweight(int T, int H, int V, const void* hidden, const
   a.nA = a.Vp / BA;
   a.nT = (H + BT - 1) / BT;
   ProfScope p("lm_dw", stream);
-  hipLaunchKernelGGL((lm_gemm_kernel<kModeDw, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
-                     stream, a);
+  hipLaunchKernelGGL(lm_dw_kernel, gemm_grid(a), dim3(NWAVES * 64), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -743,8 +870,7 @@ hipError_t launch_kl_fwd(int n, int H, int V, const void* hT, int nT, const int3
   a.nT = (a.T + BT - 1) / BT;
   {
     ProfScope p("kl_logits", stream);
-    hipLaunchKernelGGL((lm_gemm_kernel<kModeKL, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
-                       stream, a);
+    hipLaunchKernelGGL(lm_tile_kernel<kModeKL>, gemm_grid(a), dim3(NWAVES * 64), 0, stream, a);
   }
   {
     ProfScope p("kl_combine", stream);
@@ -774,32 +900,32 @@ hipError_t launch_kl_bwd(int n, int H, int V, const void* hT, int nT, const int3
   a.H = H;
   a.V = V;
   a.Vp = vocab_pad(V);
-  u16* G = reinterpret_cast<u16*>(align_ptr(ws));
+  char* base = align_ptr(ws);
+  u16* G = reinterpret_cast<u16*>(base);
+  float* part = reinterpret_cast<float*>(base + align256(size_t(n) * a.Vp * sizeof(u16)));
+  u16* zrow = reinterpret_cast<u16*>(reinterpret_cast<char*>(part) + dh_part_bytes(n, H));
+  u16* wT = reinterpret_cast<u16*>(reinterpret_cast<char*>(zrow) + align256(size_t(H) * sizeof(u16)));
   a.Gout = G;
   a.nA = a.Vp / BA;
   a.nT = (a.T + BT - 1) / BT;
-  u16* zrow = reinterpret_cast<u16*>(reinterpret_cast<char*>(G) +
-                                     align256(size_t(n) * a.Vp * sizeof(u16)) +
-                                     dh_part_bytes(n, H));
   a.zero_row = zrow;
   if (hipError_t e = zero_row(zrow, H, stream); e != hipSuccess) return e;
+  if (hipError_t e = transpose_w(a.w, wT, V, H, "kl_wt", stream); e != hipSuccess) return e;
   {
     ProfScope p("kl_grad", stream);
-    hipLaunchKernelGGL((lm_gemm_kernel<kModeKLGrad, NWAVES>), gemm_grid(a), dim3(NWAVES * 64), 0,
-                       stream, a);
+    hipLaunchKernelGGL(lm_tile_kernel<kModeKLGrad>, gemm_grid(a), dim3(NWAVES * 64), 0, stream, a);
   }
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   // dh = G W over the leaves
   LmArgs b{};
   b.w = a.w;
+  b.wT = wT;
   b.G = G;
   b.dh = static_cast<u16*>(dh);
   b.T = n;
   b.H = H;
   b.V = V;
   b.Vp = a.Vp;
-  float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(G) +
-                                         align256(size_t(n) * a.Vp * sizeof(u16)));
   return launch_dh(b, part, "kl_dh", stream);
 }
 

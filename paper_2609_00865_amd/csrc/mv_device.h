@@ -24,7 +24,32 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// D = A * B + C on a 16x16 tile with K = 32.  Lane l supplies row (l % 16) of
+// A and column (l % 16) of B, each as the 8 consecutive k values of group
+// (l / 16); D element r of lane l is row (l / 16) * 4 + r, column l % 16.
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// 16 bytes per lane from global memory straight into LDS: lane l's data lands
+// at LDS byte address lds + 16 l (lds is the wave's base, uniform across the
+// wave).  The load is counted by vmcnt only; the compiler does not track it,
+// so the caller waits with wait_vmcnt before a barrier that publishes it.
+__device__ __forceinline__ void lds_load16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory");
+}
+
+// s_waitcnt vmcnt(N) (the other counters left alone).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 

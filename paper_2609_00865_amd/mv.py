@@ -605,7 +605,8 @@ def sdcc_lambda(step: int, total_steps: int, lambda_max: float = 0.1,
 # kernel timing
 # ---------------------------------------------------------------------------
 KERNELS = ["attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq",
-           "lm_logits", "lm_combine", "lm_grad", "lm_dh", "lm_dw", "kl_logits", "kl_combine", "kl_grad", "kl_dh",
+           "lm_logits", "lm_target", "lm_combine", "lm_wt", "lm_grad", "lm_dh", "lm_dw",
+           "kl_logits", "kl_combine", "kl_wt", "kl_grad", "kl_dh",
            "grpo", "pack", "unpack", "rope",
            "materialize", "ppo_clip"]
 
