@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
 // ---------------------------------------------------------------------------
 // 2. dQ
 // ---------------------------------------------------------------------------
-template <int D>
+template <int D, bool IV>
 __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
   constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
   constexpr int KS = D / 16, DB = D / 32;
@@ -189,7 +189,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
           float p = fast_exp2(s[kb][r] * a.scale_log2 - lse2);
           if (!full) {
             const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
-            if (!mv_visible_iv(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv)) p = 0.f;
+            if (!mv_visible_k<IV>(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv)) p = 0.f;
           }
           s[kb][r] = p * (dp[kb][r] - Di);
         }
@@ -225,7 +225,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
 // ---------------------------------------------------------------------------
 // 3. dK / dV
 // ---------------------------------------------------------------------------
-template <int D>
+template <int D, bool IV>
 __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   constexpr int BK = kBwdTileK, BQ = kBwdBlockQ;
   constexpr int KS = D / 16, DB = D / 32;
@@ -368,7 +368,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
         for (int u = 0; u < 4; ++u) {
           const int r = q4 * 4 + u;
           float p = fast_exp2(s[mb][r] * a.scale_log2 - lv[u]);
-          if (!full && !mv_visible_iv(i0 + qo + u, key, om, a.mask.iv_ptr, a.mask.iv)) p = 0.f;
+          if (!full && !mv_visible_k<IV>(i0 + qo + u, key, om, a.mask.iv_ptr, a.mask.iv)) p = 0.f;
           s[mb][r] = p;
           dp[mb][r] = p * (dp[mb][r] - dd[u]);
         }
@@ -500,29 +500,28 @@ hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float 
   const dim3 g_kv(per_xcd_kv * Hkv * kNumXcd);
   const int n_red = int(m.bwd_red.size());
   const dim3 g_red(unsigned(std::max(1, n_red * Hkv)));
-  if (D == 128) {
+  // the general predicate only when some key has further live intervals
+  const bool iv = !m.iv.empty();
+  auto run = [&](auto pre, auto dkdv, auto red, auto dq) {
     { ProfScope p("attn_bwd_pre", stream);
-      hipLaunchKernelGGL(bwd_pre_kernel<128>, g_pre, b256, 0, stream, a); }
+      hipLaunchKernelGGL(pre, g_pre, b256, 0, stream, a); }
     { ProfScope p("attn_bwd_dkdv", stream);
-      hipLaunchKernelGGL(bwd_dkdv_kernel<128>, g_kv, b256, 0, stream, a); }
+      hipLaunchKernelGGL(dkdv, g_kv, b256, 0, stream, a); }
     if (n_red) {
       ProfScope p("attn_bwd_reduce", stream);
-      hipLaunchKernelGGL(bwd_reduce_kernel<128>, g_red, b256, 0, stream, a, n_red);
+      hipLaunchKernelGGL(red, g_red, b256, 0, stream, a, n_red);
     }
     { ProfScope p("attn_bwd_dq", stream);
-      hipLaunchKernelGGL(bwd_dq_kernel<128>, g_dq, b256, 0, stream, a); }
-  } else {
-    { ProfScope p("attn_bwd_pre", stream);
-      hipLaunchKernelGGL(bwd_pre_kernel<64>, g_pre, b256, 0, stream, a); }
-    { ProfScope p("attn_bwd_dkdv", stream);
-      hipLaunchKernelGGL(bwd_dkdv_kernel<64>, g_kv, b256, 0, stream, a); }
-    if (n_red) {
-      ProfScope p("attn_bwd_reduce", stream);
-      hipLaunchKernelGGL(bwd_reduce_kernel<64>, g_red, b256, 0, stream, a, n_red);
-    }
-    { ProfScope p("attn_bwd_dq", stream);
-      hipLaunchKernelGGL(bwd_dq_kernel<64>, g_dq, b256, 0, stream, a); }
-  }
+      hipLaunchKernelGGL(dq, g_dq, b256, 0, stream, a); }
+  };
+  if (D == 128 && iv)
+    run(bwd_pre_kernel<128>, bwd_dkdv_kernel<128, true>, bwd_reduce_kernel<128>, bwd_dq_kernel<128, true>);
+  else if (D == 128)
+    run(bwd_pre_kernel<128>, bwd_dkdv_kernel<128, false>, bwd_reduce_kernel<128>, bwd_dq_kernel<128, false>);
+  else if (iv)
+    run(bwd_pre_kernel<64>, bwd_dkdv_kernel<64, true>, bwd_reduce_kernel<64>, bwd_dq_kernel<64, true>);
+  else
+    run(bwd_pre_kernel<64>, bwd_dkdv_kernel<64, false>, bwd_reduce_kernel<64>, bwd_dq_kernel<64, false>);
   return hipGetLastError();
 }
 

@@ -26,7 +26,7 @@ struct FwdArgs {
   float scale_log2;
 };
 
-template <int D>
+template <int D, bool IV>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
   constexpr int KS = D / 16;          // MFMA k-steps over the head dimension
@@ -151,7 +151,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
           float x = s[kb][r] * a.scale_log2;
           if (!full) {
             const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
-            if (!mv_visible_iv(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv)) x = -INFINITY;
+            if (!mv_visible_k<IV>(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv)) x = -INFINITY;
           }
           s[kb][r] = x;
           mx = fmaxf(mx, x);
@@ -226,10 +226,16 @@ hipError_t launch_attn_fwd(const mv_view_mask& m, int Hq, int Hkv, int D, float 
   const int per_xcd = (m.n_qt + kNumXcd - 1) / kNumXcd;
   const dim3 grid(per_xcd * Hq * kNumXcd), block(256);
   ProfScope prof("attn_fwd", stream);
-  if (D == 128)
-    hipLaunchKernelGGL(attn_fwd_kernel<128>, grid, block, 0, stream, a);
+  // the general predicate only when some key has further live intervals
+  const bool iv = !m.iv.empty();
+  if (D == 128 && iv)
+    hipLaunchKernelGGL((attn_fwd_kernel<128, true>), grid, block, 0, stream, a);
+  else if (D == 128)
+    hipLaunchKernelGGL((attn_fwd_kernel<128, false>), grid, block, 0, stream, a);
+  else if (iv)
+    hipLaunchKernelGGL((attn_fwd_kernel<64, true>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL(attn_fwd_kernel<64>, grid, block, 0, stream, a);
+    hipLaunchKernelGGL((attn_fwd_kernel<64, false>), grid, block, 0, stream, a);
   return hipGetLastError();
 }
 

@@ -28,3 +28,10 @@ MV_HD bool mv_visible_iv(int i, int j, int omega_j, const int* iv_ptr, const int
     if (iv[2 * k] <= i && i < iv[2 * k + 1]) return true;
   return false;
 }
+
+// The predicate of a kernel specialised on whether the mask has interval
+// lists at all: without them (IV = false) every omega is a key's only end.
+template <bool IV>
+MV_HD bool mv_visible_k(int i, int j, int omega_j, const int* iv_ptr, const int* iv) {
+  return IV ? mv_visible_iv(i, j, omega_j, iv_ptr, iv) : mv_visible(i, j, omega_j);
+}
