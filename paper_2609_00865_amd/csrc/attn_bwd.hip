@@ -113,18 +113,21 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
   const u16* vbase = a.v + size_t(hk) * D;
   uint4 vreg[RLD], kreg[RLD];
   int omreg = 0;
+  int reg_j0 = 0;  // first key of the tile held in the registers
   auto load_tile = [&](int kt) {
     const int j0 = kt * BK;
 #pragma unroll
     for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      const int j = j0 + row;
-      const uint4 z = make_uint4(0, 0, 0, 0);
-      vreg[r] = j < T ? ld16(vbase + size_t(j) * kv_row + col) : z;
-      kreg[r] = j < T ? ld16(kbase + size_t(j) * kv_row + col) : z;
+      // keys past T load a clamped (valid) row, zeroed when stored: no
+      // branch, and nothing waits on the loads before the store
+      const int jc = min(j0 + row, T - 1);
+      vreg[r] = ld16(vbase + size_t(jc) * kv_row + col);
+      kreg[r] = ld16(kbase + size_t(jc) * kv_row + col);
     }
-    if (tid < BK) omreg = (j0 + tid < T) ? a.mask.omega[j0 + tid] : 0;
+    omreg = a.mask.omega[min(j0 + tid % BK, T - 1)];  // every thread: key tid % BK
+    reg_j0 = j0;
   };
   auto store_tile = [&](int buf) {
     u16* k_ = sKbuf + buf * BK * RPAD;
@@ -133,10 +136,12 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
     for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      st16(&v_[row * RPAD + col], vreg[r]);
-      st16(&k_[row * RPAD + col], kreg[r]);
+      const bool ok = reg_j0 + row < T;
+      const uint4 z = make_uint4(0, 0, 0, 0);
+      st16(&v_[row * RPAD + col], ok ? vreg[r] : z);
+      st16(&k_[row * RPAD + col], ok ? kreg[r] : z);
     }
-    if (tid < BK) sOmbuf[buf * BK + tid] = omreg;
+    sOmbuf[buf * BK + tid % BK] = reg_j0 + tid % BK < T ? omreg : 0;  // identical copies
   };
 
   // Tile e+1 is stored into the idle buffer (read by every wave before the
@@ -186,7 +191,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int r = q4 * 4 + u;
-          float p = fast_exp2(s[kb][r] * a.scale_log2 - lse2);
+          float p = fast_exp2(fmaf(s[kb][r], a.scale_log2, -lse2));
           if (!full) {
             const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
             if (!mv_visible_k<IV>(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv)) p = 0.f;
@@ -235,12 +240,14 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   constexpr int RLD = BQ * (D / 8) / 256;  // 16-byte row loads per thread per tensor
 
   // Q and dO blocks are staged row-major only; their transposed operands are
-  // read with the transposing LDS read (ld_operand_tr).
-  // two buffers: block b+1 is written while block b is read
-  __shared__ __align__(16) u16 sQbuf[2 * BQ * RPAD];
-  __shared__ __align__(16) u16 sdObuf[2 * BQ * RPAD];
-  __shared__ __align__(16) float sLbuf[2 * BQ];
-  __shared__ __align__(16) float sDbuf[2 * BQ];
+  // read with the transposing LDS read (ld_operand_tr).  Three buffers: while
+  // step st accumulates dV, dK from its block, step st+1 computes S and dP
+  // from the next one and block st+2 is written.
+  constexpr int NBUF = 3;
+  __shared__ __align__(16) u16 sQbuf[NBUF * BQ * RPAD];
+  __shared__ __align__(16) u16 sdObuf[NBUF * BQ * RPAD];
+  __shared__ __align__(16) float sLbuf[NBUF * BQ];
+  __shared__ __align__(16) float sDbuf[NBUF * BQ];
 
   int xcd, local;
   xcd_split(xcd, local);
@@ -281,6 +288,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const size_t q_row = size_t(a.Hq) * D;
   uint4 qreg[RLD], dreg[RLD];
   float lreg = 0.f, dreg1 = 0.f;
+  int reg_i0 = 0;  // first row of the block held in qreg / dreg
   auto load_block = [&](int hh, int qb) {
     const int i0 = qb * BQ;
     const u16* qb_ = a.q + size_t(hh) * D;
@@ -289,16 +297,17 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), cc = idx % (D / 8);
-      const int i = i0 + row;
-      const uint4 z = make_uint4(0, 0, 0, 0);
-      qreg[r] = i < T ? ld16(qb_ + size_t(i) * q_row + cc * 8) : z;
-      dreg[r] = i < T ? ld16(db_ + size_t(i) * q_row + cc * 8) : z;
+      // rows past T load a clamped (valid) row, zeroed when stored: no
+      // branch, and nothing waits on the loads before the store
+      const int ic = min(i0 + row, T - 1);
+      qreg[r] = ld16(qb_ + size_t(ic) * q_row + cc * 8);
+      dreg[r] = ld16(db_ + size_t(ic) * q_row + cc * 8);
     }
-    if (tid < BQ) {
-      const int i = i0 + tid;
-      lreg = i < T ? a.lse[size_t(hh) * T + i] * kLog2e : 0.f;
-      dreg1 = i < T ? a.Dd[size_t(hh) * T + i] : 0.f;
-    }
+    // every thread takes row tid % BQ's LSE and D (identical copies)
+    const int ic = min(i0 + tid % BQ, T - 1);
+    lreg = a.lse[size_t(hh) * T + ic];
+    dreg1 = a.Dd[size_t(hh) * T + ic];
+    reg_i0 = i0;
   };
   auto store_block = [&](int buf) {
     u16* q_ = sQbuf + buf * BQ * RPAD;
@@ -307,40 +316,29 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), cc = idx % (D / 8);
-      st16(&q_[row * RPAD + cc * 8], qreg[r]);
-      st16(&d_[row * RPAD + cc * 8], dreg[r]);
+      const bool ok = reg_i0 + row < T;
+      const uint4 z = make_uint4(0, 0, 0, 0);
+      st16(&q_[row * RPAD + cc * 8], ok ? qreg[r] : z);
+      st16(&d_[row * RPAD + cc * 8], ok ? dreg[r] : z);
     }
-    if (tid < BQ) {
-      sLbuf[buf * BQ + tid] = lreg;
-      sDbuf[buf * BQ + tid] = dreg1;
-    }
+    const bool ok = reg_i0 + tid % BQ < T;
+    sLbuf[buf * BQ + tid % BQ] = ok ? lreg * kLog2e : 0.f;
+    sDbuf[buf * BQ + tid % BQ] = ok ? dreg1 : 0.f;
   };
 
   const int nqb = qb1 - qb0;
   const int steps = nqb * G;
   const int h0 = hk * G;
-  // Block st+1 is stored into the idle buffer (read by every wave before the
-  // last barrier) and block st+2 requested before block st's MFMAs, so the
-  // stores and the HBM latency overlap the math; one barrier per block.
-  load_block(h0, qb0);
-  store_block(0);
-  if (steps > 1) load_block(h0 + 1 / nqb, qb0 + 1 % nqb);
-  __syncthreads();
-  for (int st = 0; st < steps; ++st) {
-    const int qb = qb0 + st % nqb;
-    const int buf = st & 1;
-    if (st + 1 < steps) {
-      store_block(buf ^ 1);
-      if (st + 2 < steps) load_block(h0 + (st + 2) / nqb, qb0 + (st + 2) % nqb);
-    }
+  // step st covers query block qb0 + st % nqb of head h0 + st / nqb
+  auto load_step = [&](int st) { load_block(h0 + st / nqb, qb0 + st % nqb); };
+
+  // S = Q K^T and dP = dO V^T of step st (rows: the block's queries, lanes:
+  // this wave's keys), then P and dS in place
+  f32x16 s[MB], dp[MB];
+  auto scores_mfma = [&](int st) {
+    const int buf = st % NBUF;
     const u16* sQ = sQbuf + buf * BQ * RPAD;
     const u16* sdO = sdObuf + buf * BQ * RPAD;
-    const float* sL = sLbuf + buf * BQ;
-    const float* sD = sDbuf + buf * BQ;
-    const int i0 = qb * BQ;
-    const bool full = (i0 >= j1 - 1) && (i0 + BQ <= om_min);
-
-    f32x16 s[MB], dp[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
@@ -355,7 +353,18 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
         dp[mb] = mfma32(as_bf16x8(ld16(&sdO[off])), vf[ks], dp[mb]);
       }
     }
-    // P and dS in place; rows of s/dp are queries mb*32 + q4*8 + g*4 + u
+  };
+  // rows of s/dp are queries mb*32 + q4*8 + g*4 + u of the block
+  auto scores_valu = [&](int st, bf16x8 (&pf)[KQ], bf16x8 (&dsf)[KQ]) {
+    const int buf = st % NBUF;
+    const float* sL = sLbuf + buf * BQ;
+    const float* sD = sDbuf + buf * BQ;
+    const int i0 = (qb0 + st % nqb) * BQ;
+    const bool full = (i0 >= j1 - 1) && (i0 + BQ <= om_min);
+    // single-interval keys: row i sees this lane's key iff 0 <= i - key < om - key,
+    // every row of a full step does (a select, not a branch, keeps the step
+    // one scheduling region)
+    const uint32_t range = full ? 0x7fffffffu : uint32_t(om - key);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
@@ -367,19 +376,28 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int r = q4 * 4 + u;
-          float p = fast_exp2(s[mb][r] * a.scale_log2 - lv[u]);
-          if (!full && !mv_visible_k<IV>(i0 + qo + u, key, om, a.mask.iv_ptr, a.mask.iv)) p = 0.f;
+          float p = fast_exp2(fmaf(s[mb][r], a.scale_log2, -lv[u]));
+          if (IV) {
+            if (!full && !mv_visible_iv(i0 + qo + u, key, om, a.mask.iv_ptr, a.mask.iv)) p = 0.f;
+          } else {
+            p = uint32_t(i0 + qo + u - key) < range ? p : 0.f;
+          }
           s[mb][r] = p;
           dp[mb][r] = p * (dp[mb][r] - dd[u]);
         }
       }
     }
-    bf16x8 pf[KQ], dsf[KQ];
 #pragma unroll
     for (int ks = 0; ks < KQ; ++ks) {
       pf[ks] = to_operand(s[ks >> 1], (ks & 1) * 8);
       dsf[ks] = to_operand(dp[ks >> 1], (ks & 1) * 8);
     }
+  };
+  // dV^T += dO^T P and dK^T += Q^T dS for step st
+  auto accumulate = [&](int st, const bf16x8 (&pf)[KQ], const bf16x8 (&dsf)[KQ]) {
+    const int buf = st % NBUF;
+    const u16* sQ = sQbuf + buf * BQ * RPAD;
+    const u16* sdO = sdObuf + buf * BQ * RPAD;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -388,8 +406,35 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
         dv[db] = mfma32(ld_operand_tr<RPAD>(sdO, ks * 16, db * 32), pf[ks], dv[db]);
         dk[db] = mfma32(ld_operand_tr<RPAD>(sQ, ks * 16, db * 32), dsf[ks], dk[db]);
       }
+  };
+
+  // Software pipeline, one barrier per step: step st+1's S and dP MFMAs are
+  // issued before step st's dV and dK MFMAs, and the exponentials of step
+  // st+1 run while those are in the MFMA pipe.  Block st+2 is written into
+  // the buffer step st-1 used (every wave finished with it before the last
+  // barrier) and block st+3 is requested from HBM.
+  load_step(0);
+  store_block(0);
+  if (steps > 1) {
+    load_step(1);
+    store_block(1);
+  }
+  if (steps > 2) load_step(2);
+  __syncthreads();
+  bf16x8 pf[KQ], dsf[KQ];
+  scores_mfma(0);
+  scores_valu(0, pf, dsf);
+  for (int st = 0; st + 1 < steps; ++st) {
+    if (st + 2 < steps) {
+      store_block((st + 2) % NBUF);
+      if (st + 3 < steps) load_step(st + 3);
+    }
+    scores_mfma(st + 1);
+    accumulate(st, pf, dsf);
+    scores_valu(st + 1, pf, dsf);
     __syncthreads();
   }
+  accumulate(steps - 1, pf, dsf);
 
   if (!kok) return;
   if (slot < 0) {

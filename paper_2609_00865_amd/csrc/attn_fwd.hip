@@ -76,18 +76,21 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
 
   uint4 kreg[KLD], vreg[KLD];
   int omreg = 0;
+  int reg_j0 = 0;  // first key of the tile held in the registers
   auto load_tile = [&](int kt) {
     const int j0 = kt * BK;
 #pragma unroll
     for (int r = 0; r < KLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      const int j = j0 + row;
-      const uint4 z = make_uint4(0, 0, 0, 0);
-      kreg[r] = j < T ? ld16(kbase + size_t(j) * kv_row + col) : z;
-      vreg[r] = j < T ? ld16(vbase + size_t(j) * kv_row + col) : z;
+      // keys past T load a clamped (valid) row, zeroed when stored: no
+      // branch, and nothing waits on the loads before the store
+      const int jc = min(j0 + row, T - 1);
+      kreg[r] = ld16(kbase + size_t(jc) * kv_row + col);
+      vreg[r] = ld16(vbase + size_t(jc) * kv_row + col);
     }
-    if (tid < BK) omreg = (j0 + tid < T) ? a.mask.omega[j0 + tid] : 0;
+    omreg = a.mask.omega[min(j0 + tid % BK, T - 1)];  // every thread: key tid % BK
+    reg_j0 = j0;
   };
   auto store_tile = [&](int buf) {
     u16* k_ = sKbuf + buf * BK * KPAD;
@@ -96,10 +99,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     for (int r = 0; r < KLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      st16(&k_[row * KPAD + col], kreg[r]);
-      st16(&v_[row * VPAD + col], vreg[r]);
+      const bool ok = reg_j0 + row < T;
+      const uint4 z = make_uint4(0, 0, 0, 0);
+      st16(&k_[row * KPAD + col], ok ? kreg[r] : z);
+      st16(&v_[row * VPAD + col], ok ? vreg[r] : z);
     }
-    if (tid < BK) sOmbuf[buf * BK + tid] = omreg;
+    sOmbuf[buf * BK + tid % BK] = reg_j0 + tid % BK < T ? omreg : 0;  // identical copies
   };
 
   // Tile e+1 is stored into the idle buffer (read by every wave before the
