@@ -66,10 +66,10 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
 // 2. dQ
 // ---------------------------------------------------------------------------
 template <int D, bool IV>
-__global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
+__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
   constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
   constexpr int KS = D / 16, DB = D / 32;
-  constexpr int RPAD = D + 48;
+  constexpr int RPAD = D + 8;
   constexpr int RLD = BK * D / 8 / 256;          // row-major K and V loads per thread
 
   // two buffers: key tile e+1 is written while tile e is read
@@ -166,23 +166,22 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
     const int* sOm = sOmbuf + buf * BK;
     const int j0 = kt * BK;
 
-    f32x16 s[2], dp[2];
+    // the tile's two 32-key halves one after the other: S^T and dP^T of a
+    // half, its dS^T, then its share of dQ^T (half the live accumulators)
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
+      f32x16 s, dp;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        s[kb][r] = 0.f;
-        dp[kb][r] = 0.f;
+        s[r] = 0.f;
+        dp[r] = 0.f;
       }
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const int off = (kb * 32 + c) * RPAD + ks * 16 + g * 8;
-        s[kb] = mfma32(as_bf16x8(ld16(&sK[off])), qf[ks], s[kb]);
-        dp[kb] = mfma32(as_bf16x8(ld16(&sV[off])), df[ks], dp[kb]);
+        s = mfma32(as_bf16x8(ld16(&sK[off])), qf[ks], s);
+        dp = mfma32(as_bf16x8(ld16(&sV[off])), df[ks], dp);
       }
-    }
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
         int4 om = make_int4(0, 0, 0, 0);
@@ -191,25 +190,23 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int r = q4 * 4 + u;
-          float p = fast_exp2(fmaf(s[kb][r], a.scale_log2, -lse2));
+          float p = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
           if (!full) {
             const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
             if (!mv_visible_k<IV>(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv)) p = 0.f;
           }
-          s[kb][r] = p * (dp[kb][r] - Di);
+          s[r] = p * (dp[r] - Di);
         }
       }
+      const bf16x8 dsf[2] = {to_operand(s, 0), to_operand(s, 8)};
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          // K^T operand: column block db of keys (2 kb + kk)*16.. in accumulator order
+          acc[db] = mfma32(ld_operand_tr<RPAD>(sK, (2 * kb + kk) * 16, db * 32), dsf[kk], acc[db]);
+        }
     }
-    bf16x8 dsf[4];
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) dsf[ks] = to_operand(s[ks >> 1], (ks & 1) * 8);
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        // K^T operand: column block db of keys ks*16.. in accumulator order
-        acc[db] = mfma32(ld_operand_tr<RPAD>(sK, ks * 16, db * 32), dsf[ks], acc[db]);
-      }
     __syncthreads();
   }
 
