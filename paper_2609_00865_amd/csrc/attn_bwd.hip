@@ -132,14 +132,15 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
   auto store_tile = [&](int buf) {
     u16* k_ = sKbuf + buf * BK * RPAD;
     u16* v_ = sVbuf + buf * BK * RPAD;
+    // only the ragged last tile has keys past T (a block-uniform branch)
+    const bool ragged = reg_j0 + BK > T;
 #pragma unroll
     for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      const bool ok = reg_j0 + row < T;
-      const uint4 z = make_uint4(0, 0, 0, 0);
-      st16(&v_[row * RPAD + col], ok ? vreg[r] : z);
-      st16(&k_[row * RPAD + col], ok ? kreg[r] : z);
+      if (ragged && reg_j0 + row >= T) kreg[r] = vreg[r] = make_uint4(0, 0, 0, 0);
+      st16(&v_[row * RPAD + col], vreg[r]);
+      st16(&k_[row * RPAD + col], kreg[r]);
     }
     sOmbuf[buf * BK + tid % BK] = reg_j0 + tid % BK < T ? omreg : 0;  // identical copies
   };
@@ -183,21 +184,23 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
         dp = mfma32(as_bf16x8(ld16(&sV[off])), df[ks], dp);
       }
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        int4 om = make_int4(0, 0, 0, 0);
-        if (!full) om = *reinterpret_cast<const int4*>(&sOm[kb * 32 + q4 * 8 + g * 4]);
-        const int omv[4] = {om.x, om.y, om.z, om.w};
+      for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
+      if (!full) {  // block-uniform; per element a select, not a branch
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int r = q4 * 4 + u;
-          float p = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
-          if (!full) {
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int4 om = *reinterpret_cast<const int4*>(&sOm[kb * 32 + q4 * 8 + g * 4]);
+          const int omv[4] = {om.x, om.y, om.z, om.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int r = q4 * 4 + u;
             const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
-            if (!mv_visible_k<IV>(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv)) p = 0.f;
+            const bool vis = mv_visible_k<IV>(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv);
+            s[r] = vis ? s[r] : 0.f;
           }
-          s[r] = p * (dp[r] - Di);
         }
       }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = s[r] * (dp[r] - Di);
       const bf16x8 dsf[2] = {to_operand(s, 0), to_operand(s, 8)};
 #pragma unroll
       for (int db = 0; db < DB; ++db)
@@ -309,14 +312,15 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   auto store_block = [&](int buf) {
     u16* q_ = sQbuf + buf * BQ * RPAD;
     u16* d_ = sdObuf + buf * BQ * RPAD;
+    // only the ragged last block has rows past T (a block-uniform branch)
+    const bool ragged = reg_i0 + BQ > T;
 #pragma unroll
     for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), cc = idx % (D / 8);
-      const bool ok = reg_i0 + row < T;
-      const uint4 z = make_uint4(0, 0, 0, 0);
-      st16(&q_[row * RPAD + cc * 8], ok ? qreg[r] : z);
-      st16(&d_[row * RPAD + cc * 8], ok ? dreg[r] : z);
+      if (ragged && reg_i0 + row >= T) qreg[r] = dreg[r] = make_uint4(0, 0, 0, 0);
+      st16(&q_[row * RPAD + cc * 8], qreg[r]);
+      st16(&d_[row * RPAD + cc * 8], dreg[r]);
     }
     const bool ok = reg_i0 + tid % BQ < T;
     sLbuf[buf * BQ + tid % BQ] = ok ? lreg * kLog2e : 0.f;

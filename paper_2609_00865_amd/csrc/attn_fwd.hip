@@ -95,14 +95,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   auto store_tile = [&](int buf) {
     u16* k_ = sKbuf + buf * BK * KPAD;
     u16* v_ = sVbuf + buf * BK * VPAD;
+    // only the ragged last tile has keys past T (a block-uniform branch)
+    const bool ragged = reg_j0 + BK > T;
 #pragma unroll
     for (int r = 0; r < KLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      const bool ok = reg_j0 + row < T;
-      const uint4 z = make_uint4(0, 0, 0, 0);
-      st16(&k_[row * KPAD + col], ok ? kreg[r] : z);
-      st16(&v_[row * VPAD + col], ok ? vreg[r] : z);
+      if (ragged && reg_j0 + row >= T) kreg[r] = vreg[r] = make_uint4(0, 0, 0, 0);
+      st16(&k_[row * KPAD + col], kreg[r]);
+      st16(&v_[row * VPAD + col], vreg[r]);
     }
     sOmbuf[buf * BK + tid % BK] = reg_j0 + tid % BK < T ? omreg : 0;  // identical copies
   };
@@ -142,46 +143,55 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
       }
     }
 
+    // scores stay raw (masked ones -inf); the running max m_run is in base-2
+    // units of the scaled scores
+    if (!full) {  // block-uniform; per element a select, not a branch
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int4 om = *reinterpret_cast<const int4*>(&sOm[kb * 32 + q4 * 8 + g * 4]);
+          const int omv[4] = {om.x, om.y, om.z, om.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int r = q4 * 4 + u;
+            const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
+            const bool vis = mv_visible_k<IV>(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv);
+            s[kb][r] = vis ? s[kb][r] : -INFINITY;
+          }
+        }
+    }
     float mx = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        int4 om = make_int4(0, 0, 0, 0);
-        if (!full) om = *reinterpret_cast<const int4*>(&sOm[kb * 32 + q4 * 8 + g * 4]);
-        const int omv[4] = {om.x, om.y, om.z, om.w};
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int r = q4 * 4 + u;
-          float x = s[kb][r] * a.scale_log2;
-          if (!full) {
-            const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
-            if (!mv_visible_k<IV>(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv)) x = -INFINITY;
-          }
-          s[kb][r] = x;
-          mx = fmaxf(mx, x);
-        }
-      }
-    }
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
+    // Lazy rescaling: the running max moves only when a tile's max exceeds it
+    // by more than 8 (base 2); until then p = exp2(x - m_run) <= 2^8, well
+    // inside fp32 and the bf16 operand range, and O and l keep their scale.
+    const float m_tile = mx * a.scale_log2;     // -inf for a fully masked row
+    const bool grow = m_tile > m_run + 8.f;
+    if (__any(grow)) {
+      const float alpha = grow ? fast_exp2(m_run - m_tile) : 1.f;
+      if (grow) m_run = m_tile;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+    }
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
     float psum = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(s[kb][r] - m_use);
+        const float p = fast_exp2(fmaf(s[kb][r], a.scale_log2, -m_use));
         s[kb][r] = p;
         psum += p;
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+    l_run += psum;
 
     bf16x8 pf[4];
 #pragma unroll

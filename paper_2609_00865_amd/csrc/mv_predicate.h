@@ -12,7 +12,9 @@
 #define MV_HD inline
 #endif
 
-MV_HD bool mv_visible(int i, int j, int omega_j) { return j <= i && i < omega_j; }
+// (bitwise &: both comparisons are evaluated, so a vector unit selects
+// instead of branching per element)
+MV_HD bool mv_visible(int i, int j, int omega_j) { return (j <= i) & (i < omega_j); }
 
 // A key that a later edit restores has further live intervals.  Such a key is
 // stored with the sign bit of omega set (the low 31 bits keep the end of its
