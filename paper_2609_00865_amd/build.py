@@ -19,11 +19,15 @@ DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang"
                 "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-mcode-object-version=5", "-Wall", "-Wno-unused-result",
           "-I" + os.path.join(ROOT, "include")]
+# Per-source code generation options: the attention backward reads its score
+# accumulators with the vector ALU, so its MFMAs write ordinary VGPRs.
+SOURCE_FLAGS = {"attn_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, src + ".o")
-    cmd = [HIPCC, *DEVICE_FLAGS, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *DEVICE_FLAGS, *COMMON, *SOURCE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src),
+           "-o", obj]
     if src.endswith(".hip"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)

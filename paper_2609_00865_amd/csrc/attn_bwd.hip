@@ -333,30 +333,29 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   // step st covers query block qb0 + st % nqb of head h0 + st / nqb
   auto load_step = [&](int st) { load_block(h0 + st / nqb, qb0 + st % nqb); };
 
-  // S = Q K^T and dP = dO V^T of step st (rows: the block's queries, lanes:
-  // this wave's keys), then P and dS in place
-  f32x16 s[MB], dp[MB];
-  auto scores_mfma = [&](int st) {
+  // The work of a step runs in two halves (unit 2 st + mb: the block's
+  // query rows mb*32 ..): S = Q K^T and dP = dO V^T of the half (rows: its
+  // queries, lanes: this wave's keys), then P and dS as bf16 operands, then
+  // its share of dV^T += dO^T P and dK^T += Q^T dS.
+  f32x16 s, dp;
+  auto scores_mfma = [&](int st, int mb) {
     const int buf = st % NBUF;
     const u16* sQ = sQbuf + buf * BQ * RPAD;
     const u16* sdO = sdObuf + buf * BQ * RPAD;
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
+    for (int r = 0; r < 16; ++r) {
+      s[r] = 0.f;
+      dp[r] = 0.f;
+    }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[mb][r] = 0.f;
-        dp[mb][r] = 0.f;
-      }
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int off = (mb * 32 + c) * RPAD + ks * 16 + g * 8;
-        s[mb] = mfma32(as_bf16x8(ld16(&sQ[off])), kf[ks], s[mb]);
-        dp[mb] = mfma32(as_bf16x8(ld16(&sdO[off])), vf[ks], dp[mb]);
-      }
+    for (int ks = 0; ks < KS; ++ks) {
+      const int off = (mb * 32 + c) * RPAD + ks * 16 + g * 8;
+      s = mfma32(as_bf16x8(ld16(&sQ[off])), kf[ks], s);
+      dp = mfma32(as_bf16x8(ld16(&sdO[off])), vf[ks], dp);
     }
   };
   // rows of s/dp are queries mb*32 + q4*8 + g*4 + u of the block
-  auto scores_valu = [&](int st, bf16x8 (&pf)[KQ], bf16x8 (&dsf)[KQ]) {
+  auto scores_valu = [&](int st, int mb, bf16x8 (&pf)[2], bf16x8 (&dsf)[2]) {
     const int buf = st % NBUF;
     const float* sL = sLbuf + buf * BQ;
     const float* sD = sDbuf + buf * BQ;
@@ -367,52 +366,47 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     // one scheduling region)
     const uint32_t range = full ? 0x7fffffffu : uint32_t(om - key);
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int qo = mb * 32 + q4 * 8 + g * 4;
+      const float4 l4 = *reinterpret_cast<const float4*>(&sL[qo]);
+      const float4 d4 = *reinterpret_cast<const float4*>(&sD[qo]);
+      const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dd[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int qo = mb * 32 + q4 * 8 + g * 4;
-        const float4 l4 = *reinterpret_cast<const float4*>(&sL[qo]);
-        const float4 d4 = *reinterpret_cast<const float4*>(&sD[qo]);
-        const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dd[4] = {d4.x, d4.y, d4.z, d4.w};
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int r = q4 * 4 + u;
-          float p = fast_exp2(fmaf(s[mb][r], a.scale_log2, -lv[u]));
-          if (IV) {
-            if (!full && !mv_visible_iv(i0 + qo + u, key, om, a.mask.iv_ptr, a.mask.iv)) p = 0.f;
-          } else {
-            p = uint32_t(i0 + qo + u - key) < range ? p : 0.f;
-          }
-          s[mb][r] = p;
-          dp[mb][r] = p * (dp[mb][r] - dd[u]);
+      for (int u = 0; u < 4; ++u) {
+        const int r = q4 * 4 + u;
+        float p = fast_exp2(fmaf(s[r], a.scale_log2, -lv[u]));
+        if (IV) {
+          if (!full && !mv_visible_iv(i0 + qo + u, key, om, a.mask.iv_ptr, a.mask.iv)) p = 0.f;
+        } else {
+          p = uint32_t(i0 + qo + u - key) < range ? p : 0.f;
         }
+        s[r] = p;
+        dp[r] = p * (dp[r] - dd[u]);
       }
     }
-#pragma unroll
-    for (int ks = 0; ks < KQ; ++ks) {
-      pf[ks] = to_operand(s[ks >> 1], (ks & 1) * 8);
-      dsf[ks] = to_operand(dp[ks >> 1], (ks & 1) * 8);
-    }
+    pf[0] = to_operand(s, 0);
+    pf[1] = to_operand(s, 8);
+    dsf[0] = to_operand(dp, 0);
+    dsf[1] = to_operand(dp, 8);
   };
-  // dV^T += dO^T P and dK^T += Q^T dS for step st
-  auto accumulate = [&](int st, const bf16x8 (&pf)[KQ], const bf16x8 (&dsf)[KQ]) {
+  auto accumulate = [&](int st, int mb, const bf16x8 (&pf)[2], const bf16x8 (&dsf)[2]) {
     const int buf = st % NBUF;
     const u16* sQ = sQbuf + buf * BQ * RPAD;
     const u16* sdO = sdObuf + buf * BQ * RPAD;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int ks = 0; ks < KQ; ++ks) {
-        // dO^T and Q^T operands: columns db*32.. of rows ks*16.. in accumulator order
-        dv[db] = mfma32(ld_operand_tr<RPAD>(sdO, ks * 16, db * 32), pf[ks], dv[db]);
-        dk[db] = mfma32(ld_operand_tr<RPAD>(sQ, ks * 16, db * 32), dsf[ks], dk[db]);
+      for (int kk = 0; kk < 2; ++kk) {
+        // dO^T and Q^T operands: columns db*32.. of rows (2 mb + kk)*16.. in accumulator order
+        dv[db] = mfma32(ld_operand_tr<RPAD>(sdO, (2 * mb + kk) * 16, db * 32), pf[kk], dv[db]);
+        dk[db] = mfma32(ld_operand_tr<RPAD>(sQ, (2 * mb + kk) * 16, db * 32), dsf[kk], dk[db]);
       }
   };
 
-  // Software pipeline, one barrier per step: step st+1's S and dP MFMAs are
-  // issued before step st's dV and dK MFMAs, and the exponentials of step
-  // st+1 run while those are in the MFMA pipe.  Block st+2 is written into
-  // the buffer step st-1 used (every wave finished with it before the last
+  // Software pipeline over half-step units, one barrier per step: the next
+  // unit's S and dP MFMAs are issued before this unit's dV and dK MFMAs, and
+  // the next unit's exponentials follow them.  Block st+2 is written into the
+  // buffer step st-1 used (every wave finished with it before the last
   // barrier) and block st+3 is requested from HBM.
   load_step(0);
   store_block(0);
@@ -422,20 +416,26 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   }
   if (steps > 2) load_step(2);
   __syncthreads();
-  bf16x8 pf[KQ], dsf[KQ];
-  scores_mfma(0);
-  scores_valu(0, pf, dsf);
+  bf16x8 pf[2], dsf[2];
+  scores_mfma(0, 0);
+  scores_valu(0, 0, pf, dsf);
   for (int st = 0; st + 1 < steps; ++st) {
     if (st + 2 < steps) {
       store_block((st + 2) % NBUF);
       if (st + 3 < steps) load_step(st + 3);
     }
-    scores_mfma(st + 1);
-    accumulate(st, pf, dsf);
-    scores_valu(st + 1, pf, dsf);
+    scores_mfma(st, 1);
+    accumulate(st, 0, pf, dsf);
+    scores_valu(st, 1, pf, dsf);
+    scores_mfma(st + 1, 0);
+    accumulate(st, 1, pf, dsf);
+    scores_valu(st + 1, 0, pf, dsf);
     __syncthreads();
   }
-  accumulate(steps - 1, pf, dsf);
+  scores_mfma(steps - 1, 1);
+  accumulate(steps - 1, 0, pf, dsf);
+  scores_valu(steps - 1, 1, pf, dsf);
+  accumulate(steps - 1, 1, pf, dsf);
 
   if (!kok) return;
   if (slot < 0) {
