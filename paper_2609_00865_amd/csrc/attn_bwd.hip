@@ -11,6 +11,8 @@
 //     Long ranges are cut into items that write fp32 partial tiles; a reduce
 //     pass sums them in a fixed order (deterministic, no atomics).
 // All stores write whole 16-byte or 8-byte runs of a row.
+#include <type_traits>
+
 #include "mv_device.h"
 #include "mv_predicate.h"
 
@@ -403,6 +405,117 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       }
   };
 
+  // Single-interval masks (IV = false): the same units, with every MFMA
+  // interleaved with softmax work in a fixed issue order (a scheduling fence
+  // after each group).  Unit n's S/dP (run in phase X of unit n-1) feed its
+  // softmax elements 0..7 in phase Y of unit n-1 and 8..15 in its own phase
+  // X; phase X issues unit n+1's S/dP MFMAs, phase Y unit n's dV/dK MFMAs;
+  // operands are read two MFMAs ahead.  Score registers alternate by unit
+  // parity; the row LSE, D and mask range of the unit in flight are kept.
+  f32x16 sc[2], dc[2];
+  float lv[16], dd[16];
+  int ui0 = 0, umb = 0;
+  uint32_t urange = 0;
+  auto load_ctx = [&](int st, int mb) {
+    const int buf = st % NBUF;
+    const float* sL = sLbuf + buf * BQ;
+    const float* sD = sDbuf + buf * BQ;
+    ui0 = (qb0 + st % nqb) * BQ;
+    umb = mb;
+    const bool full = (ui0 >= j1 - 1) && (ui0 + BQ <= om_min);
+    urange = full ? 0x7fffffffu : uint32_t(om - key);
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int qo = mb * 32 + q4 * 8 + g * 4;
+      const float4 l4 = *reinterpret_cast<const float4*>(&sL[qo]);
+      const float4 d4 = *reinterpret_cast<const float4*>(&sD[qo]);
+      lv[q4 * 4 + 0] = l4.x; lv[q4 * 4 + 1] = l4.y; lv[q4 * 4 + 2] = l4.z; lv[q4 * 4 + 3] = l4.w;
+      dd[q4 * 4 + 0] = d4.x; dd[q4 * 4 + 1] = d4.y; dd[q4 * 4 + 2] = d4.z; dd[q4 * 4 + 3] = d4.w;
+    }
+  };
+  // softmax element r (row umb*32 + (r/4)*8 + g*4 + r%4) of the unit in flight
+  auto elem = [&](int par, int r) {
+    float p = fast_exp2(fmaf(sc[par][r], a.scale_log2, -lv[r]));
+    p = uint32_t(ui0 + umb * 32 + (r >> 2) * 8 + g * 4 + (r & 3) - key) < urange ? p : 0.f;
+    sc[par][r] = p;
+    dc[par][r] = p * (dc[par][r] - dd[r]);
+  };
+  // phase X of the unit in set par: the next unit's (st, mb) S/dP MFMAs into
+  // set par ^ 1 (if NEXT) with elements 8..15 of this unit, then its operands
+  auto phaseX = [&](auto next_tag, int par, int st, int mb, bf16x8 (&pfo)[2], bf16x8 (&dso)[2]) {
+    constexpr bool NEXT = decltype(next_tag)::value;
+    const u16* sQ = sQbuf + (st % NBUF) * BQ * RPAD;
+    const u16* sdO = sdObuf + (st % NBUF) * BQ * RPAD;
+    const int np = par ^ 1;
+    auto opnd = [&](int j) {   // MFMA j: ks = j / 2, S (even) or dP (odd)
+      return as_bf16x8(ld16(&((j & 1) ? sdO : sQ)[(mb * 32 + c) * RPAD + (j >> 1) * 16 + g * 8]));
+    };
+    bf16x8 op[3];
+    if constexpr (NEXT) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sc[np][r] = 0.f;
+        dc[np][r] = 0.f;
+      }
+      op[0] = opnd(0);
+      op[1] = opnd(1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < 2 * KS; ++j) {
+      if constexpr (NEXT) {
+        if (j + 2 < 2 * KS) op[(j + 2) % 3] = opnd(j + 2);
+        if (j & 1)
+          dc[np] = mfma32(op[j % 3], vf[j >> 1], dc[np]);
+        else
+          sc[np] = mfma32(op[j % 3], kf[j >> 1], sc[np]);
+      }
+      if ((j & 1) && 8 + (j >> 1) < 16) elem(par, 8 + (j >> 1));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int r = 8 + KS; r < 16; ++r) elem(par, r);   // D = 64: the rest
+    pfo[0] = to_operand(sc[par], 0);
+    pfo[1] = to_operand(sc[par], 8);
+    dso[0] = to_operand(dc[par], 0);
+    dso[1] = to_operand(dc[par], 8);
+  };
+  // phase Y of unit (st, mb): its dV/dK MFMAs with elements 0..7 of the next
+  // unit (st2, mb2) in set np, whose context is loaded first (if NEXT)
+  auto phaseY = [&](auto next_tag, int st, int mb, const bf16x8 (&pfc)[2], const bf16x8 (&dsc)[2],
+                    int np, int st2, int mb2) {
+    constexpr bool NEXT = decltype(next_tag)::value;
+    if constexpr (NEXT) load_ctx(st2, mb2);
+    const u16* sQ = sQbuf + (st % NBUF) * BQ * RPAD;
+    const u16* sdO = sdObuf + (st % NBUF) * BQ * RPAD;
+    // MFMA q: db = q / 4, kk = (q / 2) % 2, dV (even q) or dK (odd q)
+    auto opnd = [&](int q) {
+      return ld_operand_tr<RPAD>((q & 1) ? sQ : sdO, (2 * mb + ((q >> 1) & 1)) * 16, (q >> 2) * 32);
+    };
+    constexpr int NQ = 4 * DB;
+    bf16x8 op[3];
+    op[0] = opnd(0);
+    op[1] = opnd(1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      if (q + 2 < NQ) op[(q + 2) % 3] = opnd(q + 2);
+      const int db = q >> 2, kk = (q >> 1) & 1;
+      if (q & 1)
+        dk[db] = mfma32(op[q % 3], dsc[kk], dk[db]);
+      else
+        dv[db] = mfma32(op[q % 3], pfc[kk], dv[db]);
+      if constexpr (NEXT) {
+        if ((q & 1) && (q >> 1) < 8) elem(np, q >> 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (NEXT) {
+#pragma unroll
+      for (int r = NQ / 2; r < 8; ++r) elem(np, r);   // D = 64: the rest
+    }
+  };
+
   // Software pipeline over half-step units, one barrier per step: the next
   // unit's S and dP MFMAs are issued before this unit's dV and dK MFMAs, and
   // the next unit's exponentials follow them.  Block st+2 is written into the
@@ -417,25 +530,61 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   if (steps > 2) load_step(2);
   __syncthreads();
   bf16x8 pf[2], dsf[2];
-  scores_mfma(0, 0);
-  scores_valu(0, 0, pf, dsf);
-  for (int st = 0; st + 1 < steps; ++st) {
-    if (st + 2 < steps) {
-      store_block((st + 2) % NBUF);
-      if (st + 3 < steps) load_step(st + 3);
+  if constexpr (IV) {
+    scores_mfma(0, 0);
+    scores_valu(0, 0, pf, dsf);
+    for (int st = 0; st + 1 < steps; ++st) {
+      if (st + 2 < steps) {
+        store_block((st + 2) % NBUF);
+        if (st + 3 < steps) load_step(st + 3);
+      }
+      scores_mfma(st, 1);
+      accumulate(st, 0, pf, dsf);
+      scores_valu(st, 1, pf, dsf);
+      scores_mfma(st + 1, 0);
+      accumulate(st, 1, pf, dsf);
+      scores_valu(st + 1, 0, pf, dsf);
+      __syncthreads();
     }
-    scores_mfma(st, 1);
-    accumulate(st, 0, pf, dsf);
-    scores_valu(st, 1, pf, dsf);
-    scores_mfma(st + 1, 0);
-    accumulate(st, 1, pf, dsf);
-    scores_valu(st + 1, 0, pf, dsf);
-    __syncthreads();
+    scores_mfma(steps - 1, 1);
+    accumulate(steps - 1, 0, pf, dsf);
+    scores_valu(steps - 1, 1, pf, dsf);
+    accumulate(steps - 1, 1, pf, dsf);
+  } else {
+    using yes = std::true_type;
+    using no = std::false_type;
+    // unit (0, 0): S/dP into set 0, its context, elements 0..7
+    load_ctx(0, 0);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      sc[0][r] = 0.f;
+      dc[0][r] = 0.f;
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int off = c * RPAD + ks * 16 + g * 8;
+      sc[0] = mfma32(as_bf16x8(ld16(&sQbuf[off])), kf[ks], sc[0]);
+      dc[0] = mfma32(as_bf16x8(ld16(&sdObuf[off])), vf[ks], dc[0]);
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) elem(0, r);
+    for (int st = 0; st + 1 < steps; ++st) {
+      if (st + 2 < steps) {
+        store_block((st + 2) % NBUF);
+        if (st + 3 < steps) load_step(st + 3);
+      }
+      phaseX(yes{}, 0, st, 1, pf, dsf);          // S/dP of (st, 1); finish (st, 0)
+      phaseY(yes{}, st, 0, pf, dsf, 1, st, 1);   // dV/dK of (st, 0); start (st, 1)
+      phaseX(yes{}, 1, st + 1, 0, pf, dsf);      // S/dP of (st+1, 0); finish (st, 1)
+      phaseY(yes{}, st, 1, pf, dsf, 0, st + 1, 0);
+      __syncthreads();
+    }
+    const int st = steps - 1;
+    phaseX(yes{}, 0, st, 1, pf, dsf);
+    phaseY(yes{}, st, 0, pf, dsf, 1, st, 1);
+    phaseX(no{}, 1, st, 1, pf, dsf);
+    phaseY(no{}, st, 1, pf, dsf, 0, st, 1);
   }
-  scores_mfma(steps - 1, 1);
-  accumulate(steps - 1, 0, pf, dsf);
-  scores_valu(steps - 1, 1, pf, dsf);
-  accumulate(steps - 1, 1, pf, dsf);
 
   if (!kok) return;
   if (slot < 0) {
