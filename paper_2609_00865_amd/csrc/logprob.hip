@@ -206,20 +206,23 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
   }
   __syncthreads();
   read_frags(0, 0, 0);
-  for (int kk = 0; kk < nk; ++kk) {
+  // (the last slice is peeled: a loop body without a path around the barrier
+  // lets the second MFMA group start without waiting for the reads behind it)
+  for (int kk = 0; kk + 1 < nk; ++kk) {
     read_frags(1, kk, 1);
     mma(0);
-    if (kk + 1 < nk) {
-      // slice kk + 1 is the only one in flight; after the barrier it is
-      // visible to every wave and every wave has read all of slice kk, whose
-      // buffer then takes slice kk + 2
-      wait_vmcnt<0>();
-      __syncthreads();
-      if (kk + 2 < nk) issue(kk + 2);
-      read_frags(0, kk + 1, 0);
-    }
+    // slice kk + 1 is the only one in flight; after the barrier it is visible
+    // to every wave and every wave has read all of slice kk, whose buffer
+    // then takes slice kk + 2
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (kk + 2 < nk) issue(kk + 2);
+    read_frags(0, kk + 1, 0);
     mma(1);
   }
+  read_frags(1, nk - 1, 1);
+  mma(0);
+  mma(1);
 
   // acc[i][j][r]: A row rb + i*16 + r, token tb + j*16
   const int rb = a0 + wa * 128 + (lane >> 4) * 4;
