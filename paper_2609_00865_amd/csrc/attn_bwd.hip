@@ -71,12 +71,15 @@ template <int D, bool IV>
 __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
   constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
   constexpr int KS = D / 16, DB = D / 32;
-  constexpr int RPAD = D + 8;
+  // row strides (elements): V rows are read along the rows only (d + 8 is
+  // conflict-free for that), K rows also with the transposing read (d + 24:
+  // conflict-free row reads, transposing reads at most two-way)
+  constexpr int VPAD = D + 8, KPAD = D + 24;
   constexpr int RLD = BK * D / 8 / 256;          // row-major K and V loads per thread
 
   // two buffers: key tile e+1 is written while tile e is read
-  __shared__ __align__(16) u16 sKbuf[2 * BK * RPAD];
-  __shared__ __align__(16) u16 sVbuf[2 * BK * RPAD];
+  __shared__ __align__(16) u16 sKbuf[2 * BK * KPAD];
+  __shared__ __align__(16) u16 sVbuf[2 * BK * VPAD];
   __shared__ __align__(16) int sOmbuf[2 * BK];
 
   int xcd, local;
@@ -132,8 +135,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
     reg_j0 = j0;
   };
   auto store_tile = [&](int buf) {
-    u16* k_ = sKbuf + buf * BK * RPAD;
-    u16* v_ = sVbuf + buf * BK * RPAD;
+    u16* k_ = sKbuf + buf * BK * KPAD;
+    u16* v_ = sVbuf + buf * BK * VPAD;
     // only the ragged last tile has keys past T (a block-uniform branch)
     const bool ragged = reg_j0 + BK > T;
 #pragma unroll
@@ -141,8 +144,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
       if (ragged && reg_j0 + row >= T) kreg[r] = vreg[r] = make_uint4(0, 0, 0, 0);
-      st16(&v_[row * RPAD + col], vreg[r]);
-      st16(&k_[row * RPAD + col], kreg[r]);
+      st16(&v_[row * VPAD + col], vreg[r]);
+      st16(&k_[row * KPAD + col], kreg[r]);
     }
     sOmbuf[buf * BK + tid % BK] = reg_j0 + tid % BK < T ? omreg : 0;  // identical copies
   };
@@ -164,8 +167,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       store_tile(buf ^ 1);
       if (e + 2 < e1) load_tile(a.mask.k_list[e + 2] >> 1);
     }
-    const u16* sK = sKbuf + buf * BK * RPAD;
-    const u16* sV = sVbuf + buf * BK * RPAD;
+    const u16* sK = sKbuf + buf * BK * KPAD;
+    const u16* sV = sVbuf + buf * BK * VPAD;
     const int* sOm = sOmbuf + buf * BK;
     const int j0 = kt * BK;
 
@@ -181,9 +184,9 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       }
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const int off = (kb * 32 + c) * RPAD + ks * 16 + g * 8;
-        s = mfma32(as_bf16x8(ld16(&sK[off])), qf[ks], s);
-        dp = mfma32(as_bf16x8(ld16(&sV[off])), df[ks], dp);
+        const int col = ks * 16 + g * 8, row = kb * 32 + c;
+        s = mfma32(as_bf16x8(ld16(&sK[row * KPAD + col])), qf[ks], s);
+        dp = mfma32(as_bf16x8(ld16(&sV[row * VPAD + col])), df[ks], dp);
       }
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
@@ -209,7 +212,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
           // K^T operand: column block db of keys (2 kb + kk)*16.. in accumulator order
-          acc[db] = mfma32(ld_operand_tr<RPAD>(sK, (2 * kb + kk) * 16, db * 32), dsf[kk], acc[db]);
+          acc[db] = mfma32(ld_operand_tr<KPAD>(sK, (2 * kb + kk) * 16, db * 32), dsf[kk], acc[db]);
         }
     }
     __syncthreads();
@@ -238,7 +241,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   constexpr int KS = D / 16, DB = D / 32;
   constexpr int MB = BQ / 32;              // 32-row MFMA blocks of a row block
   constexpr int KQ = BQ / 16;              // 16-row k steps of the dV / dK products
-  constexpr int RPAD = D + 48;
+  // row stride d + 40: conflict-free row reads, transposing reads at most two-way
+  constexpr int RPAD = D + 40;
   constexpr int RLD = BQ * (D / 8) / 256;  // 16-byte row loads per thread per tensor
 
   // Q and dO blocks are staged row-major only; their transposed operands are
