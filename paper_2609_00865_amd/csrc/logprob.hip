@@ -45,10 +45,6 @@ constexpr int SLICE_B = 256 * BKK * 2;             // bytes of one operand's k s
 constexpr int NLD = SLICE_B / 1024 / NWAVES;       // direct loads per operand, thread and slice
 constexpr int FA = 8, FB = 4;                      // 16-row MFMA blocks per wave: A rows, tokens
 static_assert(NLD * NWAVES * 1024 == SLICE_B, "slice split over the waves");
-// dW engine: k-major slices [64 tokens][256 (+32 pad)] of both operands; the
-// 576-byte row stride puts the four rows one transposing read touches 16 banks apart
-constexpr int WPAD = BA + 32;
-constexpr int DW_STAGE = 2 * BKK * WPAD;           // u16 per stage (both operands)
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int vocab_pad(int V) { return (V + BA - 1) / BA * BA; }
 }  // namespace
@@ -80,6 +76,7 @@ struct LmArgs {
   const float* dkl;   // [n] upstream gradient of each leaf's KL
   int n_leaves, n_rows_T, n_rows_S;
   int T, H, V, Vp, n_chunks;
+  int Tg;              // rows of G: T rounded up to a multiple of 64 (zero past T)
   int nA, nT;         // tiles along the A side and along tokens
   // dH mode split over the vocabulary (K) when there are too few output
   // tiles to fill the chip: split s covers k slices [s*nk_split, ...) and
@@ -260,10 +257,12 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
 #pragma unroll
     for (int j = 0; j < FB; ++j) {
       const int t = tb + j * 16;
-      if (t >= a.T) continue;
-      const int y = a.tgt[t];
-      const float ng = y >= 0 ? -a.g[t] : 0.f;
-      const float l2 = a.lse[t] * kLog2e;
+      if (t >= a.Tg) continue;
+      // rows T .. Tg - 1 are written as zeros (they pad the dW product's k)
+      const int tc = min(t, a.T - 1);
+      const int y = a.tgt[tc];
+      const float ng = (y >= 0 && t < a.T) ? -a.g[tc] : 0.f;
+      const float l2 = a.lse[tc] * kLog2e;
       u16* out = a.Gout + size_t(t) * a.Vp + rb;
 #pragma unroll
       for (int i = 0; i < FA; ++i) {
@@ -384,23 +383,77 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
 
 // dW[v][c] = sum_t G[t][v] H[t][c] (fp32 out).  Same tile shape as the tile
 // engine (256 vocabulary rows x 256 hidden columns, 8 waves of 128 x 64) with
-// MFMA 32x32x16; k = tokens.  Both operands are staged k-major
-// ([64 tokens][256]) through registers into padded LDS rows and read with the
-// transposing LDS read; the token rows past T of the last slice are zeroed.
+// MFMA 32x32x16; k = tokens, along which neither operand is contiguous.  Both
+// k slices ([64 tokens][256]) go from HBM straight into LDS, two in flight,
+// as unpadded 512-byte rows with 16-byte chunk c of token row r at position
+// c ^ ((r & 3) << 2): the transposing operand reads (four token rows x 64
+// bytes per 32 lanes) then hit distinct banks.  G's rows are padded with zeros
+// to a multiple of 64 tokens (the grad pass writes them), so the last slice
+// needs no masking: H rows past T are read clamped and meet zero G rows.
 __global__ __launch_bounds__(NWAVES * 64, 1) void lm_dw_kernel(LmArgs a) {
-  constexpr int NT = NWAVES * 64;
   constexpr int WC = BT / (NWAVES / 2);    // hidden columns per wave (64)
   constexpr int NJ = WC / 32;
-  constexpr int LDA = (BA * BKK / 8) / NT; // 16-byte loads per thread, G slice
-  constexpr int LDB = (BT * BKK / 8) / NT; // 16-byte loads per thread, H slice
-  __shared__ __align__(16) u16 smem[2 * DW_STAGE];
+  __shared__ __align__(1024) u16 smem[2 * 2 * SLICE_B / 2];   // 2 slices x (G, H)
 
   int a0, t0, split;
   if (!tile_of(a, 1, a0, t0, split)) return;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 31, g = lane >> 5;
   const int wa = wave / (NWAVES / 2), wt = wave % (NWAVES / 2);
-  const int nk = (a.T + BKK - 1) / BKK;
+  const int nk = a.Tg / BKK;
+
+  // load i of this wave fills 16-byte slots (i * NWAVES + wave) * 64 + lane:
+  // token row s / 32, chunk (s % 32) ^ ((row & 3) << 2)
+  const u16* srcG[NLD];
+  int hrow[NLD], hcol[NLD];
+#pragma unroll
+  for (int i = 0; i < NLD; ++i) {
+    const int s = (i * NWAVES + wave) * 64 + lane;
+    const int row = s >> 5, ch = (s & 31) ^ ((row & 3) << 2);
+    srcG[i] = a.G + size_t(row) * a.Vp + a0 + ch * 8;
+    hrow[i] = row;
+    hcol[i] = min(t0 + ch * 8, a.H - 8);   // hidden columns past H: outputs skipped
+  }
+  typedef __attribute__((address_space(3))) u16 lds_u16;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u16*)smem;
+  auto issue = [&](int kk) {
+    const uint32_t st = lds0 + (kk & 1) * (2 * SLICE_B) + wave * 1024;
+    const int k0 = kk * BKK;
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      lds_load16(srcG[i] + size_t(k0) * a.Vp, st + i * NWAVES * 1024);
+      const int t = min(k0 + hrow[i], a.T - 1);
+      lds_load16(a.h + size_t(t) * a.H + hcol[i], st + SLICE_B + i * NWAVES * 1024);
+    }
+  };
+
+  // transposing operand read (k order of ld_operand_tr<., true>): lane l of a
+  // 16-lane group reads token rows rb + (lane/32)*8 + l/4 and + 4, columns
+  // col0 + ((lane/16) % 2)*16 + 4 (l % 4); with rb a multiple of 16 and col0 a
+  // multiple of 32 the swizzle term of a lane is fixed
+  const int l = lane & 15;
+  const int rl = (lane >> 5) * 8 + (l >> 2);
+  const int fl = (l >> 2) & 3;
+  const int cl = ((((lane >> 4) & 1) * 2 + ((l & 3) >> 1)) << 3) + ((4 * (l & 3)) & 7);
+  const char* lds = reinterpret_cast<const char*>(smem);
+  auto tr = [&](const u16* tile, int rb, int cg) {   // cg = col0 / 32
+    const u16* p0 = tile + (rb + rl) * 256 + (((cg ^ fl) << 5) + cl);
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0 + 4 * 256));
+    typedef short i16x8 __attribute__((ext_vector_type(8)));
+    const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+  };
+  bf16x8 af[2][4], bfr[2][NJ];
+  auto read_frags = [&](int buf, int kk, int ks) {
+    const u16* sG = reinterpret_cast<const u16*>(lds + (kk & 1) * (2 * SLICE_B));
+    const u16* sH = reinterpret_cast<const u16*>(lds + (kk & 1) * (2 * SLICE_B) + SLICE_B);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) af[buf][i] = tr(sG, ks * 16, wa * 4 + i);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) bfr[buf][j] = tr(sH, ks * 16, wt * NJ + j);
+  };
 
   f32x16 acc[4][NJ];
 #pragma unroll
@@ -409,91 +462,57 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_dw_kernel(LmArgs a) {
     for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  uint4 ra[LDA], rb[LDB];
-  auto load = [&](int k0) {
-    // G slice [64 tokens][256 vocabulary] and H slice [64 tokens][256
-    // hidden]; token rows past T must add nothing (k is summed): the tail
-    // slice zeroes them (a block-uniform branch, taken once per tile)
-    auto stage = [&](bool tail) {
+  auto mma = [&](int buf) {
 #pragma unroll
-      for (int r = 0; r < LDA; ++r) {
-        const int idx = tid + r * NT;
-        const int row = idx / (BA / 8), cc = (idx % (BA / 8)) * 8;
-        const int t = k0 + row;
-        ra[r] = ld16(a.G + size_t(min(t, a.T - 1)) * a.Vp + a0 + cc);
-        if (tail && t >= a.T) ra[r] = make_uint4(0, 0, 0, 0);
-      }
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int r = 0; r < LDB; ++r) {
-        const int idx = tid + r * NT;
-        const int row = idx / (BT / 8), cc = (idx % (BT / 8)) * 8;
-        const int t = k0 + row;
-        rb[r] = ld16(a.h + size_t(min(t, a.T - 1)) * a.H + min(t0 + cc, a.H - 8));
-        if (tail && t >= a.T) rb[r] = make_uint4(0, 0, 0, 0);
-      }
-    };
-    if (k0 + BKK > a.T)
-      stage(true);
-    else
-      stage(false);
-  };
-  auto store = [&](u16* sA) {
-    u16* sB = sA + BKK * WPAD;
-#pragma unroll
-    for (int r = 0; r < LDA; ++r) {
-      const int idx = tid + r * NT;
-      st16(&sA[(idx / (BA / 8)) * WPAD + (idx % (BA / 8)) * 8], ra[r]);
-    }
-#pragma unroll
-    for (int r = 0; r < LDB; ++r) {
-      const int idx = tid + r * NT;
-      st16(&sB[(idx / (BT / 8)) * WPAD + (idx % (BT / 8)) * 8], rb[r]);
-    }
+      for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32(af[buf][i], bfr[buf][j], acc[i][j]);
   };
 
-  load(0);
-  store(smem);
-  if (nk > 1) load(BKK);
-  __syncthreads();
-  for (int kk = 0; kk < nk; ++kk) {
-    const u16* sA = smem + (kk & 1) * DW_STAGE;
-    const u16* sB = sA + BKK * WPAD;
-    // The next slice goes to the other buffer first (every wave finished
-    // reading it before the last barrier), then the slice after it is
-    // requested from HBM, so both overlap this slice's MFMAs.
-    if (kk + 1 < nk) {
-      store(smem + ((kk + 1) & 1) * DW_STAGE);
-      if (kk + 2 < nk) load((kk + 2) * BKK);
-    }
-#pragma unroll
-    for (int ks = 0; ks < BKK / 16; ++ks) {
-      bf16x8 af[4], bf[NJ];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = ld_operand_tr<WPAD, true>(sA, ks * 16, wa * 128 + i * 32);
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) bf[j] = ld_operand_tr<WPAD, true>(sB, ks * 16, wt * WC + j * 32);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
-    }
-    __syncthreads();
+  // four 16-token k steps per slice; one barrier per slice (as in the tile engine)
+  issue(0);
+  if (nk > 1) {
+    issue(1);
+    wait_vmcnt<2 * NLD>();
+  } else {
+    wait_vmcnt<0>();
   }
+  __syncthreads();
+  read_frags(0, 0, 0);
+  for (int kk = 0; kk + 1 < nk; ++kk) {
+    read_frags(1, kk, 1);
+    mma(0);
+    read_frags(0, kk, 2);
+    mma(1);
+    read_frags(1, kk, 3);
+    mma(0);
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (kk + 2 < nk) issue(kk + 2);
+    read_frags(0, kk + 1, 0);
+    mma(1);
+  }
+  read_frags(1, nk - 1, 1);
+  mma(0);
+  read_frags(0, nk - 1, 2);
+  mma(1);
+  read_frags(1, nk - 1, 3);
+  mma(0);
+  mma(1);
 
   // acc[i][j][r]: vocabulary row a0 + wa*128 + i*32 + (r/4)*8 + g*4 + r%4,
   //               hidden column t0 + wt*WC + j*32 + c
   const int arow0 = a0 + wa * 128;
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
-    const int hcol = t0 + wt * WC + j * 32 + c;
-    if (hcol >= a.H) continue;
+    const int hc = t0 + wt * WC + j * 32 + c;
+    if (hc >= a.H) continue;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int v = arow0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-        if (v < a.V) a.dw[size_t(v) * a.H + hcol] = acc[i][j][r];
+        if (v < a.V) a.dw[size_t(v) * a.H + hc] = acc[i][j][r];
       }
   }
 }
@@ -688,9 +707,11 @@ size_t logprob_fwd_ws_bytes(int T, int H, int V) {
          256;
 }
 
-// G [T, Vp] | dH partials | W^T [H, Vp]
+static int g_rows(int T) { return (T + BKK - 1) / BKK * BKK; }
+
+// G [Tg, Vp] | dH partials | W^T [H, Vp]
 size_t logprob_bwd_ws_bytes(int T, int H, int V) {
-  return align256(size_t(T) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(T, H) +
+  return align256(size_t(g_rows(T)) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(T, H) +
          wT_bytes(H, V) + 256;
 }
 
@@ -804,9 +825,10 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
   a.H = H;
   a.V = V;
   a.Vp = vocab_pad(V);
+  a.Tg = g_rows(T);
   char* base = align_ptr(ws);
   u16* G = reinterpret_cast<u16*>(base);
-  float* part = reinterpret_cast<float*>(base + align256(size_t(T) * a.Vp * sizeof(u16)));
+  float* part = reinterpret_cast<float*>(base + align256(size_t(a.Tg) * a.Vp * sizeof(u16)));
   u16* wT = reinterpret_cast<u16*>(reinterpret_cast<char*>(part) + dh_part_bytes(T, H));
   a.Gout = G;
   a.G = G;
@@ -835,6 +857,7 @@ hipError_t launch_logprob_dweight(int T, int H, int V, const void* hidden, const
   a.G = reinterpret_cast<const u16*>(align_ptr(const_cast<void*>(ws)));
   a.dw = dw;
   a.T = T;
+  a.Tg = g_rows(T);
   a.H = H;
   a.V = V;
   a.Vp = vocab_pad(V);
