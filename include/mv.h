@@ -271,7 +271,8 @@ mv_status mv_rope(const mv_branch_pack* p, const void* x, int32_t n_heads, int32
  * head_dim]; K, V, dK, dV are [total_tokens, n_heads_kv, head_dim].  Query
  * head h reads KV head h / (n_heads_q / n_heads_kv).  LSE is fp32
  * [n_heads_q, total_tokens], natural log.  Q and K are taken as given
- * (already position-encoded).  head_dim in {64, 128}.
+ * (already position-encoded).  head_dim in {64, 128}; each tensor under
+ * 4 GiB (total_tokens * n_heads_q * head_dim * 2 bytes < 2^32).
  * ------------------------------------------------------------------------ */
 typedef struct {
   int32_t total_tokens;          /* must equal the mask's                          */

@@ -121,6 +121,9 @@ mv_status check_attn(const mv_view_mask* m, const mv_attn_shape* s) {
   if (s->head_dim != 64 && s->head_dim != 128)
     return fail(MV_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
   if (!std::isfinite(s->softmax_scale)) return fail(MV_ERR_INVALID_ARG, "softmax_scale not finite");
+  // the kernels address each tensor with 32-bit byte offsets
+  if (int64_t(s->total_tokens) * s->n_heads_q * s->head_dim * 2 >= (int64_t(1) << 32))
+    return fail(MV_ERR_UNSUPPORTED, "each of Q, K, V, O must be under 4 GiB");
   return MV_OK;
 }
 

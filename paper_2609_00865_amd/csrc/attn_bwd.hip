@@ -113,41 +113,42 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
 
-  const size_t kv_row = size_t(a.Hkv) * D;
-  const u16* kbase = a.k + size_t(hk) * D;
-  const u16* vbase = a.v + size_t(hk) * D;
+  // K and V of KV head hk through raw buffers ending at the last row's end:
+  // keys past T read as zeros (omega 0: visible to no row), so the ragged
+  // last tile needs no clamp and no branch
+  const uint32_t kv_row = uint32_t(a.Hkv) * D * 2;   // bytes per key row
+  const uint32_t kv_bytes = uint32_t(T) * kv_row - uint32_t(hk) * D * 2;
+  const rsrc_t krs = make_rsrc(a.k + size_t(hk) * D, kv_bytes);
+  const rsrc_t vrs = make_rsrc(a.v + size_t(hk) * D, kv_bytes);
+  const rsrc_t omrs = make_rsrc(a.mask.omega, uint32_t(T) * 4);
+  uint32_t ldoff[RLD];   // byte offset of this thread's 16-byte chunks in a tile
+#pragma unroll
+  for (int r = 0; r < RLD; ++r) {
+    const int idx = tid + r * 256;
+    ldoff[r] = uint32_t(idx / (D / 8)) * kv_row + (idx % (D / 8)) * 16;
+  }
   uint4 vreg[RLD], kreg[RLD];
   int omreg = 0;
-  int reg_j0 = 0;  // first key of the tile held in the registers
   auto load_tile = [&](int kt) {
-    const int j0 = kt * BK;
+    const uint32_t t0 = uint32_t(kt) * BK * kv_row;
 #pragma unroll
     for (int r = 0; r < RLD; ++r) {
-      const int idx = tid + r * 256;
-      const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      // keys past T load a clamped (valid) row, zeroed when stored: no
-      // branch, and nothing waits on the loads before the store
-      const int jc = min(j0 + row, T - 1);
-      vreg[r] = ld16(vbase + size_t(jc) * kv_row + col);
-      kreg[r] = ld16(kbase + size_t(jc) * kv_row + col);
+      vreg[r] = buf_ld16(vrs, t0 + ldoff[r]);
+      kreg[r] = buf_ld16(krs, t0 + ldoff[r]);
     }
-    omreg = a.mask.omega[min(j0 + tid % BK, T - 1)];  // every thread: key tid % BK
-    reg_j0 = j0;
+    omreg = int(buf_ld4(omrs, uint32_t(kt * BK + tid % BK) * 4));  // every thread: key tid % BK
   };
   auto store_tile = [&](int buf) {
     u16* k_ = sKbuf + buf * BK * KPAD;
     u16* v_ = sVbuf + buf * BK * VPAD;
-    // only the ragged last tile has keys past T (a block-uniform branch)
-    const bool ragged = reg_j0 + BK > T;
 #pragma unroll
     for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      if (ragged && reg_j0 + row >= T) kreg[r] = vreg[r] = make_uint4(0, 0, 0, 0);
       st16(&v_[row * VPAD + col], vreg[r]);
       st16(&k_[row * KPAD + col], kreg[r]);
     }
-    sOmbuf[buf * BK + tid % BK] = reg_j0 + tid % BK < T ? omreg : 0;  // identical copies
+    sOmbuf[buf * BK + tid % BK] = omreg;  // identical copies
   };
 
   // Tile e+1 is stored into the idle buffer (read by every wave before the
@@ -291,46 +292,45 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       dv[db][r] = 0.f;
     }
 
-  const size_t q_row = size_t(a.Hq) * D;
+  // Q and dO of head hh through raw buffers ending at the last row's end:
+  // rows past T read as zeros (and LSE, D as 0), so the ragged last block
+  // needs no clamp and no branch
+  const uint32_t q_row = uint32_t(a.Hq) * D * 2;     // bytes per query row
+  uint32_t ldoff[RLD];   // byte offset of this thread's 16-byte chunks in a block
+#pragma unroll
+  for (int r = 0; r < RLD; ++r) {
+    const int idx = tid + r * 256;
+    ldoff[r] = uint32_t(idx / (D / 8)) * q_row + (idx % (D / 8)) * 16;
+  }
   uint4 qreg[RLD], dreg[RLD];
   float lreg = 0.f, dreg1 = 0.f;
-  int reg_i0 = 0;  // first row of the block held in qreg / dreg
   auto load_block = [&](int hh, int qb) {
-    const int i0 = qb * BQ;
-    const u16* qb_ = a.q + size_t(hh) * D;
-    const u16* db_ = a.dout + size_t(hh) * D;
+    const uint32_t bytes = uint32_t(T) * q_row - uint32_t(hh) * D * 2;
+    const rsrc_t qrs = make_rsrc(a.q + size_t(hh) * D, bytes);
+    const rsrc_t drs = make_rsrc(a.dout + size_t(hh) * D, bytes);
+    const uint32_t b0 = uint32_t(qb) * BQ * q_row;
 #pragma unroll
     for (int r = 0; r < RLD; ++r) {
-      const int idx = tid + r * 256;
-      const int row = idx / (D / 8), cc = idx % (D / 8);
-      // rows past T load a clamped (valid) row, zeroed when stored: no
-      // branch, and nothing waits on the loads before the store
-      const int ic = min(i0 + row, T - 1);
-      qreg[r] = ld16(qb_ + size_t(ic) * q_row + cc * 8);
-      dreg[r] = ld16(db_ + size_t(ic) * q_row + cc * 8);
+      qreg[r] = buf_ld16(qrs, b0 + ldoff[r]);
+      dreg[r] = buf_ld16(drs, b0 + ldoff[r]);
     }
     // every thread takes row tid % BQ's LSE and D (identical copies)
-    const int ic = min(i0 + tid % BQ, T - 1);
-    lreg = a.lse[size_t(hh) * T + ic];
-    dreg1 = a.Dd[size_t(hh) * T + ic];
-    reg_i0 = i0;
+    const uint32_t roff = uint32_t(qb * BQ + tid % BQ) * 4;
+    lreg = __builtin_bit_cast(float, buf_ld4(make_rsrc(a.lse + size_t(hh) * T, uint32_t(T) * 4), roff));
+    dreg1 = __builtin_bit_cast(float, buf_ld4(make_rsrc(a.Dd + size_t(hh) * T, uint32_t(T) * 4), roff));
   };
   auto store_block = [&](int buf) {
     u16* q_ = sQbuf + buf * BQ * RPAD;
     u16* d_ = sdObuf + buf * BQ * RPAD;
-    // only the ragged last block has rows past T (a block-uniform branch)
-    const bool ragged = reg_i0 + BQ > T;
 #pragma unroll
     for (int r = 0; r < RLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), cc = idx % (D / 8);
-      if (ragged && reg_i0 + row >= T) qreg[r] = dreg[r] = make_uint4(0, 0, 0, 0);
       st16(&q_[row * RPAD + cc * 8], qreg[r]);
       st16(&d_[row * RPAD + cc * 8], dreg[r]);
     }
-    const bool ok = reg_i0 + tid % BQ < T;
-    sLbuf[buf * BQ + tid % BQ] = ok ? lreg * kLog2e : 0.f;
-    sDbuf[buf * BQ + tid % BQ] = ok ? dreg1 : 0.f;
+    sLbuf[buf * BQ + tid % BQ] = lreg * kLog2e;
+    sDbuf[buf * BQ + tid % BQ] = dreg1;
   };
 
   const int nqb = qb1 - qb0;

@@ -70,42 +70,43 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  const size_t kv_row = size_t(a.Hkv) * D;
-  const u16* kbase = a.k + size_t(hk) * D;
-  const u16* vbase = a.v + size_t(hk) * D;
+  // K and V of KV head hk through raw buffers ending at the last row's end:
+  // keys past T read as zeros (and omega 0, visible to no row), so the
+  // ragged last tile needs no clamp and no branch.
+  const uint32_t kv_row = uint32_t(a.Hkv) * D * 2;   // bytes per key row
+  const uint32_t kv_bytes = uint32_t(T) * kv_row - uint32_t(hk) * D * 2;
+  const rsrc_t krs = make_rsrc(a.k + size_t(hk) * D, kv_bytes);
+  const rsrc_t vrs = make_rsrc(a.v + size_t(hk) * D, kv_bytes);
+  const rsrc_t omrs = make_rsrc(a.mask.omega, uint32_t(T) * 4);
+  uint32_t ldoff[KLD];   // byte offset of this thread's 16-byte chunks in a tile
+#pragma unroll
+  for (int r = 0; r < KLD; ++r) {
+    const int idx = tid + r * 256;
+    ldoff[r] = uint32_t(idx / (D / 8)) * kv_row + (idx % (D / 8)) * 16;
+  }
 
   uint4 kreg[KLD], vreg[KLD];
   int omreg = 0;
-  int reg_j0 = 0;  // first key of the tile held in the registers
   auto load_tile = [&](int kt) {
-    const int j0 = kt * BK;
+    const uint32_t t0 = uint32_t(kt) * BK * kv_row;
 #pragma unroll
     for (int r = 0; r < KLD; ++r) {
-      const int idx = tid + r * 256;
-      const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      // keys past T load a clamped (valid) row, zeroed when stored: no
-      // branch, and nothing waits on the loads before the store
-      const int jc = min(j0 + row, T - 1);
-      kreg[r] = ld16(kbase + size_t(jc) * kv_row + col);
-      vreg[r] = ld16(vbase + size_t(jc) * kv_row + col);
+      kreg[r] = buf_ld16(krs, t0 + ldoff[r]);
+      vreg[r] = buf_ld16(vrs, t0 + ldoff[r]);
     }
-    omreg = a.mask.omega[min(j0 + tid % BK, T - 1)];  // every thread: key tid % BK
-    reg_j0 = j0;
+    omreg = int(buf_ld4(omrs, uint32_t(kt * BK + tid % BK) * 4));  // every thread: key tid % BK
   };
   auto store_tile = [&](int buf) {
     u16* k_ = sKbuf + buf * BK * KPAD;
     u16* v_ = sVbuf + buf * BK * VPAD;
-    // only the ragged last tile has keys past T (a block-uniform branch)
-    const bool ragged = reg_j0 + BK > T;
 #pragma unroll
     for (int r = 0; r < KLD; ++r) {
       const int idx = tid + r * 256;
       const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      if (ragged && reg_j0 + row >= T) kreg[r] = vreg[r] = make_uint4(0, 0, 0, 0);
       st16(&k_[row * KPAD + col], kreg[r]);
       st16(&v_[row * VPAD + col], vreg[r]);
     }
-    sOmbuf[buf * BK + tid % BK] = reg_j0 + tid % BK < T ? omreg : 0;  // identical copies
+    sOmbuf[buf * BK + tid % BK] = omreg;  // identical copies
   };
 
   // Tile e+1 is stored into the idle buffer (read by every wave before the

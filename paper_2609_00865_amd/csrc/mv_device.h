@@ -53,6 +53,23 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 
+// A raw buffer over [base, base + bytes) (bytes < 2^32): loads take a 32-bit
+// byte offset in a VGPR, and the hardware's range check returns zeros for an
+// access at or past `bytes`, so the ragged end of a tile needs neither a
+// clamped address nor a branch.  (The range check covers the VGPR offset; no
+// SGPR offset is used.)  Word 3 is the gfx9 descriptor format (32-bit data).
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 buf_ld16(rsrc_t r, uint32_t off) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ uint32_t buf_ld4(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+
 __device__ __forceinline__ void st16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
 
 __device__ __forceinline__ uint32_t bf16_bits(float f) {
