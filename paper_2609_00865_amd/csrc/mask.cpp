@@ -8,6 +8,7 @@
 #include <algorithm>
 #include <array>
 #include <cstring>
+#include <map>
 #include <numeric>
 #include <sstream>
 
@@ -323,9 +324,39 @@ void build_bwd_schedule(mv_view_mask& m) {
       m.bwd_red.push_back(kt);
     }
   }
-  std::stable_sort(items.begin(), items.end(), [](const auto& a, const auto& b) {
-    return (a[2] - a[1]) > (b[2] - b[1]);
-  });
+  // Work order.  Items of eight neighbouring key tiles with the same chunk
+  // index walk nearly the same query blocks (each start two blocks later), so
+  // they form a group that should run side by side on one XCD, sharing the
+  // Q / dO stream in its L2.  Groups go longest first (a greedy balance of
+  // the tail); the dispatcher deals consecutive items to the 8 XCDs round
+  // robin, so run r of 8 items in group order is placed at the positions
+  // that XCD r % 8 takes next.
+  std::vector<std::array<int32_t, 4>> order;
+  {
+    std::map<std::pair<int32_t, int32_t>, std::vector<std::array<int32_t, 4>>> groups;
+    for (const auto& it : items) {
+      const int32_t c = (it[1] - it[0] * BK / BQ) / CH;
+      groups[{it[0] / 8, c}].push_back(it);
+    }
+    std::vector<std::vector<std::array<int32_t, 4>>*> gl;
+    for (auto& kv : groups) gl.push_back(&kv.second);
+    auto len = [](const std::vector<std::array<int32_t, 4>>* g) {
+      int32_t n = 0;
+      for (const auto& it : *g) n = std::max(n, it[2] - it[1]);
+      return n;
+    };
+    std::stable_sort(gl.begin(), gl.end(), [&](auto* a, auto* b) { return len(a) > len(b); });
+    for (auto* g : gl) order.insert(order.end(), g->begin(), g->end());
+  }
+  const size_t n_items = order.size(), full = n_items / 64 * 64;
+  for (size_t p = 0; p < n_items; ++p) {
+    size_t q = p;
+    if (p < full) {
+      const size_t local = p / 8, x = p % 8;
+      q = ((local / 8) * 8 + x) * 8 + local % 8;
+    }
+    items[p] = order[q];
+  }
   m.bwd_items.reserve(items.size() * 4);
   for (const auto& it : items) m.bwd_items.insert(m.bwd_items.end(), it.begin(), it.end());
   m.n_slots = slot;
