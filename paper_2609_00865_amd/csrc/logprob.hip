@@ -43,6 +43,16 @@ constexpr float kLn2 = 0.69314718055994531f;
 // tile engine
 constexpr int SLICE_B = 256 * BKK * 2;             // bytes of one operand's k slice
 constexpr int NLD = SLICE_B / 1024 / NWAVES;       // direct loads per operand, thread and slice
+
+// Panel layout of a bf16 matrix [R][K] (R padded to a multiple of 256, K a
+// multiple of 64), used for G and W^T, the operands of the dH product whose
+// k runs along the vocabulary: the 64-wide k slice of a 256-row block is one
+// contiguous 32 KiB panel of 128-byte rows, so each slice load of a tile is
+// one linear read instead of 256 rows a vocabulary row (~300 KB) apart.
+constexpr int PANEL = 256 * 64;
+__host__ __device__ inline size_t panel_index(int r, int k, int K) {
+  return (size_t(r >> 8) * (K >> 6) + (k >> 6)) * PANEL + (r & 255) * 64 + (k & 63);
+}
 constexpr int FA = 8, FB = 4;                      // 16-row MFMA blocks per wave: A rows, tokens
 static_assert(NLD * NWAVES * 1024 == SLICE_B, "slice split over the waves");
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -76,7 +86,7 @@ struct LmArgs {
   const float* dkl;   // [n] upstream gradient of each leaf's KL
   int n_leaves, n_rows_T, n_rows_S;
   int T, H, V, Vp, n_chunks;
-  int Tg;              // rows of G: T rounded up to a multiple of 64 (zero past T)
+  int Tg;              // rows of G: T rounded up to a multiple of 256 (zero past T)
   int nA, nT;         // tiles along the A side and along tokens
   // dH mode split over the vocabulary (K) when there are too few output
   // tiles to fill the chip: split s covers k slices [s*nk_split, ...) and
@@ -128,20 +138,27 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
   // Load i of this wave fills 16-byte slots (i * NWAVES + wave) * 64 + lane of
   // each operand's slice: row s / 8, k chunk (s % 8) ^ (row & 7).  Rows past
   // the operands are read from clamped (valid) rows; their products land in
-  // output rows or columns that the epilogues skip.
+  // output rows or columns that the epilogues skip.  The dH product reads
+  // both operands (W^T and G) in the panel layout, the others row-major.
+  constexpr bool PANELS = MODE == kModeDh;
+  constexpr int SSTEP = PANELS ? PANEL : BKK;   // elements from one k slice of a row to the next
   const u16* srcA[NLD];
   const u16* srcB[NLD];
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
     const int s = (i * NWAVES + wave) * 64 + lane;
     const int row = s >> 3, kc = (s & 7) ^ (row & 7);
-    const size_t koff = size_t(kbeg) * BKK + kc * 8;
-    srcA[i] = A + size_t(min(a0 + row, a_rows - 1)) * K + koff;
+    const int ar = min(a0 + row, a_rows - 1);
     const int t = min(t0 + row, a.T - 1);
+    if (PANELS) {
+      srcA[i] = A + panel_index(ar, kbeg * BKK, K) + kc * 8;
+      srcB[i] = a.G + panel_index(t, kbeg * BKK, K) + kc * 8;
+      continue;
+    }
+    const size_t koff = size_t(kbeg) * BKK + kc * 8;
+    srcA[i] = A + size_t(ar) * K + koff;
     const u16* brow;
-    if (MODE == kModeDh) {
-      brow = a.G + size_t(t) * a.Vp;
-    } else if (MODE == kModeKL || MODE == kModeKLGrad) {
+    if (MODE == kModeKL || MODE == kModeKLGrad) {
       // a row index outside its matrix reads as a zero hidden state
       const int r = (t & 1) ? a.rowsS[t >> 1] : a.rowsT[t >> 1];
       const int n_rows = (t & 1) ? a.n_rows_S : a.n_rows_T;
@@ -157,8 +174,8 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
     const uint32_t st = lds0 + (kk & 1) * (2 * SLICE_B) + wave * 1024;
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-      lds_load16(srcA[i] + size_t(kk) * BKK, st + i * NWAVES * 1024);
-      lds_load16(srcB[i] + size_t(kk) * BKK, st + SLICE_B + i * NWAVES * 1024);
+      lds_load16(srcA[i] + size_t(kk) * SSTEP, st + i * NWAVES * 1024);
+      lds_load16(srcB[i] + size_t(kk) * SSTEP, st + SLICE_B + i * NWAVES * 1024);
     }
   };
 
@@ -263,9 +280,9 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
       const int y = a.tgt[tc];
       const float ng = (y >= 0 && t < a.T) ? -a.g[tc] : 0.f;
       const float l2 = a.lse[tc] * kLog2e;
-      u16* out = a.Gout + size_t(t) * a.Vp + rb;
 #pragma unroll
       for (int i = 0; i < FA; ++i) {
+        u16* out = a.Gout + panel_index(t, rb + i * 16, a.Vp);   // 4 consecutive entries
         float vals[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -275,7 +292,7 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
         uint2 wv;
         wv.x = pack2(vals[0], vals[1]);
         wv.y = pack2(vals[2], vals[3]);
-        *reinterpret_cast<uint2*>(out + i * 16) = wv;
+        *reinterpret_cast<uint2*>(out) = wv;
       }
     }
   } else if (MODE == kModeKL) {
@@ -330,9 +347,9 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
       const int lc = leaf < a.n_leaves ? leaf : 0;
       const float gl = a.dkl[lc];
       const float lS = a.lseS[lc] * kLog2e, lT = a.lseT[lc] * kLog2e;
-      u16* out = a.Gout + size_t(lc) * a.Vp + rb;
 #pragma unroll
       for (int i = 0; i < FA; ++i) {
+        u16* out = a.Gout + panel_index(lc, rb + i * 16, a.Vp);
         float vals[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -346,7 +363,7 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
           uint2 wv;
           wv.x = pack2(vals[0], vals[1]);
           wv.y = pack2(vals[2], vals[3]);
-          *reinterpret_cast<uint2*>(out + i * 16) = wv;
+          *reinterpret_cast<uint2*>(out) = wv;
         }
       }
     }
@@ -405,13 +422,12 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_dw_kernel(LmArgs a) {
 
   // load i of this wave fills 16-byte slots (i * NWAVES + wave) * 64 + lane:
   // token row s / 32, chunk (s % 32) ^ ((row & 3) << 2)
-  const u16* srcG[NLD];
-  int hrow[NLD], hcol[NLD];
+  int gcol[NLD], hrow[NLD], hcol[NLD];
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
     const int s = (i * NWAVES + wave) * 64 + lane;
     const int row = s >> 5, ch = (s & 31) ^ ((row & 3) << 2);
-    srcG[i] = a.G + size_t(row) * a.Vp + a0 + ch * 8;
+    gcol[i] = a0 + ch * 8;
     hrow[i] = row;
     hcol[i] = min(t0 + ch * 8, a.H - 8);   // hidden columns past H: outputs skipped
   }
@@ -422,7 +438,7 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_dw_kernel(LmArgs a) {
     const int k0 = kk * BKK;
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-      lds_load16(srcG[i] + size_t(k0) * a.Vp, st + i * NWAVES * 1024);
+      lds_load16(a.G + panel_index(k0 + hrow[i], gcol[i], a.Vp), st + i * NWAVES * 1024);
       const int t = min(k0 + hrow[i], a.T - 1);
       lds_load16(a.h + size_t(t) * a.H + hcol[i], st + SLICE_B + i * NWAVES * 1024);
     }
@@ -551,10 +567,11 @@ __global__ __launch_bounds__(256) void lm_target_kernel(LmArgs a) {
     return;
   }
   const float p = fast_exp2(fmaf(s, kLog2e, -a.lse[t] * kLog2e));
-  a.Gout[size_t(t) * a.Vp + y] = u16(bf16_bits(a.g[t] * (1.f - p)));
+  a.Gout[panel_index(t, y, a.Vp)] = u16(bf16_bits(a.g[t] * (1.f - p)));
 }
 
-// wT[h][v] = w[v][h] for v < V and 0 for V <= v < Vp; 64 x 64 tiles through LDS.
+// wT[h][v] = w[v][h] for v < V and 0 for V <= v < Vp, in the panel layout;
+// 64 x 64 tiles through LDS.
 __global__ __launch_bounds__(256) void transpose_w_kernel(const u16* w, u16* wT, int V, int H,
                                                           int Vp) {
   __shared__ u16 tile[64][72];
@@ -576,7 +593,7 @@ __global__ __launch_bounds__(256) void transpose_w_kernel(const u16* w, u16* wT,
 #pragma unroll
     for (int u = 0; u < 4; ++u)
       e[u] = uint32_t(tile[c + 2 * u][r]) | (uint32_t(tile[c + 2 * u + 1][r]) << 16);
-    st16(wT + size_t(h0 + r) * Vp + v0 + c, make_uint4(e[0], e[1], e[2], e[3]));
+    st16(wT + panel_index(h0 + r, v0 + c, Vp), make_uint4(e[0], e[1], e[2], e[3]));
   }
 }
 
@@ -675,7 +692,12 @@ static size_t dh_part_bytes(int T, int H) {
   return splits > 1 ? align256(size_t(splits) * T * H * sizeof(float)) : 0;
 }
 
-static size_t wT_bytes(int H, int V) { return align256(size_t(H) * vocab_pad(V) * sizeof(u16)); }
+// rows of a panel-layout matrix
+static int panel_rows(int R) { return (R + 255) / 256 * 256; }
+
+static size_t wT_bytes(int H, int V) {
+  return align256(size_t(panel_rows(H)) * vocab_pad(V) * sizeof(u16));
+}
 
 size_t kl_fwd_ws_bytes(int n, int H, int V) {
   const int n_chunks = vocab_pad(V) / 128;
@@ -684,9 +706,9 @@ size_t kl_fwd_ws_bytes(int n, int H, int V) {
          256;
 }
 
-// G [n, Vp] | dH partials | zero row [H] | W^T [H, Vp]
+// G [n, Vp] | dH partials | zero row [H] | W^T [H, Vp] (G and W^T in panels)
 size_t kl_bwd_ws_bytes(int n, int H, int V) {
-  return align256(size_t(n) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(n, H) +
+  return align256(size_t(panel_rows(n)) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(n, H) +
          align256(size_t(H) * sizeof(u16)) + wT_bytes(H, V) + 256;
 }
 
@@ -707,9 +729,9 @@ size_t logprob_fwd_ws_bytes(int T, int H, int V) {
          256;
 }
 
-static int g_rows(int T) { return (T + BKK - 1) / BKK * BKK; }
+static int g_rows(int T) { return panel_rows(T); }
 
-// G [Tg, Vp] | dH partials | W^T [H, Vp]
+// G [Tg, Vp] | dH partials | W^T [H, Vp] (G and W^T in panels)
 size_t logprob_bwd_ws_bytes(int T, int H, int V) {
   return align256(size_t(g_rows(T)) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(T, H) +
          wT_bytes(H, V) + 256;
@@ -928,7 +950,7 @@ hipError_t launch_kl_bwd(int n, int H, int V, const void* hT, int nT, const int3
   a.Vp = vocab_pad(V);
   char* base = align_ptr(ws);
   u16* G = reinterpret_cast<u16*>(base);
-  float* part = reinterpret_cast<float*>(base + align256(size_t(n) * a.Vp * sizeof(u16)));
+  float* part = reinterpret_cast<float*>(base + align256(size_t(panel_rows(n)) * a.Vp * sizeof(u16)));
   u16* zrow = reinterpret_cast<u16*>(reinterpret_cast<char*>(part) + dh_part_bytes(n, H));
   u16* wT = reinterpret_cast<u16*>(reinterpret_cast<char*>(zrow) + align256(size_t(H) * sizeof(u16)));
   a.Gout = G;
