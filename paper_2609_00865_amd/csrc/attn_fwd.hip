@@ -131,16 +131,26 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     const int* sOm = sOmbuf + buf * BK;
     const int j0 = kt * BK;
 
-    // S^T for keys [kb*32, kb*32+32) of the tile
+    // S^T for keys [kb*32, kb*32+32) of the tile.  The two blocks' MFMAs
+    // alternate, and the K fragments are read four MFMAs ahead (a fixed
+    // order: each MFMA waits only for a read issued long before it).
     f32x16 s[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+    {
+      auto kfrag = [&](int st) {   // step st: block st % 2, k step st / 2
+        return as_bf16x8(ld16(&sK[((st & 1) * 32 + c) * KPAD + (st >> 1) * 16 + g * 8]));
+      };
+      bf16x8 kr[4];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 kf = as_bf16x8(ld16(&sK[(kb * 32 + c) * KPAD + ks * 16 + g * 8]));
-        s[kb] = mfma32(kf, qf[ks], s[kb]);
+      for (int st = 0; st < 4; ++st) kr[st] = kfrag(st);
+#pragma unroll
+      for (int st = 0; st < 2 * KS; ++st) {
+        s[st & 1] = mfma32(kr[st & 3], qf[st >> 1], s[st & 1]);
+        if (st + 4 < 2 * KS) kr[st & 3] = kfrag(st + 4);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
 
@@ -197,13 +207,20 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     bf16x8 pf[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) pf[ks] = to_operand(s[ks >> 1], (ks & 1) * 8);
+    {
+      // V^T operand of step st: column block st % DB, keys (st / DB)*16 ..
+      // in accumulator order; read four MFMAs ahead as above
+      auto vfrag = [&](int st) { return ld_operand_tr<VPAD>(sV, (st / DB) * 16, (st % DB) * 32); };
+      bf16x8 vr[4];
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+      for (int st = 0; st < 4; ++st) vr[st] = vfrag(st);
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        // V^T operand: column block db of keys ks*16.. in accumulator order
-        oacc[db] = mfma32(ld_operand_tr<VPAD>(sV, ks * 16, db * 32), pf[ks], oacc[db]);
+      for (int st = 0; st < 4 * DB; ++st) {
+        oacc[st % DB] = mfma32(vr[st & 3], pf[st / DB], oacc[st % DB]);
+        if (st + 4 < 4 * DB) vr[st & 3] = vfrag(st + 4);
+        __builtin_amdgcn_sched_barrier(0);
       }
+    }
     __syncthreads();
   }
 
