@@ -31,15 +31,20 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
   constexpr int KS = D / 16;          // MFMA k-steps over the head dimension
   constexpr int DB = D / 32;          // 32-row blocks of O^T
-  constexpr int KPAD = D + 8;         // K row stride (bf16): row reads across 32 lanes hit distinct banks
-  constexpr int VPAD = D + 32;        // V row stride: the 4 rows of a transposing read hit distinct banks
+  constexpr int CPR = D / 8;          // 16-byte chunks per K or V row
   constexpr int KLD = BK * D / 8 / 256;        // 16-byte K (and V) loads per thread
   static_assert(KLD >= 1, "tile too small for 256 threads");
 
-  // two buffers: key tile e+1 is written while tile e is read
-  __shared__ __align__(16) u16 sKbuf[2 * BK * KPAD];
-  __shared__ __align__(16) u16 sVbuf[2 * BK * VPAD];
+  // Two buffers: key tile e+1 lands while tile e is read.  K and V rows are
+  // unpadded; chunk c of row r sits at position c ^ swz(r), which spreads
+  // both the row reads of K (16 rows, one chunk) and the transposing reads
+  // of V (4 rows x 4 chunks) over distinct banks.
+  __shared__ __align__(1024) u16 sKbuf[2 * BK * D];
+  __shared__ __align__(1024) u16 sVbuf[2 * BK * D];
   __shared__ __align__(16) int sOmbuf[2 * BK];
+  auto swz = [](int r) {
+    return D == 128 ? ((r & 3) << 2) | ((r >> 2) & 3) : (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+  };
 
   int xcd, local;
   xcd_split(xcd, local);
@@ -70,64 +75,61 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  // K and V of KV head hk through raw buffers ending at the last row's end:
-  // keys past T read as zeros (and omega 0, visible to no row), so the
-  // ragged last tile needs no clamp and no branch.
+  // K and V of KV head hk go from raw buffers straight into LDS.  Load r of
+  // wave w fills chunk positions (r * 4 + w) * 64 + lane of a tile: row
+  // P / CPR, position P % CPR, which holds chunk (P % CPR) ^ swz(row).  Keys
+  // past T read row T - 1 (their omega reads as 0, so no row sees them).
   const uint32_t kv_row = uint32_t(a.Hkv) * D * 2;   // bytes per key row
   const uint32_t kv_bytes = uint32_t(T) * kv_row - uint32_t(hk) * D * 2;
   const rsrc_t krs = make_rsrc(a.k + size_t(hk) * D, kv_bytes);
   const rsrc_t vrs = make_rsrc(a.v + size_t(hk) * D, kv_bytes);
   const rsrc_t omrs = make_rsrc(a.mask.omega, uint32_t(T) * 4);
-  uint32_t ldoff[KLD];   // byte offset of this thread's 16-byte chunks in a tile
+  int lrow[KLD];
+  uint32_t lcol[KLD];    // byte offset of the loaded chunk within its row
 #pragma unroll
   for (int r = 0; r < KLD; ++r) {
-    const int idx = tid + r * 256;
-    ldoff[r] = uint32_t(idx / (D / 8)) * kv_row + (idx % (D / 8)) * 16;
+    const int P = (r * 4 + wave) * 64 + lane;
+    lrow[r] = P / CPR;
+    lcol[r] = uint32_t((P % CPR) ^ swz(P / CPR)) * 16;
   }
-
-  uint4 kreg[KLD], vreg[KLD];
+  typedef __attribute__((address_space(3))) u16 lds_u16;
+  const uint32_t ldsK = (uint32_t)(uintptr_t)(lds_u16*)sKbuf;
+  const uint32_t ldsV = (uint32_t)(uintptr_t)(lds_u16*)sVbuf;
   int omreg = 0;
-  auto load_tile = [&](int kt) {
-    const uint32_t t0 = uint32_t(kt) * BK * kv_row;
+  auto issue_tile = [&](int kt, int buf) {
+    const uint32_t st = uint32_t(buf) * BK * D * 2 + wave * 1024;
 #pragma unroll
     for (int r = 0; r < KLD; ++r) {
-      kreg[r] = buf_ld16(krs, t0 + ldoff[r]);
-      vreg[r] = buf_ld16(vrs, t0 + ldoff[r]);
+      const uint32_t off = uint32_t(min(kt * BK + lrow[r], T - 1)) * kv_row + lcol[r];
+      buf_lds16(krs, off, ldsK + st + r * 4096);
+      buf_lds16(vrs, off, ldsV + st + r * 4096);
     }
     omreg = int(buf_ld4(omrs, uint32_t(kt * BK + tid % BK) * 4));  // every thread: key tid % BK
   };
-  auto store_tile = [&](int buf) {
-    u16* k_ = sKbuf + buf * BK * KPAD;
-    u16* v_ = sVbuf + buf * BK * VPAD;
-#pragma unroll
-    for (int r = 0; r < KLD; ++r) {
-      const int idx = tid + r * 256;
-      const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      st16(&k_[row * KPAD + col], kreg[r]);
-      st16(&v_[row * VPAD + col], vreg[r]);
-    }
-    sOmbuf[buf * BK + tid % BK] = omreg;  // identical copies
-  };
 
-  // Tile e+1 is stored into the idle buffer (read by every wave before the
-  // last barrier) and tile e+2 requested before tile e's MFMAs; one barrier
-  // per tile.  Every row tile lists at least its diagonal key tile.
-  const int e0 = a.mask.q_ptr[qt], e1 = a.mask.q_ptr[qt + 1];
-  load_tile(a.mask.k_list[e0] >> 1);
-  store_tile(0);
-  if (e0 + 1 < e1) load_tile(a.mask.k_list[e0 + 1] >> 1);
+  // Tile e+1 is in flight while tile e is read; after the barrier that ends
+  // tile e its buffer takes tile e+2.  The omega values go through registers
+  // (written once their load has landed).  One barrier per tile.  Every row
+  // tile lists at least its diagonal key tile.
+  // (block-uniform: the tile list is read with scalar loads, which do not
+  // wait behind the tile loads in flight)
+  const int e0 = __builtin_amdgcn_readfirstlane(a.mask.q_ptr[qt]);
+  const int e1 = __builtin_amdgcn_readfirstlane(a.mask.q_ptr[qt + 1]);
+  issue_tile(sload_i32(a.mask.k_list + e0) >> 1, 0);
+  wait_vmcnt<0>();
+  sOmbuf[tid % BK] = omreg;   // identical copies
+  if (e0 + 1 < e1) issue_tile(sload_i32(a.mask.k_list + e0 + 1) >> 1, 1);
   __syncthreads();
+  const int swc = swz(c);                           // K row reads: rows = c mod 16
+  const int l16 = lane & 15;
+  const int swv0 = swz(g * 4 + (l16 >> 2)), swv1 = swz(g * 4 + (l16 >> 2) + 8);
   for (int e = e0; e < e1; ++e) {
-    const int ent = a.mask.k_list[e];
+    const int ent = sload_i32(a.mask.k_list + e);
     const int kt = ent >> 1;
     const bool full = ent & 1;
     const int buf = (e - e0) & 1;
-    if (e + 1 < e1) {
-      store_tile(buf ^ 1);
-      if (e + 2 < e1) load_tile(a.mask.k_list[e + 2] >> 1);
-    }
-    const u16* sK = sKbuf + buf * BK * KPAD;
-    const u16* sV = sVbuf + buf * BK * VPAD;
+    const char* sK = reinterpret_cast<const char*>(sKbuf + buf * BK * D);
+    const char* sV = reinterpret_cast<const char*>(sVbuf + buf * BK * D);
     const int* sOm = sOmbuf + buf * BK;
     const int j0 = kt * BK;
 
@@ -141,7 +143,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
       for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
     {
       auto kfrag = [&](int st) {   // step st: block st % 2, k step st / 2
-        return as_bf16x8(ld16(&sK[((st & 1) * 32 + c) * KPAD + (st >> 1) * 16 + g * 8]));
+        return as_bf16x8(ld16(sK + ((st & 1) * 32 + c) * (D * 2) + (((st >> 1) * 2 + g) ^ swc) * 16));
       };
       bf16x8 kr[4];
 #pragma unroll
@@ -210,7 +212,20 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     {
       // V^T operand of step st: column block st % DB, keys (st / DB)*16 ..
       // in accumulator order; read four MFMAs ahead as above
-      auto vfrag = [&](int st) { return ld_operand_tr<VPAD>(sV, (st / DB) * 16, (st % DB) * 32); };
+      // (the transposing read of ld_operand_tr on the swizzled rows: lane
+      // l = lane % 16 reads 8 bytes of rows rb + g*4 + l/4 and + 8, chunk
+      // (st % DB)*4 + 2((lane/16) % 2) + (l % 4)/2, half l % 2)
+      auto vfrag = [&](int st) {
+        const int rb = (st / DB) * 16 + g * 4 + (l16 >> 2);
+        const int ch = (st % DB) * 4 + ((lane >> 4) & 1) * 2 + ((l16 & 3) >> 1);
+        const char* p0 = sV + rb * (D * 2) + ((ch ^ swv0) << 4) + (l16 & 1) * 8;
+        const char* p1 = sV + (rb + 8) * (D * 2) + ((ch ^ swv1) << 4) + (l16 & 1) * 8;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p1));
+        typedef short i16x8 __attribute__((ext_vector_type(8)));
+        const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        return __builtin_bit_cast(bf16x8, v);
+      };
       bf16x8 vr[4];
 #pragma unroll
       for (int st = 0; st < 4; ++st) vr[st] = vfrag(st);
@@ -221,7 +236,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+    // tile e+1 has landed (and its omega values are written) before the
+    // barrier that publishes it; then tile e's buffer takes tile e+2
+    wait_vmcnt<0>();
+    if (e + 1 < e1) sOmbuf[(buf ^ 1) * BK + tid % BK] = omreg;
     __syncthreads();
+    if (e + 2 < e1) issue_tile(sload_i32(a.mask.k_list + e + 2) >> 1, buf);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);

@@ -41,7 +41,17 @@ __device__ __forceinline__ void lds_load16(const void* src, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
                :
                : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
-               : "memory");
+               : "memory", "m0");
+}
+
+// A block-uniform 32-bit word read through the scalar data cache (a scalar
+// load, tracked by lgkmcnt): it does not wait behind vector loads in flight,
+// as a vector load of the same word would.  p must be uniform; the data must
+// not change during the kernel.
+__device__ __forceinline__ int sload_i32(const int* p) {
+  int v;
+  asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(p));
+  return v;
 }
 
 // s_waitcnt vmcnt(N) (the other counters left alone).
@@ -61,6 +71,17 @@ __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
+// 16 bytes per lane from a raw buffer straight into LDS: lane l's data
+// lands at LDS byte address lds + 16 l (lds uniform across the wave).  As
+// with lds_load16 the load is counted by vmcnt only; the caller waits with
+// wait_vmcnt before the barrier that publishes it.  Offsets must stay in
+// range (an out-of-range lane's LDS bytes are not relied upon).
+__device__ __forceinline__ void buf_lds16(rsrc_t r, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(off), "s"(r), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory", "m0");
 }
 __device__ __forceinline__ uint4 buf_ld16(rsrc_t r, uint32_t off) {
   const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
