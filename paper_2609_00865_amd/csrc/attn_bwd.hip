@@ -71,15 +71,12 @@ template <int D, bool IV>
 __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
   constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
   constexpr int KS = D / 16, DB = D / 32;
-  // row strides (elements): V rows are read along the rows only (d + 8 is
-  // conflict-free for that), K rows also with the transposing read (d + 24:
-  // conflict-free row reads, transposing reads at most two-way)
-  constexpr int VPAD = D + 8, KPAD = D + 24;
-  constexpr int RLD = BK * D / 8 / 256;          // row-major K and V loads per thread
 
-  // two buffers: key tile e+1 is written while tile e is read
-  __shared__ __align__(16) u16 sKbuf[2 * BK * KPAD];
-  __shared__ __align__(16) u16 sVbuf[2 * BK * VPAD];
+  // Two buffers: key tile e+1 lands while tile e is read.  K and V rows are
+  // unpadded and swizzled (kv_swz): K is read along its rows and with the
+  // transposing read, V along its rows.
+  __shared__ __align__(1024) u16 sKbuf[2 * BK * D];
+  __shared__ __align__(1024) u16 sVbuf[2 * BK * D];
   __shared__ __align__(16) int sOmbuf[2 * BK];
 
   int xcd, local;
@@ -113,63 +110,40 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
 
-  // K and V of KV head hk through raw buffers ending at the last row's end:
-  // keys past T read as zeros (omega 0: visible to no row), so the ragged
-  // last tile needs no clamp and no branch
+  // K and V of KV head hk go from raw buffers straight into LDS.  Keys past
+  // T read row T - 1 (their omega reads as 0, so no row sees them).
   const uint32_t kv_row = uint32_t(a.Hkv) * D * 2;   // bytes per key row
   const uint32_t kv_bytes = uint32_t(T) * kv_row - uint32_t(hk) * D * 2;
   const rsrc_t krs = make_rsrc(a.k + size_t(hk) * D, kv_bytes);
   const rsrc_t vrs = make_rsrc(a.v + size_t(hk) * D, kv_bytes);
   const rsrc_t omrs = make_rsrc(a.mask.omega, uint32_t(T) * 4);
-  uint32_t ldoff[RLD];   // byte offset of this thread's 16-byte chunks in a tile
-#pragma unroll
-  for (int r = 0; r < RLD; ++r) {
-    const int idx = tid + r * 256;
-    ldoff[r] = uint32_t(idx / (D / 8)) * kv_row + (idx % (D / 8)) * 16;
-  }
-  uint4 vreg[RLD], kreg[RLD];
+  const KvTileLoader<D, BK> ldr(tid);
   int omreg = 0;
-  auto load_tile = [&](int kt) {
-    const uint32_t t0 = uint32_t(kt) * BK * kv_row;
-#pragma unroll
-    for (int r = 0; r < RLD; ++r) {
-      vreg[r] = buf_ld16(vrs, t0 + ldoff[r]);
-      kreg[r] = buf_ld16(krs, t0 + ldoff[r]);
-    }
+  auto issue_tile = [&](int kt, int buf) {
+    const uint32_t st = uint32_t(buf) * BK * D * 2;
+    ldr.issue(krs, vrs, kt, T, kv_row, lds_addr(sKbuf) + st, lds_addr(sVbuf) + st);
     omreg = int(buf_ld4(omrs, uint32_t(kt * BK + tid % BK) * 4));  // every thread: key tid % BK
   };
-  auto store_tile = [&](int buf) {
-    u16* k_ = sKbuf + buf * BK * KPAD;
-    u16* v_ = sVbuf + buf * BK * VPAD;
-#pragma unroll
-    for (int r = 0; r < RLD; ++r) {
-      const int idx = tid + r * 256;
-      const int row = idx / (D / 8), col = (idx % (D / 8)) * 8;
-      st16(&v_[row * VPAD + col], vreg[r]);
-      st16(&k_[row * KPAD + col], kreg[r]);
-    }
-    sOmbuf[buf * BK + tid % BK] = omreg;  // identical copies
-  };
 
-  // Tile e+1 is stored into the idle buffer (read by every wave before the
-  // last barrier) and tile e+2 requested before tile e's MFMAs; one barrier
-  // per tile.  Every row tile lists at least its diagonal key tile.
-  const int e0 = a.mask.q_ptr[qt], e1 = a.mask.q_ptr[qt + 1];
-  load_tile(a.mask.k_list[e0] >> 1);
-  store_tile(0);
-  if (e0 + 1 < e1) load_tile(a.mask.k_list[e0 + 1] >> 1);
+  // Tile e+1 is in flight while tile e is read; after the barrier that ends
+  // tile e its buffer takes tile e+2.  The omega values go through registers
+  // (written once their load has landed).  One barrier per tile.  Every row
+  // tile lists at least its diagonal key tile; the list is read with scalar
+  // loads, which do not wait behind the tile loads in flight.
+  const int e0 = __builtin_amdgcn_readfirstlane(a.mask.q_ptr[qt]);
+  const int e1 = __builtin_amdgcn_readfirstlane(a.mask.q_ptr[qt + 1]);
+  issue_tile(sload_i32(a.mask.k_list + e0) >> 1, 0);
+  wait_vmcnt<0>();
+  sOmbuf[tid % BK] = omreg;   // identical copies
+  if (e0 + 1 < e1) issue_tile(sload_i32(a.mask.k_list + e0 + 1) >> 1, 1);
   __syncthreads();
   for (int e = e0; e < e1; ++e) {
-    const int ent = a.mask.k_list[e];
+    const int ent = sload_i32(a.mask.k_list + e);
     const int kt = ent >> 1;
     const bool full = ent & 1;
     const int buf = (e - e0) & 1;
-    if (e + 1 < e1) {
-      store_tile(buf ^ 1);
-      if (e + 2 < e1) load_tile(a.mask.k_list[e + 2] >> 1);
-    }
-    const u16* sK = sKbuf + buf * BK * KPAD;
-    const u16* sV = sVbuf + buf * BK * VPAD;
+    const char* sK = reinterpret_cast<const char*>(sKbuf + buf * BK * D);
+    const char* sV = reinterpret_cast<const char*>(sVbuf + buf * BK * D);
     const int* sOm = sOmbuf + buf * BK;
     const int j0 = kt * BK;
 
@@ -185,9 +159,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       }
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const int col = ks * 16 + g * 8, row = kb * 32 + c;
-        s = mfma32(as_bf16x8(ld16(&sK[row * KPAD + col])), qf[ks], s);
-        dp = mfma32(as_bf16x8(ld16(&sV[row * VPAD + col])), df[ks], dp);
+        s = mfma32(ld_row_swz<D>(sK, kb * 32 + c, ks * 2 + g), qf[ks], s);
+        dp = mfma32(ld_row_swz<D>(sV, kb * 32 + c, ks * 2 + g), df[ks], dp);
       }
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
@@ -213,10 +186,15 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
           // K^T operand: column block db of keys (2 kb + kk)*16.. in accumulator order
-          acc[db] = mfma32(ld_operand_tr<KPAD>(sK, (2 * kb + kk) * 16, db * 32), dsf[kk], acc[db]);
+          acc[db] = mfma32(ld_tr_swz<D>(sK, (2 * kb + kk) * 16, db * 32), dsf[kk], acc[db]);
         }
     }
+    // tile e+1 has landed (and its omega values are written) before the
+    // barrier that publishes it; then tile e's buffer takes tile e+2
+    wait_vmcnt<0>();
+    if (e + 1 < e1) sOmbuf[(buf ^ 1) * BK + tid % BK] = omreg;
     __syncthreads();
+    if (e + 2 < e1) issue_tile(sload_i32(a.mask.k_list + e + 2) >> 1, buf);
   }
 
   if (!qok) return;

@@ -31,20 +31,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
   constexpr int KS = D / 16;          // MFMA k-steps over the head dimension
   constexpr int DB = D / 32;          // 32-row blocks of O^T
-  constexpr int CPR = D / 8;          // 16-byte chunks per K or V row
-  constexpr int KLD = BK * D / 8 / 256;        // 16-byte K (and V) loads per thread
-  static_assert(KLD >= 1, "tile too small for 256 threads");
-
   // Two buffers: key tile e+1 lands while tile e is read.  K and V rows are
-  // unpadded; chunk c of row r sits at position c ^ swz(r), which spreads
-  // both the row reads of K (16 rows, one chunk) and the transposing reads
-  // of V (4 rows x 4 chunks) over distinct banks.
+  // unpadded and swizzled (kv_swz).
   __shared__ __align__(1024) u16 sKbuf[2 * BK * D];
   __shared__ __align__(1024) u16 sVbuf[2 * BK * D];
   __shared__ __align__(16) int sOmbuf[2 * BK];
-  auto swz = [](int r) {
-    return D == 128 ? ((r & 3) << 2) | ((r >> 2) & 3) : (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
-  };
 
   int xcd, local;
   xcd_split(xcd, local);
@@ -75,35 +66,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  // K and V of KV head hk go from raw buffers straight into LDS.  Load r of
-  // wave w fills chunk positions (r * 4 + w) * 64 + lane of a tile: row
-  // P / CPR, position P % CPR, which holds chunk (P % CPR) ^ swz(row).  Keys
-  // past T read row T - 1 (their omega reads as 0, so no row sees them).
+  // K and V of KV head hk go from raw buffers straight into LDS.  Keys past
+  // T read row T - 1 (their omega reads as 0, so no row sees them).
   const uint32_t kv_row = uint32_t(a.Hkv) * D * 2;   // bytes per key row
   const uint32_t kv_bytes = uint32_t(T) * kv_row - uint32_t(hk) * D * 2;
   const rsrc_t krs = make_rsrc(a.k + size_t(hk) * D, kv_bytes);
   const rsrc_t vrs = make_rsrc(a.v + size_t(hk) * D, kv_bytes);
   const rsrc_t omrs = make_rsrc(a.mask.omega, uint32_t(T) * 4);
-  int lrow[KLD];
-  uint32_t lcol[KLD];    // byte offset of the loaded chunk within its row
-#pragma unroll
-  for (int r = 0; r < KLD; ++r) {
-    const int P = (r * 4 + wave) * 64 + lane;
-    lrow[r] = P / CPR;
-    lcol[r] = uint32_t((P % CPR) ^ swz(P / CPR)) * 16;
-  }
-  typedef __attribute__((address_space(3))) u16 lds_u16;
-  const uint32_t ldsK = (uint32_t)(uintptr_t)(lds_u16*)sKbuf;
-  const uint32_t ldsV = (uint32_t)(uintptr_t)(lds_u16*)sVbuf;
+  const KvTileLoader<D, BK> ldr(tid);
   int omreg = 0;
   auto issue_tile = [&](int kt, int buf) {
-    const uint32_t st = uint32_t(buf) * BK * D * 2 + wave * 1024;
-#pragma unroll
-    for (int r = 0; r < KLD; ++r) {
-      const uint32_t off = uint32_t(min(kt * BK + lrow[r], T - 1)) * kv_row + lcol[r];
-      buf_lds16(krs, off, ldsK + st + r * 4096);
-      buf_lds16(vrs, off, ldsV + st + r * 4096);
-    }
+    const uint32_t st = uint32_t(buf) * BK * D * 2;
+    ldr.issue(krs, vrs, kt, T, kv_row, lds_addr(sKbuf) + st, lds_addr(sVbuf) + st);
     omreg = int(buf_ld4(omrs, uint32_t(kt * BK + tid % BK) * 4));  // every thread: key tid % BK
   };
 
@@ -120,9 +94,6 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   sOmbuf[tid % BK] = omreg;   // identical copies
   if (e0 + 1 < e1) issue_tile(sload_i32(a.mask.k_list + e0 + 1) >> 1, 1);
   __syncthreads();
-  const int swc = swz(c);                           // K row reads: rows = c mod 16
-  const int l16 = lane & 15;
-  const int swv0 = swz(g * 4 + (l16 >> 2)), swv1 = swz(g * 4 + (l16 >> 2) + 8);
   for (int e = e0; e < e1; ++e) {
     const int ent = sload_i32(a.mask.k_list + e);
     const int kt = ent >> 1;
@@ -143,7 +114,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
       for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
     {
       auto kfrag = [&](int st) {   // step st: block st % 2, k step st / 2
-        return as_bf16x8(ld16(sK + ((st & 1) * 32 + c) * (D * 2) + (((st >> 1) * 2 + g) ^ swc) * 16));
+        return ld_row_swz<D>(sK, (st & 1) * 32 + c, (st >> 1) * 2 + g);
       };
       bf16x8 kr[4];
 #pragma unroll
@@ -212,20 +183,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     {
       // V^T operand of step st: column block st % DB, keys (st / DB)*16 ..
       // in accumulator order; read four MFMAs ahead as above
-      // (the transposing read of ld_operand_tr on the swizzled rows: lane
-      // l = lane % 16 reads 8 bytes of rows rb + g*4 + l/4 and + 8, chunk
-      // (st % DB)*4 + 2((lane/16) % 2) + (l % 4)/2, half l % 2)
-      auto vfrag = [&](int st) {
-        const int rb = (st / DB) * 16 + g * 4 + (l16 >> 2);
-        const int ch = (st % DB) * 4 + ((lane >> 4) & 1) * 2 + ((l16 & 3) >> 1);
-        const char* p0 = sV + rb * (D * 2) + ((ch ^ swv0) << 4) + (l16 & 1) * 8;
-        const char* p1 = sV + (rb + 8) * (D * 2) + ((ch ^ swv1) << 4) + (l16 & 1) * 8;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p1));
-        typedef short i16x8 __attribute__((ext_vector_type(8)));
-        const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        return __builtin_bit_cast(bf16x8, v);
-      };
+      auto vfrag = [&](int st) { return ld_tr_swz<D>(sV, (st / DB) * 16, (st % DB) * 32); };
       bf16x8 vr[4];
 #pragma unroll
       for (int st = 0; st < 4; ++st) vr[st] = vfrag(st);

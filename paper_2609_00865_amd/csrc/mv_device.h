@@ -151,6 +151,78 @@ __device__ __forceinline__ bf16x8 ld_operand_tr(const u16* tile, int rbase, int 
   return __builtin_bit_cast(bf16x8, v);
 }
 
+// Key tiles in LDS without padding (attention forward and dQ).  A tile of
+// BK rows of D bf16 holds row r's D/8 16-byte chunks permuted: chunk c sits
+// at position c ^ kv_swz<D>(r).  The permutation spreads both the row reads
+// of an MFMA operand (16 rows, one chunk each) and the transposing reads (4
+// rows x 4 chunks) over distinct banks; it depends on r % 16 only.
+template <int D>
+__device__ __forceinline__ int kv_swz(int r) {
+  return D == 128 ? ((r & 3) << 2) | ((r >> 2) & 3) : (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+}
+
+// Row-read operand: 16 bytes (8 consecutive k) of chunk ch of row r.
+template <int D>
+__device__ __forceinline__ bf16x8 ld_row_swz(const char* tile, int r, int ch) {
+  return as_bf16x8(ld16(tile + r * (D * 2) + ((ch ^ kv_swz<D>(r)) << 4)));
+}
+
+// ld_operand_tr (accumulator k order) on a swizzled tile: lane l = lane % 16
+// reads 8 bytes of rows rbase + g*4 + l/4 and + 8 at chunk col0/8 +
+// 2((lane/16) % 2) + (l % 4)/2, half l % 2.  rbase a multiple of 16, col0 of 32.
+template <int D>
+__device__ __forceinline__ bf16x8 ld_tr_swz(const char* tile, int rbase, int col0) {
+  const int lane = threadIdx.x & 63, l = lane & 15;
+  const int r = (lane >> 5) * 4 + (l >> 2);
+  const int ch = (col0 >> 3) + ((lane >> 4) & 1) * 2 + ((l & 3) >> 1);
+  const char* p0 = tile + (rbase + r) * (D * 2) + ((ch ^ kv_swz<D>(r)) << 4) + (l & 1) * 8;
+  const char* p1 = tile + (rbase + r + 8) * (D * 2) + ((ch ^ kv_swz<D>(r + 8)) << 4) + (l & 1) * 8;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p1));
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// Loads K and V tiles of BK key rows (one KV head; rows kv_row bytes apart
+// in memory) straight into swizzled LDS tiles with 256 threads.  Load r of
+// wave w fills chunk positions P = (r * 4 + w) * 64 + lane: row P / (D/8),
+// position P % (D/8), i.e. chunk (P % (D/8)) ^ kv_swz<D>(row).  Rows past
+// the last key read the last key (the caller masks them).
+template <int D, int BK>
+struct KvTileLoader {
+  static constexpr int KLD = BK * D / 8 / 256;   // loads per thread and tensor
+  static_assert(KLD >= 1, "tile too small for 256 threads");
+  int row[KLD];
+  uint32_t col[KLD];   // byte offset of the loaded chunk within its row
+  __device__ __forceinline__ explicit KvTileLoader(int tid) {
+#pragma unroll
+    for (int r = 0; r < KLD; ++r) {
+      const int P = (r * 4 + (tid >> 6)) * 64 + (tid & 63);
+      row[r] = P / (D / 8);
+      col[r] = uint32_t((P % (D / 8)) ^ kv_swz<D>(P / (D / 8))) * 16;
+    }
+  }
+  // K and V of key tile kt into the tiles at LDS byte addresses ldsK, ldsV
+  __device__ __forceinline__ void issue(rsrc_t krs, rsrc_t vrs, int kt, int T, uint32_t kv_row,
+                                        uint32_t ldsK, uint32_t ldsV) const {
+    const uint32_t wv = uint32_t(threadIdx.x >> 6) * 1024;
+#pragma unroll
+    for (int r = 0; r < KLD; ++r) {
+      const uint32_t off = uint32_t(min(kt * BK + row[r], T - 1)) * kv_row + col[r];
+      buf_lds16(krs, off, ldsK + wv + r * 4096);
+      buf_lds16(vrs, off, ldsV + wv + r * 4096);
+    }
+  }
+};
+
+// LDS byte address of a __shared__ object
+template <typename X>
+__device__ __forceinline__ uint32_t lds_addr(X* p) {
+  typedef __attribute__((address_space(3))) X lds_x;
+  return (uint32_t)(uintptr_t)(lds_x*)p;
+}
+
 // The dispatcher deals consecutive block ids to the 8 XCDs round-robin.
 // Returns (xcd, index of the block among those of its XCD).
 __device__ __forceinline__ void xcd_split(int& xcd, int& local) {
