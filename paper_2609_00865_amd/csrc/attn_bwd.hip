@@ -220,19 +220,19 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   constexpr int KS = D / 16, DB = D / 32;
   constexpr int MB = BQ / 32;              // 32-row MFMA blocks of a row block
   constexpr int KQ = BQ / 16;              // 16-row k steps of the dV / dK products
-  // row stride d + 40: conflict-free row reads, transposing reads at most two-way
-  constexpr int RPAD = D + 40;
-  constexpr int RLD = BQ * (D / 8) / 256;  // 16-byte row loads per thread per tensor
-
-  // Q and dO blocks are staged row-major only; their transposed operands are
-  // read with the transposing LDS read (ld_operand_tr).  Three buffers: while
-  // step st accumulates dV, dK from its block, step st+1 computes S and dP
-  // from the next one and block st+2 is written.
-  constexpr int NBUF = 3;
-  __shared__ __align__(16) u16 sQbuf[NBUF * BQ * RPAD];
-  __shared__ __align__(16) u16 sdObuf[NBUF * BQ * RPAD];
-  __shared__ __align__(16) float sLbuf[NBUF * BQ];
+  // Q and dO blocks, with the rows' LSE and D, go from raw buffers straight
+  // into LDS; Q and dO rows are unpadded and swizzled (kv_swz), read along
+  // their rows and with the transposing read.  Four buffers: while step st
+  // accumulates dV, dK from its block, step st+1 computes S and dP from the
+  // next one, and blocks st+2 and st+3 are in flight (each has two steps to
+  // land).
+  constexpr int NBUF = 4;
+  __shared__ __align__(1024) u16 sQbuf[NBUF * BQ * D];
+  __shared__ __align__(1024) u16 sdObuf[NBUF * BQ * D];
+  __shared__ __align__(16) float sLbuf[NBUF * BQ];   // LSE (natural log)
   __shared__ __align__(16) float sDbuf[NBUF * BQ];
+  auto qtile = [&](int st) { return reinterpret_cast<const char*>(sQbuf + (st % NBUF) * BQ * D); };
+  auto dotile = [&](int st) { return reinterpret_cast<const char*>(sdObuf + (st % NBUF) * BQ * D); };
 
   int xcd, local;
   xcd_split(xcd, local);
@@ -270,52 +270,35 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       dv[db][r] = 0.f;
     }
 
-  // Q and dO of head hh through raw buffers ending at the last row's end:
-  // rows past T read as zeros (and LSE, D as 0), so the ragged last block
-  // needs no clamp and no branch
-  const uint32_t q_row = uint32_t(a.Hq) * D * 2;     // bytes per query row
-  uint32_t ldoff[RLD];   // byte offset of this thread's 16-byte chunks in a block
-#pragma unroll
-  for (int r = 0; r < RLD; ++r) {
-    const int idx = tid + r * 256;
-    ldoff[r] = uint32_t(idx / (D / 8)) * q_row + (idx % (D / 8)) * 16;
-  }
-  uint4 qreg[RLD], dreg[RLD];
-  float lreg = 0.f, dreg1 = 0.f;
-  auto load_block = [&](int hh, int qb) {
-    const uint32_t bytes = uint32_t(T) * q_row - uint32_t(hh) * D * 2;
-    const rsrc_t qrs = make_rsrc(a.q + size_t(hh) * D, bytes);
-    const rsrc_t drs = make_rsrc(a.dout + size_t(hh) * D, bytes);
-    const uint32_t b0 = uint32_t(qb) * BQ * q_row;
-#pragma unroll
-    for (int r = 0; r < RLD; ++r) {
-      qreg[r] = buf_ld16(qrs, b0 + ldoff[r]);
-      dreg[r] = buf_ld16(drs, b0 + ldoff[r]);
-    }
-    // every thread takes row tid % BQ's LSE and D (identical copies)
-    const uint32_t roff = uint32_t(qb * BQ + tid % BQ) * 4;
-    lreg = __builtin_bit_cast(float, buf_ld4(make_rsrc(a.lse + size_t(hh) * T, uint32_t(T) * 4), roff));
-    dreg1 = __builtin_bit_cast(float, buf_ld4(make_rsrc(a.Dd + size_t(hh) * T, uint32_t(T) * 4), roff));
-  };
-  auto store_block = [&](int buf) {
-    u16* q_ = sQbuf + buf * BQ * RPAD;
-    u16* d_ = sdObuf + buf * BQ * RPAD;
-#pragma unroll
-    for (int r = 0; r < RLD; ++r) {
-      const int idx = tid + r * 256;
-      const int row = idx / (D / 8), cc = idx % (D / 8);
-      st16(&q_[row * RPAD + cc * 8], qreg[r]);
-      st16(&d_[row * RPAD + cc * 8], dreg[r]);
-    }
-    sLbuf[buf * BQ + tid % BQ] = lreg * kLog2e;
-    sDbuf[buf * BQ + tid % BQ] = dreg1;
-  };
-
   const int nqb = qb1 - qb0;
   const int steps = nqb * G;
   const int h0 = hk * G;
-  // step st covers query block qb0 + st % nqb of head h0 + st / nqb
-  auto load_step = [&](int st) { load_block(h0 + st / nqb, qb0 + st % nqb); };
+  // Step st covers query block qb0 + st % nqb of head h0 + st / nqb.  Rows
+  // past T read row T - 1 (finite values; no key is visible to them).  Every
+  // wave issues the same number of loads per step (LPS): its share of Q and
+  // dO, and the block's LSE (even waves) or D (odd waves; the second pair of
+  // waves writes the same words again).
+  const uint32_t q_row = uint32_t(a.Hq) * D * 2;     // bytes per query row
+  const KvTileLoader<D, BQ> ldr(tid);
+  constexpr int LPS = 2 * KvTileLoader<D, BQ>::KLD + 1;
+  static_assert(BQ == 64, "one LSE / D word per lane");
+  auto issue_step = [&](int st) {
+    const int hh = h0 + st / nqb, qb = qb0 + st % nqb, buf = st % NBUF;
+    const uint32_t bytes = uint32_t(T) * q_row - uint32_t(hh) * D * 2;
+    ldr.issue(make_rsrc(a.q + size_t(hh) * D, bytes), make_rsrc(a.dout + size_t(hh) * D, bytes), qb,
+              T, q_row, lds_addr(sQbuf) + buf * BQ * D * 2, lds_addr(sdObuf) + buf * BQ * D * 2);
+    const bool odd = __builtin_amdgcn_readfirstlane(wave) & 1;   // wave-uniform
+    const float* vec = (odd ? a.Dd : a.lse) + size_t(hh) * T;
+    buf_lds4(make_rsrc(vec, uint32_t(T) * 4), uint32_t(min(qb * BQ + lane, T - 1)) * 4,
+             (odd ? lds_addr(sDbuf) : lds_addr(sLbuf)) + buf * BQ * 4);
+  };
+  // before the barrier that ends step st: block st+2 landed (st+3 may fly)
+  auto wait_step = [&](int st) {
+    if (st + 3 < steps)
+      wait_vmcnt<LPS>();
+    else
+      wait_vmcnt<0>();
+  };
 
   // The work of a step runs in two halves (unit 2 st + mb: the block's
   // query rows mb*32 ..): S = Q K^T and dP = dO V^T of the half (rows: its
@@ -323,9 +306,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   // its share of dV^T += dO^T P and dK^T += Q^T dS.
   f32x16 s, dp;
   auto scores_mfma = [&](int st, int mb) {
-    const int buf = st % NBUF;
-    const u16* sQ = sQbuf + buf * BQ * RPAD;
-    const u16* sdO = sdObuf + buf * BQ * RPAD;
+    const char* sQ = qtile(st);
+    const char* sdO = dotile(st);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       s[r] = 0.f;
@@ -333,9 +315,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     }
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const int off = (mb * 32 + c) * RPAD + ks * 16 + g * 8;
-      s = mfma32(as_bf16x8(ld16(&sQ[off])), kf[ks], s);
-      dp = mfma32(as_bf16x8(ld16(&sdO[off])), vf[ks], dp);
+      s = mfma32(ld_row_swz<D>(sQ, mb * 32 + c, ks * 2 + g), kf[ks], s);
+      dp = mfma32(ld_row_swz<D>(sdO, mb * 32 + c, ks * 2 + g), vf[ks], dp);
     }
   };
   // rows of s/dp are queries mb*32 + q4*8 + g*4 + u of the block
@@ -354,7 +335,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       const int qo = mb * 32 + q4 * 8 + g * 4;
       const float4 l4 = *reinterpret_cast<const float4*>(&sL[qo]);
       const float4 d4 = *reinterpret_cast<const float4*>(&sD[qo]);
-      const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dd[4] = {d4.x, d4.y, d4.z, d4.w};
+      const float lv[4] = {l4.x * kLog2e, l4.y * kLog2e, l4.z * kLog2e, l4.w * kLog2e};
+      const float dd[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int r = q4 * 4 + u;
@@ -374,16 +356,15 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     dsf[1] = to_operand(dp, 8);
   };
   auto accumulate = [&](int st, int mb, const bf16x8 (&pf)[2], const bf16x8 (&dsf)[2]) {
-    const int buf = st % NBUF;
-    const u16* sQ = sQbuf + buf * BQ * RPAD;
-    const u16* sdO = sdObuf + buf * BQ * RPAD;
+    const char* sQ = qtile(st);
+    const char* sdO = dotile(st);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         // dO^T and Q^T operands: columns db*32.. of rows (2 mb + kk)*16.. in accumulator order
-        dv[db] = mfma32(ld_operand_tr<RPAD>(sdO, (2 * mb + kk) * 16, db * 32), pf[kk], dv[db]);
-        dk[db] = mfma32(ld_operand_tr<RPAD>(sQ, (2 * mb + kk) * 16, db * 32), dsf[kk], dk[db]);
+        dv[db] = mfma32(ld_tr_swz<D>(sdO, (2 * mb + kk) * 16, db * 32), pf[kk], dv[db]);
+        dk[db] = mfma32(ld_tr_swz<D>(sQ, (2 * mb + kk) * 16, db * 32), dsf[kk], dk[db]);
       }
   };
 
@@ -411,7 +392,10 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       const int qo = mb * 32 + q4 * 8 + g * 4;
       const float4 l4 = *reinterpret_cast<const float4*>(&sL[qo]);
       const float4 d4 = *reinterpret_cast<const float4*>(&sD[qo]);
-      lv[q4 * 4 + 0] = l4.x; lv[q4 * 4 + 1] = l4.y; lv[q4 * 4 + 2] = l4.z; lv[q4 * 4 + 3] = l4.w;
+      lv[q4 * 4 + 0] = l4.x * kLog2e;
+      lv[q4 * 4 + 1] = l4.y * kLog2e;
+      lv[q4 * 4 + 2] = l4.z * kLog2e;
+      lv[q4 * 4 + 3] = l4.w * kLog2e;
       dd[q4 * 4 + 0] = d4.x; dd[q4 * 4 + 1] = d4.y; dd[q4 * 4 + 2] = d4.z; dd[q4 * 4 + 3] = d4.w;
     }
   };
@@ -426,11 +410,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   // set par ^ 1 (if NEXT) with elements 8..15 of this unit, then its operands
   auto phaseX = [&](auto next_tag, int par, int st, int mb, bf16x8 (&pfo)[2], bf16x8 (&dso)[2]) {
     constexpr bool NEXT = decltype(next_tag)::value;
-    const u16* sQ = sQbuf + (st % NBUF) * BQ * RPAD;
-    const u16* sdO = sdObuf + (st % NBUF) * BQ * RPAD;
+    const char* sQ = qtile(st);
+    const char* sdO = dotile(st);
     const int np = par ^ 1;
     auto opnd = [&](int j) {   // MFMA j: ks = j / 2, S (even) or dP (odd)
-      return as_bf16x8(ld16(&((j & 1) ? sdO : sQ)[(mb * 32 + c) * RPAD + (j >> 1) * 16 + g * 8]));
+      return ld_row_swz<D>((j & 1) ? sdO : sQ, mb * 32 + c, (j >> 1) * 2 + g);
     };
     bf16x8 op[3];
     if constexpr (NEXT) {
@@ -468,11 +452,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
                     int np, int st2, int mb2) {
     constexpr bool NEXT = decltype(next_tag)::value;
     if constexpr (NEXT) load_ctx(st2, mb2);
-    const u16* sQ = sQbuf + (st % NBUF) * BQ * RPAD;
-    const u16* sdO = sdObuf + (st % NBUF) * BQ * RPAD;
+    const char* sQ = qtile(st);
+    const char* sdO = dotile(st);
     // MFMA q: db = q / 4, kk = (q / 2) % 2, dV (even q) or dK (odd q)
     auto opnd = [&](int q) {
-      return ld_operand_tr<RPAD>((q & 1) ? sQ : sdO, (2 * mb + ((q >> 1) & 1)) * 16, (q >> 2) * 32);
+      return ld_tr_swz<D>((q & 1) ? sQ : sdO, (2 * mb + ((q >> 1) & 1)) * 16, (q >> 2) * 32);
     };
     constexpr int NQ = 4 * DB;
     bf16x8 op[3];
@@ -500,32 +484,27 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
 
   // Software pipeline over half-step units, one barrier per step: the next
   // unit's S and dP MFMAs are issued before this unit's dV and dK MFMAs, and
-  // the next unit's exponentials follow them.  Block st+2 is written into the
-  // buffer step st-1 used (every wave finished with it before the last
-  // barrier) and block st+3 is requested from HBM.
-  load_step(0);
-  store_block(0);
-  if (steps > 1) {
-    load_step(1);
-    store_block(1);
-  }
-  if (steps > 2) load_step(2);
+  // the next unit's exponentials follow them.  Block st+3 is requested into
+  // the buffer step st-1 used (every wave finished with it before the last
+  // barrier).
+  issue_step(0);
+  if (steps > 1) issue_step(1);
+  if (steps > 2) issue_step(2);
+  wait_step(-1);   // blocks 0 and 1 landed
   __syncthreads();
   bf16x8 pf[2], dsf[2];
   if constexpr (IV) {
     scores_mfma(0, 0);
     scores_valu(0, 0, pf, dsf);
     for (int st = 0; st + 1 < steps; ++st) {
-      if (st + 2 < steps) {
-        store_block((st + 2) % NBUF);
-        if (st + 3 < steps) load_step(st + 3);
-      }
+      if (st + 3 < steps) issue_step(st + 3);
       scores_mfma(st, 1);
       accumulate(st, 0, pf, dsf);
       scores_valu(st, 1, pf, dsf);
       scores_mfma(st + 1, 0);
       accumulate(st, 1, pf, dsf);
       scores_valu(st + 1, 0, pf, dsf);
+      wait_step(st);
       __syncthreads();
     }
     scores_mfma(steps - 1, 1);
@@ -544,21 +523,18 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     }
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const int off = c * RPAD + ks * 16 + g * 8;
-      sc[0] = mfma32(as_bf16x8(ld16(&sQbuf[off])), kf[ks], sc[0]);
-      dc[0] = mfma32(as_bf16x8(ld16(&sdObuf[off])), vf[ks], dc[0]);
+      sc[0] = mfma32(ld_row_swz<D>(qtile(0), c, ks * 2 + g), kf[ks], sc[0]);
+      dc[0] = mfma32(ld_row_swz<D>(dotile(0), c, ks * 2 + g), vf[ks], dc[0]);
     }
 #pragma unroll
     for (int r = 0; r < 8; ++r) elem(0, r);
     for (int st = 0; st + 1 < steps; ++st) {
-      if (st + 2 < steps) {
-        store_block((st + 2) % NBUF);
-        if (st + 3 < steps) load_step(st + 3);
-      }
+      if (st + 3 < steps) issue_step(st + 3);
       phaseX(yes{}, 0, st, 1, pf, dsf);          // S/dP of (st, 1); finish (st, 0)
       phaseY(yes{}, st, 0, pf, dsf, 1, st, 1);   // dV/dK of (st, 0); start (st, 1)
       phaseX(yes{}, 1, st + 1, 0, pf, dsf);      // S/dP of (st+1, 0); finish (st, 1)
       phaseY(yes{}, st, 1, pf, dsf, 0, st + 1, 0);
+      wait_step(st);
       __syncthreads();
     }
     const int st = steps - 1;

@@ -83,6 +83,13 @@ __device__ __forceinline__ void buf_lds16(rsrc_t r, uint32_t off, uint32_t lds) 
                : "v"(off), "s"(r), "s"(__builtin_amdgcn_readfirstlane(lds))
                : "memory", "m0");
 }
+// 4 bytes per lane from a raw buffer straight into LDS (lane l at lds + 4 l).
+__device__ __forceinline__ void buf_lds4(rsrc_t r, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dword %0, %1, 0 offen lds"
+               :
+               : "v"(off), "s"(r), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory", "m0");
+}
 __device__ __forceinline__ uint4 buf_ld16(rsrc_t r, uint32_t off) {
   const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
   return make_uint4(v[0], v[1], v[2], v[3]);
