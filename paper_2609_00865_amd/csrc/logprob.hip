@@ -269,20 +269,26 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
       if (lane < 16 && t < a.T) a.part[size_t(t) * a.n_chunks + chunk] = make_float2(m2, s);
     }
   } else if (MODE == kModeGrad) {
-    // -g_t softmax(z_t)_v everywhere (zero in the vocabulary padding); the
-    // target entry gets its one-hot term from lm_target_kernel afterwards
+    // -g_t softmax(z_t)_v everywhere (zero in the vocabulary padding; rows
+    // T .. Tg - 1, which pad the dW product's k, are zeros too); the target
+    // entry gets its one-hot term from lm_target_kernel afterwards.  The
+    // tile's block of G is one contiguous 128 KiB run of four panels: it is
+    // assembled in LDS in that order (the 16-byte chunks of each 128-byte
+    // row permuted by the row's low bits, against bank conflicts) and written
+    // with 16-byte stores that cover whole lines.
+    char* sg = reinterpret_cast<char*>(smem);
+    __syncthreads();   // every wave has read its last operand fragments
 #pragma unroll
     for (int j = 0; j < FB; ++j) {
       const int t = tb + j * 16;
-      if (t >= a.Tg) continue;
-      // rows T .. Tg - 1 are written as zeros (they pad the dW product's k)
+      const int tl = t - t0;                       // row within the tile's panels
       const int tc = min(t, a.T - 1);
       const int y = a.tgt[tc];
       const float ng = (y >= 0 && t < a.T) ? -a.g[tc] : 0.f;
       const float l2 = a.lse[tc] * kLog2e;
 #pragma unroll
       for (int i = 0; i < FA; ++i) {
-        u16* out = a.Gout + panel_index(t, rb + i * 16, a.Vp);   // 4 consecutive entries
+        const int vl = rb + i * 16 - a0;             // 4 consecutive entries vl ..
         float vals[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -292,8 +298,17 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
         uint2 wv;
         wv.x = pack2(vals[0], vals[1]);
         wv.y = pack2(vals[2], vals[3]);
-        *reinterpret_cast<uint2*>(out) = wv;
+        const int c = vl & 63;
+        *reinterpret_cast<uint2*>(sg + (vl >> 6) * 32768 + tl * 128 +
+                                  ((((c >> 3) ^ (tl & 7)) << 4) | ((c & 7) * 2))) = wv;
       }
+    }
+    __syncthreads();
+    uint4* gt = reinterpret_cast<uint4*>(a.Gout + panel_index(t0, a0, a.Vp));
+#pragma unroll 4
+    for (int k = tid; k < 128 * 1024 / 16; k += NWAVES * 64) {
+      const int q = k >> 11, r = (k >> 3) & 255, c16 = k & 7;
+      gt[k] = *reinterpret_cast<const uint4*>(sg + (q << 15) + (r << 7) + ((c16 ^ (r & 7)) << 4));
     }
   } else if (MODE == kModeKL) {
     // lanes c (even, teacher) and c ^ 1 (student) hold the same vocabulary
