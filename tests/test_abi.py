@@ -63,6 +63,19 @@ def test_attention_argument_errors():
     assert "uploaded" in mv.mv_last_error().decode()
 
 
+def test_attention_tensor_size_limit():
+    """The kernels address each tensor with 32-bit byte offsets: a Q of 4 GiB
+    or more is refused (262144 tokens x 64 heads x 128 x 2 B = 2^32 B)."""
+    big = mv.ViewMask([synth.Trajectory(0, 262144, ())])
+    fwd = lambda sh: _status(mv.mv_attn_fwd(big.handle, ctypes.byref(sh), *([FAKE] * 5), None))
+    assert fwd(_shape(T=262144, hq=64, hkv=8, d=128)) == "MV_ERR_UNSUPPORTED"
+    assert "4 GiB" in mv.mv_last_error().decode()
+    # one token fewer fits: the request gets as far as the upload check
+    small = mv.ViewMask([synth.Trajectory(0, 262143, ())])
+    sh = _shape(T=262143, hq=64, hkv=8, d=128)
+    assert _status(mv.mv_attn_fwd(small.handle, ctypes.byref(sh), *([FAKE] * 5), None)) == "MV_ERR_STATE"
+
+
 def test_backward_workspace_errors():
     m = _mask()
     sh = _shape()
