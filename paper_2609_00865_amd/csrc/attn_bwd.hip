@@ -43,25 +43,32 @@ struct BwdArgs {
 // ---------------------------------------------------------------------------
 // 1. D = rowsum(dO * O)
 // ---------------------------------------------------------------------------
+// D/8 consecutive lanes share one (row, head) vector, 16 bytes each, so a
+// wave reads whole contiguous rows; the partial dot products are summed
+// across those lanes.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
+  constexpr int LPV = D / 8;   // lanes per vector
   const int64_t gid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (gid >= int64_t(a.T) * a.Hq) return;
-  const int i = int(gid / a.Hq), h = int(gid % a.Hq);
-  const u16* op = a.o + size_t(gid) * D;
-  const u16* dp = a.dout + size_t(gid) * D;
+  const int64_t vec = gid / LPV;   // row * Hq + head
+  const bool ok = vec < int64_t(a.T) * a.Hq;
   float acc = 0.f;
-#pragma unroll
-  for (int c = 0; c < D / 8; ++c) {
-    const uint4 x = ld16(op + c * 8), y = ld16(dp + c * 8);
+  if (ok) {
+    const size_t off = size_t(gid) * 8;   // = vec * D + (gid % LPV) * 8
+    const uint4 x = ld16(a.o + off), y = ld16(a.dout + off);
     const uint32_t xs[4] = {x.x, x.y, x.z, x.w}, ys[4] = {y.x, y.y, y.z, y.w};
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      acc += bf16_to_f32(xs[w] & 0xffff) * bf16_to_f32(ys[w] & 0xffff);
-      acc += bf16_to_f32(xs[w] >> 16) * bf16_to_f32(ys[w] >> 16);
+      acc = fmaf(bf16_to_f32(xs[w] & 0xffff), bf16_to_f32(ys[w] & 0xffff), acc);
+      acc = fmaf(bf16_to_f32(xs[w] >> 16), bf16_to_f32(ys[w] >> 16), acc);
     }
   }
-  a.Dd[size_t(h) * a.T + i] = acc;
+#pragma unroll
+  for (int m = LPV / 2; m > 0; m >>= 1) acc += __shfl_xor(acc, m);
+  if (ok && gid % LPV == 0) {
+    const int i = int(vec / a.Hq), h = int(vec % a.Hq);
+    a.Dd[size_t(h) * a.T + i] = acc;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -594,11 +601,27 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(BwdArgs a, int n_red) {
     const int kk = rem / (D / 4), d0 = (rem % (D / 4)) * 4;
     const int key = kt * BK + kk;
     if (key >= a.T) continue;
+    // partials summed in slot order (the result does not depend on
+    // scheduling); four loads in flight
+    const size_t stride = size_t(a.Hkv) * 2 * BK * D;   // floats from one slot to the next
+    const float* p = a.partial + ((size_t(first) * a.Hkv + hk) * 2 + which) * BK * D +
+                     size_t(kk) * D + d0;
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int i = 0; i < n; ++i) {
-      const float* p = a.partial + ((size_t(first + i) * a.Hkv + hk) * 2 + which) * BK * D +
-                       size_t(kk) * D + d0;
-      const float4 x = *reinterpret_cast<const float4*>(p);
+    int i = 0;
+    for (; i + 4 <= n; i += 4) {
+      float4 x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) x[u] = *reinterpret_cast<const float4*>(p + (i + u) * stride);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        s.x += x[u].x;
+        s.y += x[u].y;
+        s.z += x[u].z;
+        s.w += x[u].w;
+      }
+    }
+    for (; i < n; ++i) {
+      const float4 x = *reinterpret_cast<const float4*>(p + i * stride);
       s.x += x.x;
       s.y += x.y;
       s.z += x.z;
@@ -646,7 +669,7 @@ hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float 
 
   const int64_t rows = int64_t(m.T) * Hq;
   const dim3 b256(256);
-  const dim3 g_pre(unsigned((rows + 255) / 256));
+  const dim3 g_pre(unsigned((rows * (D / 8) + 255) / 256));
   const int per_xcd_q = (m.n_qt + kNumXcd - 1) / kNumXcd;
   const dim3 g_dq(per_xcd_q * Hq * kNumXcd);
   const int per_xcd_kv = (a.n_items + kNumXcd - 1) / kNumXcd;
