@@ -37,7 +37,10 @@ namespace mv {
 namespace {
 constexpr int BA = 256, BT = 256, BKK = 64;
 constexpr int NWAVES = 8;                  // waves per tile (2 x 4 grid)
-constexpr int GROUP_T = 4;                 // token tiles per raster group
+// token tiles per raster group: 8 x 4 A tiles run side by side on an XCD
+// for the products over the hidden dimension (measured ~1% faster than
+// 4 x 8), 4 x 8 for dH and dW
+constexpr int GROUP_T_H = 8, GROUP_T_V = 4;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
 // tile engine
@@ -98,7 +101,8 @@ struct LmArgs {
 
 // Output tile (a0, t0) and k split of this block.  Blocks are dealt to XCDs
 // round-robin; each XCD gets a contiguous range of the rasterised tile order
-// (groups of GROUP_T token tiles x all A tiles).  False: no tile (grid tail).
+// (groups of GT token tiles x all A tiles).  False: no tile (grid tail).
+template <int GT>
 __device__ __forceinline__ bool tile_of(const LmArgs& a, int n_splits, int& a0, int& t0,
                                         int& split) {
   const int n_out = a.nA * a.nT;
@@ -110,11 +114,11 @@ __device__ __forceinline__ bool tile_of(const LmArgs& a, int n_splits, int& a0, 
   if (local >= per_xcd || Lx >= n_tiles) return false;
   split = Lx / n_out;
   const int L = Lx % n_out;
-  const int grp = L / (GROUP_T * a.nA);
-  const int rem = L % (GROUP_T * a.nA);
-  const int t_in = min(GROUP_T, a.nT - grp * GROUP_T);
+  const int grp = L / (GT * a.nA);
+  const int rem = L % (GT * a.nA);
+  const int t_in = min(GT, a.nT - grp * GT);
   a0 = (rem / t_in) * BA;
-  t0 = (grp * GROUP_T + rem % t_in) * BT;
+  t0 = (grp * GT + rem % t_in) * BT;
   return true;
 }
 
@@ -123,7 +127,8 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
   __shared__ __align__(1024) u16 smem[2 * 2 * SLICE_B / 2];   // 2 slices x 2 operands
 
   int a0, t0, split;
-  if (!tile_of(a, MODE == kModeDh ? a.k_split : 1, a0, t0, split)) return;
+  constexpr int GT = MODE == kModeDh ? GROUP_T_V : GROUP_T_H;
+  if (!tile_of<GT>(a, MODE == kModeDh ? a.k_split : 1, a0, t0, split)) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wa = wave >> 2, wt = wave & 3;
@@ -428,7 +433,7 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_dw_kernel(LmArgs a) {
   __shared__ __align__(1024) u16 smem[2 * 2 * SLICE_B / 2];   // 2 slices x (G, H)
 
   int a0, t0, split;
-  if (!tile_of(a, 1, a0, t0, split)) return;
+  if (!tile_of<GROUP_T_V>(a, 1, a0, t0, split)) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 31, g = lane >> 5;
