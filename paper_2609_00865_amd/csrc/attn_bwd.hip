@@ -225,8 +225,6 @@ template <int D, bool IV>
 __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   constexpr int BK = kBwdTileK, BQ = kBwdBlockQ;
   constexpr int KS = D / 16, DB = D / 32;
-  constexpr int MB = BQ / 32;              // 32-row MFMA blocks of a row block
-  constexpr int KQ = BQ / 16;              // 16-row k steps of the dV / dK products
   // Q and dO blocks, with the rows' LSE and D, go from raw buffers straight
   // into LDS; Q and dO rows are unpadded and swizzled (kv_swz), read along
   // their rows and with the transposing read.  Four buffers: while step st
