@@ -6,10 +6,12 @@
 // on the accumulator rows, one query per lane, so the softmax statistics of a
 // row stay inside a lane pair), applies the shared visibility predicate on
 // partial tiles only, updates the online softmax in base 2, and accumulates
-// O^T += V^T P^T with a second MFMA.  K and V are staged row-major in LDS; the
-// V^T operand is read with the transposing LDS read.  The next tile's global
-// loads are in flight during the current tile's math.  Query tiles are visited heaviest first and the heads of one query
-// tile are kept on one XCD so that GQA heads share K/V in that XCD's L2.
+// O^T += V^T P^T with a second MFMA.  K and V go from buffer loads straight
+// into LDS as unpadded rows with permuted 16-byte chunks (kv_swz); the V^T
+// operand is read with the transposing LDS read.  The next tile's loads are
+// in flight during the current tile's math.  Query tiles are visited
+// heaviest first and the heads of one query tile are kept on one XCD so that
+// GQA heads share K/V in that XCD's L2.
 #include "mv_device.h"
 #include "mv_predicate.h"
 
