@@ -100,6 +100,19 @@ def test_full_size_sampled():
     assert_bf16_close(dh.cpu()[idx], ref_dh, "lmhead dH")
 
 
+@pytest.mark.parametrize("T,H,V", [(300, 256, 1000), (2000, 512, 3000)])
+def test_repeat_is_bit_identical(T, H, V):
+    """Fixed-order reductions throughout (per-chunk partials merged in chunk
+    order, the split dH summed in split order, no atomics): a second forward
+    and backward reproduce every bit.  Both shapes split dH over the
+    vocabulary and have ragged token and vocabulary tiles."""
+    h, w, y, old, g = _inputs(T, H, V, 9, skip_every=11)
+    first = _gpu(h, w, y, old, g)
+    second = _gpu(h, w, y, old, g)
+    for a, b in zip(first, second):
+        assert torch.equal(a, b)
+
+
 @pytest.mark.parametrize("T,H,V", [(300, 256, 1000), (257, 192, 600), (64, 128, 256),
                                    (1, 64, 17)])
 def test_dweight_small_ragged(T, H, V):
