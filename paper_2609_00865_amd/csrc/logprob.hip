@@ -464,7 +464,7 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_dw_kernel(LmArgs a) {
     }
   };
 
-  // transposing operand read (k order of ld_operand_tr<., true>): lane l of a
+  // transposing operand read in natural k order (rows g*8 + 0..7): lane l of a
   // 16-lane group reads token rows rb + (lane/32)*8 + l/4 and + 4, columns
   // col0 + ((lane/16) % 2)*16 + 4 (l % 4); with rb a multiple of 16 and col0 a
   // multiple of 32 the swizzle term of a lane is fixed

@@ -134,32 +134,6 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-// MFMA operand read *across* the rows of a row-major bf16 LDS tile (stride PAD
-// elements), using gfx950's transposing LDS read: within each group of 16
-// lanes, lane i receives element i % 4 of the 8-byte chunks addressed by lanes
-// 4k + i / 4 (k = 0..3).  Lane l = lane % 16 therefore addresses row
-// rbase + g*4 + l/4, columns col0 + 16*((lane/16) % 2) + 4*(l % 4) .. +4, and
-// lane (c = lane % 32, g = lane / 32) receives column col0 + c of rows
-// rbase + g*4 + {0,1,2,3} and rbase + 8 + g*4 + {0,1,2,3}: the k order of an
-// MFMA accumulator's rows (see mfma32), so the result pairs with an operand
-// taken straight from an accumulator.
-// With NATURAL = true the 8 rows are rbase + g*8 + {0..7} instead, the k order
-// of an operand read from a row-major tile along its rows.
-template <int PAD, bool NATURAL = false>
-__device__ __forceinline__ bf16x8 ld_operand_tr(const u16* tile, int rbase, int col0) {
-  const int lane = threadIdx.x & 63;
-  const int l = lane & 15;
-  const int row = rbase + (lane >> 5) * (NATURAL ? 8 : 4) + (l >> 2);
-  const int col = col0 + ((lane >> 4) & 1) * 16 + 4 * (l & 3);
-  const u16* p0 = tile + row * PAD + col;
-  const u16* p1 = p0 + (NATURAL ? 4 : 8) * PAD;
-  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0));
-  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p1));
-  typedef short i16x8 __attribute__((ext_vector_type(8)));
-  const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-  return __builtin_bit_cast(bf16x8, v);
-}
-
 // Key tiles in LDS without padding (attention forward and dQ).  A tile of
 // BK rows of D bf16 holds row r's D/8 16-byte chunks permuted: chunk c sits
 // at position c ^ kv_swz<D>(r).  The permutation spreads both the row reads
@@ -176,9 +150,16 @@ __device__ __forceinline__ bf16x8 ld_row_swz(const char* tile, int r, int ch) {
   return as_bf16x8(ld16(tile + r * (D * 2) + ((ch ^ kv_swz<D>(r)) << 4)));
 }
 
-// ld_operand_tr (accumulator k order) on a swizzled tile: lane l = lane % 16
-// reads 8 bytes of rows rbase + g*4 + l/4 and + 8 at chunk col0/8 +
-// 2((lane/16) % 2) + (l % 4)/2, half l % 2.  rbase a multiple of 16, col0 of 32.
+// MFMA operand read *across* the rows of a swizzled tile, with gfx950's
+// transposing LDS read: within each group of 16 lanes, lane i receives
+// element i % 4 of the 8-byte pieces addressed by lanes 4k + i / 4 (k = 0..3).
+// Lane l = lane % 16 addresses rows rbase + g*4 + l/4 and + 8, columns
+// col0 + 16((lane/16) % 2) + 4(l % 4) .. +4 (chunk col0/8 + 2((lane/16) % 2) +
+// (l % 4)/2, half l % 2), so lane (c = lane % 32, g = lane / 32) receives
+// column col0 + c of rows rbase + g*4 + {0,1,2,3} and rbase + 8 + g*4 +
+// {0,1,2,3}: the k order of an MFMA accumulator's rows (see mfma32), so the
+// result pairs with an operand taken straight from an accumulator.  rbase a
+// multiple of 16, col0 of 32.
 template <int D>
 __device__ __forceinline__ bf16x8 ld_tr_swz(const char* tile, int rbase, int col0) {
   const int lane = threadIdx.x & 63, l = lane & 15;
