@@ -9,10 +9,18 @@ One step = the whole path over one batch of synthetic input:
 The eviction records are turned into the mask on the host before the timed
 region (the mask is an input, like the tensors); its build time is reported.
 
-Printed JSON (one line): useful TFLOP/s of the whole step (attention useful
-FLOPs 14 d P Hq with P the visible (row, key) pairs, plus LM-head 6 T H V),
-per-part breakdowns, the roofline of the dominant kernel measured with HIP
-events on the launch stream, and the CPU oracle's rate on a bounded sample.
+Printed JSON (one line).  `value` is the metric itself: useful TFLOP/s of the
+view-masked attention forward + backward of the 32K-token trajectories
+(14 d P Hq FLOPs, P the visible (row, key) pairs), timed with events around
+the attention part of every step; `tokens_per_s` is trajectory tokens over the
+same attention time.  `ms_per_step` covers the whole step (attention and LM
+head); the LM head and the step blend are sub-objects.  After the step, the
+attention alone is timed on the other trajectory shapes (the second seed of the
+4 x 32K batch, the 131072-token trajectory with 64/8 heads for both seeds, the
+8192-token trajectory), and the SDCC pass, the LM-head weight gradient and the
+branch-replicated layer on their own.  The roofline object covers the step's
+longest kernel; `roofline_attention` the attention's longest kernel, with its
+useful FLOPs.  The CPU oracle is timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -50,22 +58,31 @@ def parse():
                     help="skip the separately timed SDCC junction-KL pass")
     ap.add_argument("--no-packed", action="store_true",
                     help="skip the separately timed branch-replicated attention layer")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the attention timings on the other trajectory shapes")
     return ap.parse_args()
 
 
-def kernel_flops(P, d, hq, T_lm, H, V, n_leaves=0):
-    """Algorithmic FLOPs of one launch of each kernel."""
+def attn_kernel_flops(st, d, hq):
+    """Useful and executed FLOPs of one launch of each attention kernel.
+
+    Useful: the backward's five products over the visible pairs P (S
+    recomputed once, dP, dV, dK, dQ) split as the kernels split them: dK/dV
+    holds S, dP, dV and dK (8 d P Hq), dQ only its own product (2 d P Hq; its
+    S and dP are recomputations beyond the five).  Executed: every product a
+    kernel runs over the (row, key) pairs of the tiles it visits."""
+    P = st["visible_pairs"]
+    fp, bp = st["fwd_tile_pairs"], st["bwd_tile_pairs"]
     return {
-        "kl_logits": 4.0 * n_leaves * H * V,  # teacher and student logits of every leaf
-        "kl_grad": 4.0 * n_leaves * H * V,    # both recomputed for q - p
-        "kl_dh": 2.0 * n_leaves * H * V,      # (q - p) W into the student rows
-        "attn_fwd": 4.0 * d * P * hq,         # S = Q K^T and O = P V over visible pairs
-        "attn_bwd_dkdv": 8.0 * d * P * hq,    # S, dP recomputed; dV = P^T dO, dK = dS^T Q
-        "attn_bwd_dq": 6.0 * d * P * hq,      # S, dP recomputed; dQ = dS K
-        "lm_logits": 2.0 * T_lm * H * V,
-        "lm_grad": 2.0 * T_lm * H * V,
-        "lm_dh": 2.0 * T_lm * H * V,
+        "attn_fwd": {"useful": 4.0 * d * P * hq, "executed": 4.0 * d * fp * hq},
+        "attn_bwd_dkdv": {"useful": 8.0 * d * P * hq, "executed": 8.0 * d * bp * hq},
+        "attn_bwd_dq": {"useful": 2.0 * d * P * hq, "executed": 6.0 * d * fp * hq},
     }
+
+
+def lm_kernel_flops(T_lm, H, V):
+    """Algorithmic FLOPs of one launch of each LM-head product."""
+    return {n: 2.0 * T_lm * H * V for n in ("lm_logits", "lm_grad", "lm_dh")}
 
 
 def measured_traffic(kernel):
@@ -132,14 +149,17 @@ def cpu_baseline(trajs, wl, lmw, attn_flops_step, lm_flops_step):
     log(f"cpu oracle lm-head sample: {l_s:.2f}s, {lm_rate / 1e9:.1f} GFLOP/s")
     step_s = attn_flops_step / attn_rate + lm_flops_step / lm_rate
     return {
-        "value": (attn_flops_step + lm_flops_step) / step_s / 1e12,
+        "value": attn_rate / 1e12,
         "unit": "TFLOP/s",
         "cores": cores,
         "kind": "oracle",
-        "sample": (f"attention: trajectory 0 rows [0,{R}) x KV groups 0-1 ({len(heads)} heads), "
-                   f"fp32 LogitTree fwd+bwd, {a_s:.2f}s; lm-head: {n} tokens x full vocab, "
-                   f"fp32 fwd+bwd, {l_s:.2f}s; scaled to one step by useful FLOPs "
-                   f"(oracle step = {step_s:.0f}s)"),
+        "sample": (f"attention (the metric): trajectory 0 rows [0,{R}) x KV groups 0-1 "
+                   f"({len(heads)} heads), fp32 LogitTree fwd+bwd, {a_s:.2f}s, rate in useful "
+                   f"FLOPs 14 d P Hq; lm-head: {n} tokens x full vocab, fp32 fwd+bwd, {l_s:.2f}s "
+                   f"({lm_rate / 1e12:.3f} TFLOP/s); whole step scaled by useful FLOPs "
+                   f"= {step_s:.0f}s"),
+        "lm_head_tflops": lm_rate / 1e12,
+        "step_s": step_s,
     }
 
 
@@ -283,6 +303,76 @@ def time_packed(args, mv, synth, trajs, wl, dev):
     }
 
 
+def time_attention(args, mv, synth, workload, seed, dev):
+    """View-masked attention forward + backward alone on one workload, timed
+    with events on the launch stream (per-kernel durations from the library's
+    own launch events)."""
+    import torch
+    wl = synth.ATTN_WORKLOADS[workload]
+    trajs = synth.make_trajectories(workload, seed)
+    b0 = time.perf_counter()
+    mask = mv.ViewMask(trajs)
+    build_ms = (time.perf_counter() - b0) * 1e3
+    mask.upload(dev)
+    st = mask.stats()
+    q, k, v, do = synth.make_attn_tensors(workload, seed, device="cuda")
+    ws = mv.attn_bwd_workspace(mask, q, k)
+
+    def attn():
+        o, lse = mv.attn_fwd(mask, q, k, v)
+        mv.attn_bwd(mask, q, k, v, o, do, lse, workspace=ws)
+
+    for _ in range(args.warmup):
+        attn()
+    torch.cuda.synchronize()
+    mv.profile_enable(True)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        attn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    kt = {}
+    for name in ("attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq"):
+        tot, cnt = mv.profile_read(name)
+        if cnt:
+            kt[name] = round(tot / cnt, 3)
+    mv.profile_enable(False)
+    d, hq = wl.head_dim, wl.n_heads_q
+    P = st["visible_pairs"]
+    useful = 14.0 * d * P * hq
+    tflops = useful / (ms * 1e-3) / 1e12
+    fwd_ms = kt.get("attn_fwd", float("nan"))
+    bwd_ms = sum(x for n, x in kt.items() if n != "attn_fwd")
+    del q, k, v, do, ws
+    torch.cuda.empty_cache()
+    log(f"attention {workload} seed {seed}: {ms:.2f} ms fwd+bwd, {tflops:.0f} TFLOP/s "
+        f"({tflops / PEAK_BF16_TFLOPS:.1%} of peak)")
+    return {
+        "workload": workload,
+        "seed": seed,
+        "shape": (f"{wl.n_traj} x {wl.traj_len} tokens, {wl.n_heads_q}/{wl.n_heads_kv} heads, "
+                  f"d={d}"),
+        "visible_pairs": P,
+        "ms": round(ms, 3),
+        "fwd_ms": round(fwd_ms, 3),
+        "bwd_ms": round(bwd_ms, 3),
+        "useful_tflop": round(useful / 1e12, 3),
+        "useful_tflops": round(tflops, 2),
+        "frac_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "trajectory_tokens_per_s": round(wl.total_tokens / (ms * 1e-3), 1),
+        "fwd_frac_peak": round(4.0 * d * P * hq / (fwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "bwd_frac_peak": round(10.0 * d * P * hq / (bwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        # forward 4 and dQ 6 products over the forward tiles, dK/dV 8 over its own
+        "executed_vs_useful": round((10.0 * st["fwd_tile_pairs"] + 8.0 * st["bwd_tile_pairs"])
+                                    / (14.0 * P), 4),
+        "kernels_ms": kt,
+        "mask_build_ms": round(build_ms, 2),
+    }
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -318,10 +408,15 @@ def main():
     lpb_ws = mv.token_logprob_bwd_workspace(h, w)
     torch.cuda.synchronize()
     log("inputs resident")
+    stream = torch.cuda.current_stream()
 
-    def step():
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
         o, lse = mv.attn_fwd(mask, q, k, v)
         mv.attn_bwd(mask, q, k, v, o, do, lse, workspace=attn_ws)
+        if ev is not None:
+            ev[1].record(stream)
         logp, ratio, clipped, lse_lm = mv.token_logprob(h, w, y, old, lmw.eps_low, lmw.eps_high,
                                                         workspace=lp_ws)
         mv.token_logprob_bwd(h, w, y, lse_lm, g, workspace=lpb_ws)
@@ -340,42 +435,85 @@ def main():
         log("calibration copy of 1 GiB done")
 
     mv.profile_enable(True)
-    stream = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    attn_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     e0.record(stream)
     for i in range(args.steps):
-        step()
+        step(attn_ev[i])
     e1.record(stream)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
     ms_per_step = e0.elapsed_time(e1) / args.steps
+    attn_ms = sum(a.elapsed_time(b) for a, b in attn_ev) / args.steps
     kt = {}
     for name in mv.KERNELS:
         tot, n = mv.profile_read(name)
         if n:
             kt[name] = {"ms_per_launch": tot / n, "launches": n}
     mv.profile_enable(False)
-    log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step (host wall {wall_ms:.2f})")
+    bad = mv.token_logprob_bad_targets(lp_ws) + mv.token_logprob_bad_targets(lpb_ws)
+    assert bad == 0, f"{bad} target ids outside the vocabulary"
+    log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step (host wall {wall_ms:.2f}), "
+        f"attention {attn_ms:.2f} ms")
     dweight = time_dweight(args, mv, h, w, lpb_ws)
     sdcc = None if args.no_sdcc else time_sdcc(args, mv, synth, mask, wl, lmw, dev)
+    del h, w, y, old, g, lp_ws, lpb_ws
+    torch.cuda.empty_cache()
     packed = None if args.no_packed else time_packed(args, mv, synth, trajs, wl, dev)
+    others = []
+    if not args.no_configs:
+        del q, k, v, do, attn_ws
+        torch.cuda.empty_cache()
+        for wname, sd in ((ATTN_WORKLOAD, 1 - args.seed), ("long128k", 0), ("long128k", 1),
+                          ("medium", 0)):
+            others.append(time_attention(args, mv, synth, wname, sd, dev))
 
     d, hq = wl.head_dim, wl.n_heads_q
     T_lm, H, V = lmw.n_tokens, lmw.hidden, lmw.vocab
     attn_useful = 14.0 * d * P * hq
     lm_useful = 6.0 * T_lm * H * V
     step_flops = attn_useful + lm_useful
-    per_launch = kernel_flops(P, d, hq, T_lm, H, V)
-    per_launch = {n: f for n, f in per_launch.items() if not n.startswith("kl")}
-    attn_ms = sum(kt[n]["ms_per_launch"] for n in kt if n.startswith("attn"))
+    af = attn_kernel_flops(st, d, hq)
+    lf = lm_kernel_flops(T_lm, H, V)
     lm_ms = sum(kt[n]["ms_per_launch"] for n in kt if n.startswith("lm"))
-    dom = max((n for n in kt if n in per_launch), key=lambda n: kt[n]["ms_per_launch"])
-    dom_tflops = per_launch[dom] / (kt[dom]["ms_per_launch"] * 1e-3) / 1e12
-    value = step_flops / (ms_per_step * 1e-3) / 1e12
+    attn_kernels_ms = sum(kt[n]["ms_per_launch"] for n in kt if n.startswith("attn"))
+    value = attn_useful / (attn_ms * 1e-3) / 1e12
     tokens = wl.total_tokens
 
+    per_kernel = {}
+    for n, x in kt.items():
+        e = {"ms": round(x["ms_per_launch"], 3)}
+        if n in af:
+            for kind in ("useful", "executed"):
+                r = af[n][kind] / (x["ms_per_launch"] * 1e-3) / 1e12
+                e[f"{kind}_tflop"] = round(af[n][kind] / 1e12, 3)
+                e[f"{kind}_tflops"] = round(r, 2)
+                e[f"{kind}_frac_peak"] = round(r / PEAK_BF16_TFLOPS, 4)
+        elif n in lf:
+            r = lf[n] / (x["ms_per_launch"] * 1e-3) / 1e12
+            e["tflops"] = round(r, 2)
+            e["frac_peak"] = round(r / PEAK_BF16_TFLOPS, 4)
+        per_kernel[n] = e
+
+    def roofline(names, flops_of, label):
+        dom = max((n for n in kt if n in names), key=lambda n: kt[n]["ms_per_launch"])
+        ach = flops_of(dom) / (kt[dom]["ms_per_launch"] * 1e-3) / 1e12
+        return {
+            "bound": "mfma",
+            "kernel": dom,
+            "achieved": round(ach, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+            "traffic": measured_traffic(dom),
+            "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated)",
+            "flops": label,
+        }
+
+    all_flops = {**{n: af[n]["useful"] for n in af}, **lf}
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -392,43 +530,50 @@ def main():
         "config": {
             "workload": (f"{ATTN_WORKLOAD}: {wl.n_traj} x {wl.traj_len}-token packed trajectories, "
                          f"{wl.n_heads_q}/{wl.n_heads_kv} heads, d={d}, 16 edits/trajectory, "
-                         f"attention fwd+bwd; {LM_WORKLOAD}: {T_lm} tokens x {H} hidden x {V} "
-                         f"vocab log-prob/ratio/clip fwd+bwd"),
+                         f"view-masked attention fwd+bwd (value); the step also runs "
+                         f"{LM_WORKLOAD}: {T_lm} tokens x {H} hidden x {V} vocab log-prob/"
+                         f"ratio/clip fwd+bwd"),
             "global_batch": wl.n_traj,
             "seq_len": wl.traj_len,
             "parallelism": "single GPU",
+            "seed": args.seed,
             "visible_pairs": P,
-            "useful_tflop_per_step": round(step_flops / 1e12, 3),
+            "attention_useful_tflop_per_step": round(attn_useful / 1e12, 3),
         },
         "frac_peak": round(value / PEAK_BF16_TFLOPS, 4),
-        "tokens_per_s": round(tokens / (ms_per_step * 1e-3), 1),
+        "tokens_per_s": round(tokens / (attn_ms * 1e-3), 1),
         "attn": {
             "ms": round(attn_ms, 3),
-            "useful_tflops": round(attn_useful / (attn_ms * 1e-3) / 1e12, 2),
-            "frac_peak": round(attn_useful / (attn_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-            "trajectory_tokens_per_s": round(tokens / (attn_ms * 1e-3), 1),
+            "kernels_ms_sum": round(attn_kernels_ms, 3),
             "useful_tflop": round(attn_useful / 1e12, 3),
+            "useful_tflops": round(value, 2),
+            "frac_peak": round(value / PEAK_BF16_TFLOPS, 4),
+            "trajectory_tokens_per_s": round(tokens / (attn_ms * 1e-3), 1),
+            "executed_vs_useful": round(sum(af[n]["executed"] for n in af) / attn_useful, 4),
         },
         "lmhead": {
             "ms": round(lm_ms, 3),
             "useful_tflops": round(lm_useful / (lm_ms * 1e-3) / 1e12, 2),
             "frac_peak": round(lm_useful / (lm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
             "tokens_per_s": round(T_lm / (lm_ms * 1e-3), 1),
+            "dweight": dweight,
         },
-        "kernels_ms": {n: round(x["ms_per_launch"], 3) for n, x in kt.items()},
+        "step": {
+            "ms": round(ms_per_step, 3),
+            "useful_tflop": round(step_flops / 1e12, 3),
+            "useful_tflops": round(step_flops / (ms_per_step * 1e-3) / 1e12, 2),
+            "frac_peak": round(step_flops / (ms_per_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "host_wall_ms": round(wall_ms, 3),
+        },
+        "kernels": per_kernel,
         "mask_build_ms": round(build_ms, 2),
-        "roofline": {
-            "bound": "mfma",
-            "kernel": dom,
-            "achieved": round(dom_tflops, 2),
-            "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": measured_traffic(dom),
-            "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated)",
-        },
+        "roofline": roofline(all_flops, lambda n: all_flops[n],
+                             "algorithmic FLOPs per launch (attention kernels: useful)"),
+        "roofline_attention": roofline(af, lambda n: af[n]["useful"],
+                                       "useful FLOPs per launch (visible pairs only)"),
     }
-    out["lmhead"]["dweight"] = dweight
+    if others:
+        out["attention_configs"] = others
     if sdcc is not None:
         out["sdcc"] = sdcc
     if packed is not None:

@@ -113,6 +113,8 @@ typedef struct {
   int32_t bwd_items;             /* key-tile work items of the dK/dV pass             */
   int32_t bwd_partial_slots;     /* fp32 partial tiles the dK/dV pass reduces         */
   int32_t n_leaves;              /* diverging leaves (see mv_view_mask_leaves)        */
+  int64_t fwd_tile_pairs;        /* (row, key) pairs of the forward / dQ tiles run    */
+  int64_t bwd_tile_pairs;        /* (row, key) pairs of the dK/dV tiles run           */
 } mv_mask_stats;
 
 /* Which conditioning a mask encodes. */
@@ -315,7 +317,10 @@ mv_status mv_attn_bwd(const mv_view_mask* m, const mv_attn_shape* shape,
  * clipped_t = clamp(ratio_t, 1 - eps_low, 1 + eps_high) are the GRPO
  * importance ratio and its clip (Appendix C, "Pitfall A, RL view";
  * Appendix F).  target[t] == -1 marks a token without loss: logp 0, ratio 1,
- * clipped 1, zero gradient.  Targets must lie in [-1, vocab).
+ * clipped 1, zero gradient.  Targets should lie in [-1, vocab); an id outside
+ * that range is never used as an index: the kernels treat its token as one
+ * without loss and count it in the workspace's status word, which
+ * mv_token_logprob_bad_targets reads back.
  *
  * Layouts: hidden bf16 [n_tokens, hidden]; weight bf16 [vocab, hidden];
  * target int32 [n_tokens]; per-token fp32 vectors [n_tokens].
@@ -349,6 +354,16 @@ mv_status mv_token_logprob_bwd(const mv_logprob_shape* shape, const void* hidden
                                const float* lse, const float* dlogp, void* dhidden,
                                void* workspace, size_t workspace_bytes,
                                hipStream_t stream);
+
+/*
+ * Number of target ids outside [-1, vocab) that the last mv_token_logprob or
+ * mv_token_logprob_bwd call on `workspace` met (every such token was scored
+ * as one without loss).  Waits for the stream's work, then copies one word
+ * to *host_count.  The count belongs to the workspace: a later call that
+ * uses the same workspace resets it.
+ */
+mv_status mv_token_logprob_bad_targets(const void* workspace, int32_t* host_count,
+                                       hipStream_t stream);
 
 /*
  * Gradient into the LM-head weights, dweight = G^T hidden (fp32 [vocab,

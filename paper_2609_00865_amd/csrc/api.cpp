@@ -77,6 +77,7 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
                               void* dhidden, void* ws, hipStream_t stream);
 hipError_t launch_logprob_dweight(int T, int H, int V, const void* hidden, const void* ws,
                                   float* dw, hipStream_t stream);
+int* logprob_status_word(const void* ws);
 size_t grpo_ws_bytes(int T, int n_traj);
 hipError_t launch_grpo(int T, int n_traj, int G, float eps_lo, float eps_hi, float beta,
                        float adv_eps, const int32_t* traj_ptr, const float* reward,
@@ -399,6 +400,20 @@ mv_status mv_token_logprob_dweight(const mv_logprob_shape* s, const void* hidden
   return hip_status(mv::launch_logprob_dweight(s->n_tokens, s->hidden, s->vocab, hidden, ws,
                                                dweight, stream),
                     "LM-head weight gradient launch");
+}
+
+mv_status mv_token_logprob_bad_targets(const void* ws, int32_t* host_count,
+                                       hipStream_t stream) {
+  if (ws == nullptr || host_count == nullptr) return fail(MV_ERR_INVALID_ARG, "null argument");
+  int32_t v = 0;
+  if (hipError_t e = hipMemcpyAsync(&v, mv::logprob_status_word(ws), sizeof(v),
+                                    hipMemcpyDeviceToHost, stream);
+      e != hipSuccess)
+    return hip_status(e, "status copy");
+  if (hipError_t e = hipStreamSynchronize(stream); e != hipSuccess)
+    return hip_status(e, "status wait");
+  *host_count = v;
+  return MV_OK;
 }
 
 size_t mv_grpo_loss_workspace_bytes(const mv_grpo_shape* s) {

@@ -97,6 +97,7 @@ struct LmArgs {
   int k_split, nk_split;
   float* dh_part;
   float* dw;          // [V, H] fp32 (dW)
+  int* bad_targets;   // count of target ids outside [-1, V) met by this call
 };
 
 // Output tile (a0, t0) and k split of this block.  Blocks are dealt to XCDs
@@ -289,7 +290,9 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_tile_kernel(LmArgs a) {
       const int tl = t - t0;                       // row within the tile's panels
       const int tc = min(t, a.T - 1);
       const int y = a.tgt[tc];
-      const float ng = (y >= 0 && t < a.T) ? -a.g[tc] : 0.f;
+      // an id outside [0, V) carries no loss (-1 by convention; any other is
+      // counted by lm_target_kernel)
+      const float ng = (uint32_t(y) < uint32_t(a.V) && t < a.T) ? -a.g[tc] : 0.f;
       const float l2 = a.lse[tc] * kLog2e;
 #pragma unroll
       for (int i = 0; i < FA; ++i) {
@@ -557,14 +560,20 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_dw_kernel(LmArgs a) {
 // (BWD = false): stored for the combine pass (0 for a token without loss).
 // Backward: rewrites G[t][y_t], which the grad tile left at -g_t p, to
 // g_t (1 - p) with p = softmax(z_t)_{y_t} from the forward's lse.
+// An id outside [-1, V) is never used as an index: the token is treated as
+// one without loss and counted in *bad_targets (this kernel sees every token
+// exactly once per call).
 template <bool BWD>
 __global__ __launch_bounds__(256) void lm_target_kernel(LmArgs a) {
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (t >= a.T) return;
   const int y = a.tgt[t];
-  if (y < 0) {
-    if (!BWD && lane == 0) a.tlogit[t] = 0.f;
+  if (uint32_t(y) >= uint32_t(a.V)) {
+    if (lane == 0) {
+      if (!BWD) a.tlogit[t] = 0.f;
+      if (y != -1) atomicAdd(a.bad_targets, 1);
+    }
     return;
   }
   const u16* hp = a.h + size_t(t) * a.H;
@@ -637,11 +646,11 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(LmArgs a, const float* 
   if (lane != 0) return;
   const float l = (m + __log2f(s)) * kLn2;
   lse[t] = l;
-  const int y = a.tgt[t];
-  const float lp = y >= 0 ? a.tlogit[t] - l : 0.f;
+  const bool scored = uint32_t(a.tgt[t]) < uint32_t(a.V);
+  const float lp = scored ? a.tlogit[t] - l : 0.f;
   logp[t] = lp;
   if (logp_old != nullptr) {
-    const float r = y >= 0 ? expf(lp - logp_old[t]) : 1.f;
+    const float r = scored ? expf(lp - logp_old[t]) : 1.f;
     ratio[t] = r;
     clipped[t] = fminf(fmaxf(r, 1.f - eps_lo), 1.f + eps_hi);
   }
@@ -742,23 +751,45 @@ static hipError_t zero_row(u16* p, int H, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// Both log-prob workspaces start (at their first 256-byte aligned address)
+// with a 256-byte status block: word 0 counts the target ids outside
+// [-1, V) the last call met.  The call's own buffers follow it.
+constexpr size_t kStatusBytes = 256;
+
+// status | per-(token, chunk) (max, sum) | target logits
 size_t logprob_fwd_ws_bytes(int T, int H, int V) {
   (void)H;
   const int n_chunks = vocab_pad(V) / 128;
-  return align256(size_t(T) * n_chunks * sizeof(float2)) + align256(size_t(T) * sizeof(float)) +
-         256;
+  return kStatusBytes + align256(size_t(T) * n_chunks * sizeof(float2)) +
+         align256(size_t(T) * sizeof(float)) + 256;
 }
 
 static int g_rows(int T) { return panel_rows(T); }
 
-// G [Tg, Vp] | dH partials | W^T [H, Vp] (G and W^T in panels)
+// status | G [Tg, Vp] | dH partials | W^T [H, Vp] (G and W^T in panels)
 size_t logprob_bwd_ws_bytes(int T, int H, int V) {
-  return align256(size_t(g_rows(T)) * vocab_pad(V) * sizeof(u16)) + dh_part_bytes(T, H) +
-         wT_bytes(H, V) + 256;
+  return kStatusBytes + align256(size_t(g_rows(T)) * vocab_pad(V) * sizeof(u16)) +
+         dh_part_bytes(T, H) + wT_bytes(H, V) + 256;
 }
 
 static char* align_ptr(void* p) {
   return reinterpret_cast<char*>((reinterpret_cast<uintptr_t>(p) + 255) & ~uintptr_t(255));
+}
+
+__global__ __launch_bounds__(64) void clear_status_kernel(int* status) {
+  if (threadIdx.x == 0) status[0] = 0;
+}
+
+// The status block of a log-prob workspace, cleared on the stream (a kernel,
+// not a memset, so that the call can be captured in a graph).
+static int* clear_status(void* ws, hipStream_t stream) {
+  int* st = reinterpret_cast<int*>(align_ptr(ws));
+  hipLaunchKernelGGL(clear_status_kernel, dim3(1), dim3(64), 0, stream, st);
+  return st;
+}
+
+int* logprob_status_word(const void* ws) {
+  return reinterpret_cast<int*>(align_ptr(const_cast<void*>(ws)));
 }
 
 static dim3 gemm_grid(const LmArgs& a) {
@@ -833,7 +864,8 @@ hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, c
   a.V = V;
   a.Vp = vocab_pad(V);
   a.n_chunks = a.Vp / 128;
-  char* base = align_ptr(ws);
+  a.bad_targets = clear_status(ws, stream);
+  char* base = align_ptr(ws) + kStatusBytes;
   a.part = reinterpret_cast<float2*>(base);
   a.tlogit = reinterpret_cast<float*>(base + align256(size_t(T) * a.n_chunks * sizeof(float2)));
   a.nA = a.Vp / BA;
@@ -868,7 +900,8 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
   a.V = V;
   a.Vp = vocab_pad(V);
   a.Tg = g_rows(T);
-  char* base = align_ptr(ws);
+  a.bad_targets = clear_status(ws, stream);
+  char* base = align_ptr(ws) + kStatusBytes;
   u16* G = reinterpret_cast<u16*>(base);
   float* part = reinterpret_cast<float*>(base + align256(size_t(a.Tg) * a.Vp * sizeof(u16)));
   u16* wT = reinterpret_cast<u16*>(reinterpret_cast<char*>(part) + dh_part_bytes(T, H));
@@ -896,7 +929,7 @@ hipError_t launch_logprob_dweight(int T, int H, int V, const void* hidden, const
                                   float* dw, hipStream_t stream) {
   LmArgs a{};
   a.h = static_cast<const u16*>(hidden);
-  a.G = reinterpret_cast<const u16*>(align_ptr(const_cast<void*>(ws)));
+  a.G = reinterpret_cast<const u16*>(align_ptr(const_cast<void*>(ws)) + kStatusBytes);
   a.dw = dw;
   a.T = T;
   a.Tg = g_rows(T);

@@ -288,6 +288,7 @@ void build_fwd_schedule(mv_view_mask& m) {
   });
   m.stats.tiles_full = int32_t(full);
   m.stats.tiles_partial = int32_t(partial);
+  m.stats.fwd_tile_pairs = int64_t(full + partial) * BQ * BK;
   m.stats.tiles_skipped = int32_t(skipped);
 }
 
@@ -357,6 +358,9 @@ void build_bwd_schedule(mv_view_mask& m) {
     }
     items[p] = order[q];
   }
+  int64_t bwd_pairs = 0;
+  for (const auto& it : items) bwd_pairs += int64_t(it[2] - it[1]) * BQ * BK;
+  m.stats.bwd_tile_pairs = bwd_pairs;
   m.bwd_items.reserve(items.size() * 4);
   for (const auto& it : items) m.bwd_items.insert(m.bwd_items.end(), it.begin(), it.end());
   m.n_slots = slot;

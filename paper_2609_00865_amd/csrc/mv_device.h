@@ -33,17 +33,25 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-// (M0, which these loads take as the LDS base, is a reserved register that
-// the compiler sets right before each of its own uses, so it needs no clobber.)
+// M0, which these loads take as the LDS base, is a register the compiler
+// may also use (and does not let inline asm clobber), so each helper saves it
+// in a scratch SGPR and restores it right after the issue: from the
+// compiler's view M0 is unchanged.  (The hardware reads M0 when the load is
+// issued.)  The compiler's own LDS-DMA builtins are not used because it
+// cannot tell which LDS buffer they write and would wait for every load in
+// flight before any LDS read.
 // 16 bytes per lane from global memory straight into LDS: lane l's data lands
 // at LDS byte address lds + 16 l (lds is the wave's base, uniform across the
 // wave).  The load is counted by vmcnt only; the compiler does not track it,
 // so the caller waits with wait_vmcnt before a barrier that publishes it.
 __device__ __forceinline__ void lds_load16(const void* src, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
-               : "memory");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory");
 }
 
 // A block-uniform 32-bit word read through the scalar data cache (a scalar
@@ -80,17 +88,23 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
 // wait_vmcnt before the barrier that publishes it.  Offsets must stay in
 // range (an out-of-range lane's LDS bytes are not relied upon).
 __device__ __forceinline__ void buf_lds16(rsrc_t r, uint32_t off, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
-               :
-               : "v"(off), "s"(r), "s"(__builtin_amdgcn_readfirstlane(lds))
-               : "memory");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(r), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory");
 }
 // 4 bytes per lane from a raw buffer straight into LDS (lane l at lds + 4 l).
 __device__ __forceinline__ void buf_lds4(rsrc_t r, uint32_t off, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dword %0, %1, 0 offen lds"
-               :
-               : "v"(off), "s"(r), "s"(__builtin_amdgcn_readfirstlane(lds))
-               : "memory");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\tbuffer_load_dword %1, %2, 0 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(r), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory");
 }
 __device__ __forceinline__ uint4 buf_ld16(rsrc_t r, uint32_t off) {
   const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);

@@ -55,7 +55,8 @@ class MaskStats(ctypes.Structure):
                 ("max_view", ctypes.c_int32), ("n_segments", ctypes.c_int32),
                 ("tiles_full", ctypes.c_int32), ("tiles_partial", ctypes.c_int32),
                 ("tiles_skipped", ctypes.c_int32), ("bwd_items", ctypes.c_int32),
-                ("bwd_partial_slots", ctypes.c_int32), ("n_leaves", ctypes.c_int32)]
+                ("bwd_partial_slots", ctypes.c_int32), ("n_leaves", ctypes.c_int32),
+                ("fwd_tile_pairs", ctypes.c_int64), ("bwd_tile_pairs", ctypes.c_int64)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -144,6 +145,8 @@ mv_token_logprob_bwd = _sig("mv_token_logprob_bwd", ctypes.c_int, _P(LogprobShap
                             _vp, _vp, _vp, _vp, _vp, _sz, _vp)
 mv_token_logprob_dweight = _sig("mv_token_logprob_dweight", ctypes.c_int, _P(LogprobShape), _vp,
                                 _vp, _sz, _vp, _vp)
+mv_token_logprob_bad_targets = _sig("mv_token_logprob_bad_targets", ctypes.c_int, _vp, _P(_i32),
+                                    _vp)
 mv_ppo_clip_dlogp = _sig("mv_ppo_clip_dlogp", ctypes.c_int, _i32, _vp, _vp, _f32, _f32, _f32,
                          _vp, _vp)
 mv_build_branch_pack = _sig("mv_build_branch_pack", ctypes.c_int, _P(TrajectoryC), _i32, _i32,
@@ -184,7 +187,7 @@ EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_ma
             "mv_branch_pack_stats", "mv_branch_pack_layout", "mv_branch_pack_mask",
             "mv_branch_pack_device_bytes", "mv_branch_pack_upload", "mv_branch_pack_free",
             "mv_pack_rows", "mv_unpack_rows_sum", "mv_rope", "mv_token_logprob_dweight",
-            "mv_view_mask_intervals",
+            "mv_view_mask_intervals", "mv_token_logprob_bad_targets",
             "mv_profile_enable", "mv_profile_read"]
 
 VIEW_LIVE, VIEW_FINAL = 0, 1
@@ -433,6 +436,14 @@ def token_logprob_dweight(hidden, weight, workspace, stream=None):
     check(mv_token_logprob_dweight(ctypes.byref(s), _ptr(hidden), _ptr(workspace),
                                    workspace.numel(), _ptr(dw), _stream(stream)))
     return dw
+
+
+def token_logprob_bad_targets(workspace, stream=None) -> int:
+    """Target ids outside [-1, vocab) that the last token_logprob /
+    token_logprob_bwd call on `workspace` met (waits for the stream)."""
+    n = ctypes.c_int32()
+    check(mv_token_logprob_bad_targets(_ptr(workspace), ctypes.byref(n), _stream(stream)))
+    return n.value
 
 
 def ppo_clip_dlogp(ratio, adv, eps_low=0.2, eps_high=0.2, scale=1.0, stream=None):

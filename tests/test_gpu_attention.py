@@ -54,20 +54,25 @@ def test_tiny(seed):
     _check_full(trajs, q, k, v, do, f"tiny/{seed}")
 
 
-def test_tiny_negative_controls():
-    """The Naive-Full and Naive-Compressed masks fail the same gates by >= 10x."""
-    trajs = synth.make_trajectories("tiny", 0)
+@pytest.mark.parametrize("seed", [0, 1])
+def test_tiny_negative_controls(seed):
+    """The Naive-Full and Naive-Compressed masks fail the same gates by >= 10x,
+    for the output and for every gradient."""
+    trajs = synth.make_trajectories("tiny", seed)
     t = trajs[0]
-    q, k, v, do = synth.make_attn_tensors("tiny", 0)
+    q, k, v, do = synth.make_attn_tensors("tiny", seed)
     _, g = _run(trajs, q, k, v, do)
     for kind in ("full", "compressed"):
         M = torch.zeros(512, 512, dtype=torch.bool)
         for r, s in enumerate(V.naive_views(t, kind)):
             M[r, list(s)] = True
-        On, _ = OA.dense(trajs, q.to(F64), k.to(F64), v.to(F64), mask=M)
-        max_abs, rel, _ = errors(g["o"], On)
-        print(f"negative control {kind}: max_abs={max_abs:.3e} rel_fro={rel:.3e}", flush=True)
-        assert max_abs >= 10 * ATOL_BF16 and rel >= 10 * REL_FRO
+        On, _, dQn, dKn, dVn = OA.dense(trajs, q.to(F64), k.to(F64), v.to(F64),
+                                        dout=do.to(F64), mask=M)
+        for name, ref in (("o", On), ("dq", dQn), ("dk", dKn), ("dv", dVn)):
+            max_abs, rel, _ = errors(g[name], ref)
+            print(f"negative control {kind} {name}: max_abs={max_abs:.3e} rel_fro={rel:.3e}",
+                  flush=True)
+            assert max_abs >= 10 * ATOL_BF16 and rel >= 10 * REL_FRO
 
 
 @pytest.mark.parametrize("d,hq,hkv,lens,seed", [
@@ -147,29 +152,39 @@ def _sample_rows(trajs, rng, n_random=24):
 
 
 def _sampled_keys(trajs, death, rng, max_range, with_prompt_key):
+    """Keys of the last trajectory whose dK/dV the oracle recomputes: evicted
+    span ends, summary starts, the last rows and random keys with at most
+    max_range rows seeing them; optionally a prompt key (seen by every later
+    row of its trajectory) and always one key seen by more than 32 query
+    blocks of 64 rows, so that split key tiles (partials summed by the reduce
+    pass) are compared too."""
     keys = []
-    for t in trajs[-1:]:
-        if with_prompt_key:
-            keys.append(t.begin + 5)
-        ev = [p for e in t.edits[:3] for (b, x) in e.evict for p in (b, x - 1)]
-        keys += ev
-        summ = [e.summary[0] for e in t.edits[:2]]
-        keys += summ
-        keys.append(t.end - 3)
-    keys += [int(x) for x in rng.integers(0, len(death), size=40)]
+    t = trajs[-1]
+    if with_prompt_key:
+        keys.append(t.begin + 5)
+    split = [j for j in range(t.begin, t.end) if 32 * 64 < death[j] - j <= max_range]
+    if split:
+        keys.append(int(split[int(rng.integers(0, len(split)))]))
+    keys += [p for e in t.edits[:3] for (b, x) in e.evict for p in (b, x - 1)]
+    keys += [e.summary[0] for e in t.edits[:2]]
+    keys.append(t.end - 3)
+    keys += [int(x) for x in rng.integers(t.begin, t.end, size=40)]
     out = []
     for j in keys:
-        if (death[j] - j <= max_range or (with_prompt_key and j == trajs[-1].begin + 5)) and j not in out:
+        if (death[j] - j <= max_range or (with_prompt_key and j == t.begin + 5)) and j not in out:
             out.append(j)
     return out[:8]
 
 
 @pytest.mark.slow
+@pytest.mark.timeout(600)
 @pytest.mark.parametrize("workload,kv_heads,prompt_key", [("b4x32k", [0, 3], True),
-                                                          ("long128k", [5], False)])
+                                                          ("long128k", [5], True)])
 def test_full_size_sampled(workload, kv_heads, prompt_key):
     """At the benchmark's size: sampled rows (O, LSE, dQ) and sampled keys
-    (dK, dV, over every row that sees them) against the oracle."""
+    (dK, dV, over every row that sees them) against the oracle.  The prompt
+    key of the 128K trajectory is seen by all its 131072 rows: its key tile
+    is cut into 64 items whose fp32 partials the reduce pass sums."""
     trajs = synth.make_trajectories(workload, 0)
     wl = synth.ATTN_WORKLOADS[workload]
     G = wl.n_heads_q // wl.n_heads_kv
@@ -194,6 +209,7 @@ def test_full_size_sampled(workload, kv_heads, prompt_key):
     keys = _sampled_keys(trajs, death, rng, max_range=6000, with_prompt_key=prompt_key)
     hk = kv_heads[0]
     grp = list(range(hk * G, (hk + 1) * G))
+    print(f"[gpu] {workload} sampled keys {[(j, death[j] - j) for j in keys]}", flush=True)
     for j in keys:
         _, _, _, dK, dV = OA.logittree(trajs, qc, kc, vc, dout=dc, heads=grp, dtype=F32,
                                        row_range=(j, death[j]), row_chunk=2048)

@@ -14,9 +14,11 @@ F64 = torch.float64
 
 
 def _inputs(T, H, V, seed, skip_every=0):
+    """Inputs with every skip_every-th token (the last of each run, so a
+    single token stays scored) marked as one without loss."""
     h, w, y, old, g = synth.make_logprob_inputs(T, H, V, seed)
     if skip_every:
-        y[::skip_every] = -1
+        y[skip_every - 1::skip_every] = -1
     return h, w, y, old, g
 
 
@@ -45,7 +47,43 @@ def _check(h, w, y, old, g, what, eps_lo=0.2, eps_hi=0.2):
 @pytest.mark.parametrize("T,H,V", [(300, 256, 1000), (257, 128, 600), (64, 192, 256),
                                    (1, 64, 17)])
 def test_small_ragged(T, H, V):
-    _check(*_inputs(T, H, V, 1, skip_every=7), f"lp{T}x{H}x{V}")
+    inputs = _inputs(T, H, V, 1, skip_every=7)
+    assert (inputs[2] >= 0).any()
+    _check(*inputs, f"lp{T}x{H}x{V}")
+
+
+def test_out_of_range_targets_are_skipped_and_counted():
+    """Ids outside [-1, vocab) are never used as an index: their tokens are
+    scored as tokens without loss (logp 0, ratio 1, zero dH) and counted in
+    the workspace's status word; the other tokens are unaffected."""
+    T, H, V = 200, 128, 1000
+    h, w, y, old, g = _inputs(T, H, V, 12)
+    bad = {3: V, 50: V + 12345, 77: -2, 199: 2 ** 31 - 1}
+    for t, val in bad.items():
+        y[t] = val
+    y[10] = -1                          # the ordinary convention: not counted
+    print(f"[gpu] logprob out-of-range targets T={T} H={H} V={V}", flush=True)
+    hd, wd, yd, od, gd = h.cuda(), w.cuda(), y.cuda(), old.cuda(), g.cuda()
+    ws_f = mv.token_logprob_workspace(hd, wd)
+    ws_b = mv.token_logprob_bwd_workspace(hd, wd)
+    logp, ratio, clipped, lse = mv.token_logprob(hd, wd, yd, od, workspace=ws_f)
+    dh = mv.token_logprob_bwd(hd, wd, yd, lse, gd, workspace=ws_b)
+    assert mv.token_logprob_bad_targets(ws_f) == len(bad)
+    assert mv.token_logprob_bad_targets(ws_b) == len(bad)
+    logp, ratio, clipped, dh = logp.cpu(), ratio.cpu(), clipped.cpu(), dh.cpu()
+    skip = torch.tensor(sorted(list(bad) + [10]))
+    assert torch.all(logp[skip] == 0) and torch.all(ratio[skip] == 1)
+    assert torch.all(clipped[skip] == 1) and torch.all(dh[skip].float() == 0)
+    y_ref = y.clone()
+    y_ref[skip] = -1
+    rl, rr, rc, rlse = OL.token_logprob(h, w, y_ref, old)
+    keep = y_ref >= 0
+    assert_rel_close(logp[keep], rl[keep], "bad-id case logp")
+    assert_rel_close(ratio, rr, "bad-id case ratio", rel=2e-3)
+    assert_bf16_close(dh, OL.token_logprob_bwd(h, w, y_ref, g), "bad-id case dH")
+    # a later call on the same workspace starts from zero
+    mv.token_logprob(hd, wd, y_ref.cuda(), od, workspace=ws_f)
+    assert mv.token_logprob_bad_targets(ws_f) == 0
 
 
 def test_clip_edges_exercised():
