@@ -308,6 +308,28 @@ mv_status mv_attn_bwd(const mv_view_mask* m, const mv_attn_shape* shape,
                       void* dq, void* dk, void* dv,
                       void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * backward as mv_attn_bwd, with its workspace replaced by a static scratch
+ * array of MV_ATTN_BWD_NOALLOC_SCRATCH_BYTES that the library keeps on each
+ * GPU it runs on until the process ends.  The caller still passes every input
+ * and output.  A call whose workspace (mv_attn_bwd_workspace_bytes) exceeds
+ * the scratch is refused with MV_ERR_WORKSPACE before anything is enqueued.
+ * No device memory is allocated or freed, and no events are created (the
+ * profiling switch does not apply).  The first call on a device looks up the
+ * scratch's address there (a runtime query, once per device).  All calls on
+ * one GPU share its scratch: calls that overlap in time on one GPU (other
+ * streams, other threads) race and must be serialised by the caller.  Results
+ * are bit-identical to mv_attn_bwd's.
+ */
+#define MV_ATTN_BWD_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+mv_status mv_attn_bwd_noalloc(const mv_view_mask* m, const mv_attn_shape* shape,
+                              const void* q, const void* k, const void* v,
+                              const void* o, const void* dout, const float* lse,
+                              void* dq, void* dk, void* dv, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Fused LM-head token log-prob, importance ratio and clip.
  *

@@ -33,8 +33,9 @@ void prof_clear_locked() {
 }
 }  // namespace
 
-ProfScope::ProfScope(const char* name, hipStream_t stream) : name_(name), stream_(stream) {
-  if (!g_prof_on.load(std::memory_order_relaxed)) return;
+ProfScope::ProfScope(const char* name, hipStream_t stream, bool allowed)
+    : name_(name), stream_(stream) {
+  if (!allowed || !g_prof_on.load(std::memory_order_relaxed)) return;
   if (hipEventCreate(&start_) != hipSuccess) {
     start_ = nullptr;
     return;
@@ -60,8 +61,9 @@ hipError_t launch_attn_fwd(const mv_view_mask& m, int Hq, int Hkv, int D, float 
 hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float scale,
                            const void* q, const void* k, const void* v, const void* o,
                            const void* dout, const float* lse, void* dq, void* dk, void* dv,
-                           void* ws, hipStream_t stream);
+                           void* ws, hipStream_t stream, bool profile = true);
 size_t attn_bwd_ws_bytes(const mv_view_mask& m, int Hq, int Hkv, int D);
+hipError_t attn_bwd_scratch(void** ptr);
 hipError_t launch_materialize(const mv_view_mask& m, int row_begin, int row_end, uint32_t* bits,
                               hipStream_t stream);
 hipError_t launch_ppo_clip(int n, const float* ratio, const float* adv, float eps_lo,
@@ -247,6 +249,30 @@ mv_status mv_attn_bwd(const mv_view_mask* m, const mv_attn_shape* s, const void*
   return hip_status(mv::launch_attn_bwd(*m, s->n_heads_q, s->n_heads_kv, s->head_dim,
                                         attn_scale(s), q, k, v, o, dout, lse, dq, dk, dv, ws,
                                         stream),
+                    "attention backward launch");
+}
+
+mv_status mv_attn_bwd_noalloc(const mv_view_mask* m, const mv_attn_shape* s, const void* q,
+                              const void* k, const void* v, const void* o, const void* dout,
+                              const float* lse, void* dq, void* dk, void* dv,
+                              hipStream_t stream) {
+  if (mv_status st = check_attn(m, s); st != MV_OK) return st;
+  if (mv_status st = check_ptrs({q, k, v, o, dout, lse, dq, dk, dv}); st != MV_OK) return st;
+  const size_t need = mv::attn_bwd_ws_bytes(*m, s->n_heads_q, s->n_heads_kv, s->head_dim);
+  if (need > MV_ATTN_BWD_NOALLOC_SCRATCH_BYTES) {
+    std::ostringstream os;
+    os << "attention backward needs " << need << " bytes of scratch; the static scratch of "
+       << "mv_attn_bwd_noalloc holds " << size_t(MV_ATTN_BWD_NOALLOC_SCRATCH_BYTES)
+       << " (use mv_attn_bwd with a workspace)";
+    return fail(MV_ERR_WORKSPACE, os.str());
+  }
+  if (mv_status st = check_uploaded(m); st != MV_OK) return st;
+  void* scratch = nullptr;
+  if (hipError_t e = mv::attn_bwd_scratch(&scratch); e != hipSuccess)
+    return hip_status(e, "scratch address");
+  return hip_status(mv::launch_attn_bwd(*m, s->n_heads_q, s->n_heads_kv, s->head_dim,
+                                        attn_scale(s), q, k, v, o, dout, lse, dq, dk, dv, scratch,
+                                        stream, /*profile=*/false),
                     "attention backward launch");
 }
 

@@ -11,7 +11,9 @@
 //     Long ranges are cut into items that write fp32 partial tiles; a reduce
 //     pass sums them in a fixed order (deterministic, no atomics).
 // All stores write whole 16-byte or 8-byte runs of a row.
+#include <mutex>
 #include <type_traits>
+#include <unordered_map>
 
 #include "mv_device.h"
 #include "mv_predicate.h"
@@ -633,6 +635,33 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(BwdArgs a, int n_red) {
   }
 }
 
+// Scratch of mv_attn_bwd_noalloc: the backward's workspace (row statistics
+// D and the fp32 partials of split key tiles) in a file-scope device array,
+// one copy on every GPU the library runs on, held until the process ends.
+// Every kernel that reads a byte of it writes that byte earlier in the same
+// call, so nothing needs clearing; calls that overlap on one GPU race.
+static __device__ __align__(256) unsigned char scratch[MV_ATTN_BWD_NOALLOC_SCRATCH_BYTES];
+
+// The device address of `scratch` on the current device.  In host code the
+// array's name is only a stand-in for the symbol, never a device address: the
+// address comes from the runtime once per device and is kept.
+hipError_t attn_bwd_scratch(void** ptr) {
+  static std::mutex mu;
+  static std::unordered_map<int, void*> addr;
+  int dev = -1;
+  if (hipError_t e = hipGetDevice(&dev); e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = addr.find(dev);
+  if (it == addr.end()) {
+    void* p = nullptr;
+    if (hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)); e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    it = addr.emplace(dev, p).first;
+  }
+  *ptr = it->second;
+  return hipSuccess;
+}
+
 size_t attn_bwd_ws_bytes(const mv_view_mask& m, int Hq, int Hkv, int D) {
   return align256(size_t(Hq) * m.T * sizeof(float)) +
          align256(size_t(m.n_slots) * Hkv * 2 * kBwdTileK * D * sizeof(float)) + 256;
@@ -641,7 +670,7 @@ size_t attn_bwd_ws_bytes(const mv_view_mask& m, int Hq, int Hkv, int D) {
 hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float scale,
                            const void* q, const void* k, const void* v, const void* o,
                            const void* dout, const float* lse, void* dq, void* dk, void* dv,
-                           void* ws, hipStream_t stream) {
+                           void* ws, hipStream_t stream, bool profile) {
   BwdArgs a;
   a.q = static_cast<const u16*>(q);
   a.k = static_cast<const u16*>(k);
@@ -677,15 +706,15 @@ hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float 
   // the general predicate only when some key has further live intervals
   const bool iv = !m.iv.empty();
   auto run = [&](auto pre, auto dkdv, auto red, auto dq) {
-    { ProfScope p("attn_bwd_pre", stream);
+    { ProfScope p("attn_bwd_pre", stream, profile);
       hipLaunchKernelGGL(pre, g_pre, b256, 0, stream, a); }
-    { ProfScope p("attn_bwd_dkdv", stream);
+    { ProfScope p("attn_bwd_dkdv", stream, profile);
       hipLaunchKernelGGL(dkdv, g_kv, b256, 0, stream, a); }
     if (n_red) {
-      ProfScope p("attn_bwd_reduce", stream);
+      ProfScope p("attn_bwd_reduce", stream, profile);
       hipLaunchKernelGGL(red, g_red, b256, 0, stream, a, n_red);
     }
-    { ProfScope p("attn_bwd_dq", stream);
+    { ProfScope p("attn_bwd_dq", stream, profile);
       hipLaunchKernelGGL(dq, g_dq, b256, 0, stream, a); }
   };
   if (D == 128 && iv)

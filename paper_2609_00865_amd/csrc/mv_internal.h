@@ -26,10 +26,11 @@ constexpr int kNumXcd = 8;
 
 void set_error(const std::string& msg);
 
-// Brackets one kernel launch with HIP events when profiling is enabled.
+// Brackets one kernel launch with HIP events when profiling is enabled (and
+// `allowed`: a caller that must not create events passes false).
 class ProfScope {
  public:
-  ProfScope(const char* name, hipStream_t stream);
+  ProfScope(const char* name, hipStream_t stream, bool allowed = true);
   ~ProfScope();
   ProfScope(const ProfScope&) = delete;
   ProfScope& operator=(const ProfScope&) = delete;

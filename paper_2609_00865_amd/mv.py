@@ -135,6 +135,8 @@ mv_attn_fwd = _sig("mv_attn_fwd", ctypes.c_int, _vp, _P(AttnShape), _vp, _vp, _v
 mv_attn_bwd_workspace_bytes = _sig("mv_attn_bwd_workspace_bytes", _sz, _vp, _P(AttnShape))
 mv_attn_bwd = _sig("mv_attn_bwd", ctypes.c_int, _vp, _P(AttnShape), _vp, _vp, _vp, _vp, _vp,
                    _vp, _vp, _vp, _vp, _vp, _sz, _vp)
+mv_attn_bwd_noalloc = _sig("mv_attn_bwd_noalloc", ctypes.c_int, _vp, _P(AttnShape), _vp, _vp, _vp,
+                           _vp, _vp, _vp, _vp, _vp, _vp, _vp)
 mv_token_logprob_workspace_bytes = _sig("mv_token_logprob_workspace_bytes", _sz,
                                         _P(LogprobShape))
 mv_token_logprob = _sig("mv_token_logprob", ctypes.c_int, _P(LogprobShape), _vp, _vp, _vp, _vp,
@@ -187,7 +189,7 @@ EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_ma
             "mv_branch_pack_stats", "mv_branch_pack_layout", "mv_branch_pack_mask",
             "mv_branch_pack_device_bytes", "mv_branch_pack_upload", "mv_branch_pack_free",
             "mv_pack_rows", "mv_unpack_rows_sum", "mv_rope", "mv_token_logprob_dweight",
-            "mv_view_mask_intervals", "mv_token_logprob_bad_targets",
+            "mv_view_mask_intervals", "mv_token_logprob_bad_targets", "mv_attn_bwd_noalloc",
             "mv_profile_enable", "mv_profile_read"]
 
 VIEW_LIVE, VIEW_FINAL = 0, 1
@@ -375,6 +377,24 @@ def attn_bwd(mask: ViewMask, q, k, v, o, dout, lse, scale: Optional[float] = Non
     check(mv_attn_bwd(mask.handle, ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
                       _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws),
                       ws.numel(), _stream(stream)))
+    return dq, dk, dv
+
+
+# Bytes of the static scratch mv_attn_bwd_noalloc works in (mv.h)
+ATTN_BWD_NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def attn_bwd_noalloc(mask: ViewMask, q, k, v, o, dout, lse, scale: Optional[float] = None,
+                     stream=None, out=None):
+    """The backward through mv_attn_bwd_noalloc (no workspace).  `out` =
+    (dq, dk, dv) preallocated by the caller; otherwise torch allocates them."""
+    _need_bf16_cuda(q, k, v, o, dout)
+    shape = _attn_shape(mask, q, k, scale)
+    dq, dk, dv = out if out is not None else (torch.empty_like(q), torch.empty_like(k),
+                                              torch.empty_like(v))
+    check(mv_attn_bwd_noalloc(mask.handle, ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v),
+                              _ptr(o), _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
+                              _stream(stream)))
     return dq, dk, dv
 
 

@@ -86,6 +86,26 @@ def test_backward_workspace_errors():
     assert mv.mv_attn_bwd_workspace_bytes(m.handle, ctypes.byref(_shape(d=96))) == 0
 
 
+def test_noalloc_backward_scratch_limit():
+    """mv_attn_bwd_noalloc refuses, before anything is enqueued, a backward
+    whose workspace exceeds its static scratch (the 4 x 32K batch needs
+    ~840 MiB); the 8K trajectory's (~37.5 MiB) fits and gets as far as the
+    upload check."""
+    big = mv.ViewMask(synth.make_trajectories("b4x32k", 0))
+    sh = _shape(T=big.total_tokens, hq=28, hkv=4, d=128)
+    assert mv.mv_attn_bwd_workspace_bytes(big.handle, ctypes.byref(sh)) > \
+        mv.ATTN_BWD_NOALLOC_SCRATCH_BYTES
+    st = mv.mv_attn_bwd_noalloc(big.handle, ctypes.byref(sh), *([FAKE] * 9), None)
+    assert _status(st) == "MV_ERR_WORKSPACE"
+    assert "scratch" in mv.mv_last_error().decode()
+    med = mv.ViewMask(synth.make_trajectories("medium", 0))
+    sh = _shape(T=med.total_tokens, hq=16, hkv=4, d=128)
+    assert 0 < mv.mv_attn_bwd_workspace_bytes(med.handle, ctypes.byref(sh)) <= \
+        mv.ATTN_BWD_NOALLOC_SCRATCH_BYTES
+    st = mv.mv_attn_bwd_noalloc(med.handle, ctypes.byref(sh), *([FAKE] * 9), None)
+    assert _status(st) == "MV_ERR_STATE"
+
+
 def test_logprob_argument_errors():
     s = mv.LogprobShape(16, 100, 50, 0.2, 0.2)
     assert _status(mv.mv_token_logprob(ctypes.byref(s), *([FAKE] * 9), 1 << 30, None)) == "MV_ERR_UNSUPPORTED"
