@@ -8,10 +8,17 @@
 // partial tiles only, updates the online softmax in base 2, and accumulates
 // O^T += V^T P^T with a second MFMA.  K and V go from buffer loads straight
 // into LDS as unpadded rows with permuted 16-byte chunks (kv_swz); the V^T
-// operand is read with the transposing LDS read.  The next tile's loads are
-// in flight during the current tile's math.  Query tiles are visited
-// heaviest first and the heads of one query tile are kept on one XCD so that
-// GQA heads share K/V in that XCD's L2.
+// operand is read with the transposing LDS read.
+//
+// Each wave runs a two-stage software pipeline over the tile list: while the
+// score MFMAs of tile t+1 run, the vector ALU turns tile t's scores into
+// probabilities; while the PV MFMAs of tile t run, it masks tile t+1 and
+// takes its row maxima.  K and V have separate double buffers with their own
+// turns (two barriers per tile), so each load has about one and a half tiles
+// to land.  Query tiles are visited heaviest first and the heads of one query
+// tile are kept on one XCD so that GQA heads share K/V in that XCD's L2.
+#include <type_traits>
+
 #include "mv_device.h"
 #include "mv_predicate.h"
 
@@ -33,11 +40,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   constexpr int BQ = kFwdTileQ, BK = kFwdTileK;
   constexpr int KS = D / 16;          // MFMA k-steps over the head dimension
   constexpr int DB = D / 32;          // 32-row blocks of O^T
-  // Two buffers: key tile e+1 lands while tile e is read.  K and V rows are
-  // unpadded and swizzled (kv_swz).
+  constexpr int NL = KvTileLoader<D, BK>::KLD;   // 16-byte loads per thread per K or V tile
+  constexpr int NLK = NL + 1;                    // a K tile also brings its keys' omega
+  static_assert(BK == 64, "one omega word per lane");
+  static_assert(2 * KS == 16 || 2 * KS == 8, "score MFMAs per tile");
+  // K and V each in two buffers (tile t in buffer t & 1); omega in four
+  // (tile t in t & 3).  Rows are unpadded and swizzled (kv_swz).
   __shared__ __align__(1024) u16 sKbuf[2 * BK * D];
   __shared__ __align__(1024) u16 sVbuf[2 * BK * D];
-  __shared__ __align__(16) int sOmbuf[2 * BK];
+  __shared__ __align__(16) int sOmbuf[4 * BK];
 
   int xcd, local;
   xcd_split(xcd, local);
@@ -66,72 +77,51 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
+  // running max (base-2 units of the scaled scores), the max the current
+  // tile's probabilities use, and this lane's share of the row sum
   float m_run = -INFINITY, l_run = 0.f;
 
   // K and V of KV head hk go from raw buffers straight into LDS.  Keys past
-  // T read row T - 1 (their omega reads as 0, so no row sees them).
+  // T read row T - 1 (their omega reads as 0 through the range-checked
+  // buffer, so no row sees them).
   const uint32_t kv_row = uint32_t(a.Hkv) * D * 2;   // bytes per key row
   const uint32_t kv_bytes = uint32_t(T) * kv_row - uint32_t(hk) * D * 2;
   const rsrc_t krs = make_rsrc(a.k + size_t(hk) * D, kv_bytes);
   const rsrc_t vrs = make_rsrc(a.v + size_t(hk) * D, kv_bytes);
   const rsrc_t omrs = make_rsrc(a.mask.omega, uint32_t(T) * 4);
   const KvTileLoader<D, BK> ldr(tid);
-  int omreg = 0;
-  auto issue_tile = [&](int kt, int buf) {
-    const uint32_t st = uint32_t(buf) * BK * D * 2;
-    ldr.issue(krs, vrs, kt, T, kv_row, lds_addr(sKbuf) + st, lds_addr(sVbuf) + st);
-    omreg = int(buf_ld4(omrs, uint32_t(kt * BK + tid % BK) * 4));  // every thread: key tid % BK
-  };
-
-  // Tile e+1 is in flight while tile e is read; after the barrier that ends
-  // tile e its buffer takes tile e+2.  The omega values go through registers
-  // (written once their load has landed).  One barrier per tile.  Every row
-  // tile lists at least its diagonal key tile.
-  // (block-uniform: the tile list is read with scalar loads, which do not
-  // wait behind the tile loads in flight)
+  // (block-uniform: the tile list is read with scalar loads, only right
+  // after barriers, where no LDS read is outstanding)
   const int e0 = __builtin_amdgcn_readfirstlane(a.mask.q_ptr[qt]);
-  const int e1 = __builtin_amdgcn_readfirstlane(a.mask.q_ptr[qt + 1]);
-  issue_tile(sload_i32(a.mask.k_list + e0) >> 1, 0);
-  wait_vmcnt<0>();
-  sOmbuf[tid % BK] = omreg;   // identical copies
-  if (e0 + 1 < e1) issue_tile(sload_i32(a.mask.k_list + e0 + 1) >> 1, 1);
-  __syncthreads();
-  for (int e = e0; e < e1; ++e) {
-    const int ent = sload_i32(a.mask.k_list + e);
-    const int kt = ent >> 1;
-    const bool full = ent & 1;
-    const int buf = (e - e0) & 1;
-    const char* sK = reinterpret_cast<const char*>(sKbuf + buf * BK * D);
-    const char* sV = reinterpret_cast<const char*>(sVbuf + buf * BK * D);
-    const int* sOm = sOmbuf + buf * BK;
-    const int j0 = kt * BK;
+  const int n = __builtin_amdgcn_readfirstlane(a.mask.q_ptr[qt + 1]) - e0;   // >= 1
+  const int* klist = a.mask.k_list + e0;
+  auto issue_k = [&](int t) {   // K tile t and its omega values (NLK loads)
+    const int kt = sload_i32(klist + t) >> 1;
+    ldr.issue_one(krs, kt, T, kv_row, lds_addr(sKbuf) + uint32_t(t & 1) * BK * D * 2);
+    buf_lds4(omrs, uint32_t(kt * BK + lane) * 4, lds_addr(sOmbuf) + uint32_t(t & 3) * BK * 4);
+  };
+  auto issue_v = [&](int t) {   // V tile t (NL loads)
+    const int kt = sload_i32(klist + t) >> 1;
+    ldr.issue_one(vrs, kt, T, kv_row, lds_addr(sVbuf) + uint32_t(t & 1) * BK * D * 2);
+  };
+  auto ktile = [&](int t) { return reinterpret_cast<const char*>(sKbuf + (t & 1) * BK * D); };
+  auto vtile = [&](int t) { return reinterpret_cast<const char*>(sVbuf + (t & 1) * BK * D); };
 
-    // S^T for keys [kb*32, kb*32+32) of the tile.  The two blocks' MFMAs
-    // alternate, and the K fragments are read four MFMAs ahead (a fixed
-    // order: each MFMA waits only for a read issued long before it).
-    f32x16 s[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-    {
-      auto kfrag = [&](int st) {   // step st: block st % 2, k step st / 2
-        return ld_row_swz<D>(sK, (st & 1) * 32 + c, (st >> 1) * 2 + g);
-      };
-      bf16x8 kr[4];
-#pragma unroll
-      for (int st = 0; st < 4; ++st) kr[st] = kfrag(st);
-#pragma unroll
-      for (int st = 0; st < 2 * KS; ++st) {
-        s[st & 1] = mfma32(kr[st & 3], qf[st >> 1], s[st & 1]);
-        if (st + 4 < 2 * KS) kr[st & 3] = kfrag(st + 4);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
+  // Score sets: tile t's in sc[t & 1] (keys kb*32 + accumulator row).
+  f32x16 sc[2][2];
 
-    // scores stay raw (masked ones -inf); the running max m_run is in base-2
-    // units of the scaled scores
-    if (!full) {  // block-uniform; per element a select, not a branch
+  // S^T of tile t into set P, as MFMA j of 2 KS (block j % 2, k step j / 2)
+  // with the K fragments read four MFMAs ahead.
+  auto kfrag = [&](const char* sK, int j) {
+    return ld_row_swz<D>(sK, (j & 1) * 32 + c, (j >> 1) * 2 + g);
+  };
+  // Mask (partial tiles) and row max of tile t's scores in set P: returns
+  // the tile's max in base-2 units (-inf for a row that sees none of it).
+  auto mask_tile = [&](f32x16 (&s)[2], int t) {
+    const int ent = sload_i32(klist + t);
+    if (!(ent & 1)) {   // block-uniform; per element a select, not a branch
+      const int j0 = (ent >> 1) * BK;
+      const int* sOm = sOmbuf + (t & 3) * BK;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -147,16 +137,20 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
           }
         }
     }
+  };
+  // element i (0..31) of a tile: block i / 16, accumulator row i % 16
+  auto tile_max = [&](const f32x16 (&s)[2]) {
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    // Lazy rescaling: the running max moves only when a tile's max exceeds it
-    // by more than 8 (base 2); until then p = exp2(x - m_run) <= 2^8, well
-    // inside fp32 and the bf16 operand range, and O and l keep their scale.
-    const float m_tile = mx * a.scale_log2;     // -inf for a fully masked row
+    return max_halves(mx) * a.scale_log2;
+  };
+  // Lazy rescaling: the running max moves only when a tile's max exceeds it
+  // by more than 8 (base 2); until then p = exp2(x - m_run) <= 2^8, well
+  // inside fp32 and the bf16 operand range, and O and l keep their scale.
+  auto rescale = [&](float m_tile) {
     const bool grow = m_tile > m_run + 8.f;
     if (__any(grow)) {
       const float alpha = grow ? fast_exp2(m_run - m_tile) : 1.f;
@@ -167,41 +161,135 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
     }
+  };
+
+  // ---- prologue: K0, K1, V0 (the issue order the pipeline's waits assume)
+  issue_k(0);
+  if (n > 1) issue_k(1);
+  issue_v(0);
+  if (n > 1)
+    wait_vmcnt<NLK + NL>();
+  else
+    wait_vmcnt<NL>();
+  __syncthreads();
+  {
+    const char* sK = ktile(0);
+#pragma unroll
+    for (int j = 0; j < 2 * KS; ++j)
+      sc[0][j & 1] = mfma32(kfrag(sK, j), qf[j >> 1], j < 2 ? f32x16{} : sc[0][j & 1]);
+  }
+  mask_tile(sc[0], 0);
+  rescale(tile_max(sc[0]));
+  __syncthreads();                      // every wave is done with K0's buffer
+  if (n > 2) issue_k(2);
+
+  // ---- one pipeline step: tile t (scores in set P) and tile t+1 (scores
+  // into set P ^ 1).  On the last tile (no t+1) the score MFMAs still run,
+  // on stale LDS, and their results are dropped: the interleaved phases
+  // stay free of branches.
+  auto step = [&](auto par_tag, int t) {
+    constexpr int P = decltype(par_tag)::value;
+    f32x16 (&cur)[2] = sc[P];
+    f32x16 (&nxt)[2] = sc[P ^ 1];
+    const bool next = t + 1 < n;   // block-uniform
+
+    // barrier 1: K[t+1] landed (loads issued after it: V[t], K[t+2])
+    if (t + 2 < n)
+      wait_vmcnt<NL + NLK>();
+    else if (next)
+      wait_vmcnt<NL>();
+    __syncthreads();
+    if (next) issue_v(t + 1);   // into V[t-1]'s buffer (read before this barrier)
+
+    // phase 1: S^T of tile t+1 (16 MFMAs) with the exponentials of tile t's
+    // elements 0..23 (spread evenly over the MFMA slots) and their bf16
+    // operands
     const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
     float psum = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(fmaf(s[kb][r], a.scale_log2, -m_use));
-        s[kb][r] = p;
-        psum += p;
-      }
-    l_run += psum;
-
     bf16x8 pf[4];
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) pf[ks] = to_operand(s[ks >> 1], (ks & 1) * 8);
+    auto celem = [&](int i) {
+      const float x = fast_exp2(fmaf(cur[i >> 4][i & 15], a.scale_log2, -m_use));
+      cur[i >> 4][i & 15] = x;
+      psum += x;
+    };
     {
-      // V^T operand of step st: column block st % DB, keys (st / DB)*16 ..
-      // in accumulator order; read four MFMAs ahead as above
+      const char* sK = ktile(t + 1);
+      bf16x8 kr[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) kr[j] = kfrag(sK, j);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int j = 0; j < 2 * KS; ++j) {
+        nxt[j & 1] = mfma32(kr[j & 3], qf[j >> 1], j < 2 ? f32x16{} : nxt[j & 1]);
+        if (j + 4 < 2 * KS) kr[j & 3] = kfrag(sK, j + 4);
+        // elements [24 j / NS, 24 (j + 1) / NS) in slot j; operand k (elements
+        // 8k .. 8k+7) packed in the slot that finishes it
+        constexpr int NS = 2 * KS;
+        const int i0 = 24 * j / NS, i1 = 24 * (j + 1) / NS;
+#pragma unroll
+        for (int i = i0; i < i1; ++i) celem(i);
+        if (i1 / 8 != i0 / 8) {
+          const int k = i1 / 8 - 1;
+          pf[k] = to_operand(cur[k >> 1], (k & 1) * 8);
+          // an empty asm that consumes the operand keeps its computation in
+          // this phase (the compiler would otherwise sink it past the
+          // barrier, next to the MFMAs that read it)
+          asm volatile("" : "+v"(pf[k]));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    asm volatile("" : "+v"(psum));
+
+    // barrier 2: V[t] landed (loads issued after it: K[t+2], V[t+1])
+    if (t + 2 < n)
+      wait_vmcnt<NLK + NL>();
+    else if (next)
+      wait_vmcnt<NL>();
+    else
+      wait_vmcnt<0>();
+    __syncthreads();
+    if (t + 3 < n) issue_k(t + 3);   // into K[t+1]'s buffer (read in phase 1)
+    if (next) mask_tile(nxt, t + 1);
+
+    // phase 2: O^T += V^T P^T of tile t (16 MFMAs, V^T read four ahead) with
+    // tile t's elements 24..31 first, then tile t+1's row max
+    {
+      const char* sV = vtile(t);
       auto vfrag = [&](int st) { return ld_tr_swz<D>(sV, (st / DB) * 16, (st % DB) * 32); };
       bf16x8 vr[4];
 #pragma unroll
       for (int st = 0; st < 4; ++st) vr[st] = vfrag(st);
+      float mx = -INFINITY;
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int st = 0; st < 4 * DB; ++st) {
+        if (st == 0) {
+#pragma unroll
+          for (int i = 24; i < 32; ++i) celem(i);
+          pf[3] = to_operand(cur[1], 8);
+        }
         oacc[st % DB] = mfma32(vr[st & 3], pf[st / DB], oacc[st % DB]);
         if (st + 4 < 4 * DB) vr[st & 3] = vfrag(st + 4);
+        // the next tile's elements, spread over the slots after the first
+        constexpr int NS = 4 * DB - 1;
+        if (st >= 1) {
+          const int i0 = 32 * (st - 1) / NS, i1 = 32 * st / NS;
+#pragma unroll
+          for (int i = i0; i < i1; ++i) mx = fmaxf(mx, nxt[i >> 4][i & 15]);
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
+      l_run += psum;
+      if (next) rescale(max_halves(mx) * a.scale_log2);
     }
-    // tile e+1 has landed (and its omega values are written) before the
-    // barrier that publishes it; then tile e's buffer takes tile e+2
-    wait_vmcnt<0>();
-    if (e + 1 < e1) sOmbuf[(buf ^ 1) * BK + tid % BK] = omreg;
-    __syncthreads();
-    if (e + 2 < e1) issue_tile(sload_i32(a.mask.k_list + e + 2) >> 1, buf);
+  };
+
+  using p0 = std::integral_constant<int, 0>;
+  using p1 = std::integral_constant<int, 1>;
+  for (int t = 0; t < n; t += 2) {
+    step(p0{}, t);
+    if (t + 1 < n) step(p1{}, t + 1);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);

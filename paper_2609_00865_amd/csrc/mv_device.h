@@ -54,13 +54,26 @@ __device__ __forceinline__ void lds_load16(const void* src, uint32_t lds) {
       : "memory");
 }
 
+// A wave-uniform pointer taken through readfirstlane, so that it is held in
+// scalar registers (the inline asm below takes scalar operands; the compiler
+// may otherwise keep a uniform value in vector registers).
+template <typename X>
+__device__ __forceinline__ X* uniform_ptr(X* p) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(a));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(a >> 32));
+  return reinterpret_cast<X*>((uint64_t(hi) << 32) | lo);
+}
+
 // A block-uniform 32-bit word read through the scalar data cache (a scalar
 // load, tracked by lgkmcnt): it does not wait behind vector loads in flight,
 // as a vector load of the same word would.  p must be uniform; the data must
 // not change during the kernel.
 __device__ __forceinline__ int sload_i32(const int* p) {
   int v;
-  asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(p));
+  asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)"
+               : "=s"(v)
+               : "s"(uniform_ptr(p)));
   return v;
 }
 
@@ -80,7 +93,8 @@ __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<
 // SGPR offset is used.)  Word 3 is the gfx9 descriptor format (32-bit data).
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(uniform_ptr(base)), 0,
+                                           __builtin_amdgcn_readfirstlane(bytes), 0x00020000);
 }
 // 16 bytes per lane from a raw buffer straight into LDS: lane l's data
 // lands at LDS byte address lds + 16 l (lds uniform across the wave).  As
@@ -145,6 +159,14 @@ __device__ __forceinline__ bf16x8 to_operand(const f32x16& acc, int base) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// max of x over lanes l and l ^ 32 (gfx950's permlane32_swap: a VALU op, no
+// LDS round trip)
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
+                                                  __builtin_bit_cast(uint32_t, x), false, false);
+  return fmaxf(__builtin_bit_cast(float, uint32_t(r[0])), __builtin_bit_cast(float, uint32_t(r[1])));
+}
+
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
@@ -205,6 +227,17 @@ struct KvTileLoader {
       const int P = (r * 4 + (tid >> 6)) * 64 + (tid & 63);
       row[r] = P / (D / 8);
       col[r] = uint32_t((P % (D / 8)) ^ kv_swz<D>(P / (D / 8))) * 16;
+    }
+  }
+  // one tensor's key tile kt into the tile at LDS byte address lds (KLD
+  // loads per thread)
+  __device__ __forceinline__ void issue_one(rsrc_t rs, int kt, int T, uint32_t kv_row,
+                                            uint32_t lds) const {
+    const uint32_t wv = uint32_t(threadIdx.x >> 6) * 1024;
+#pragma unroll
+    for (int r = 0; r < KLD; ++r) {
+      const uint32_t off = uint32_t(min(kt * BK + row[r], T - 1)) * kv_row + col[r];
+      buf_lds16(rs, off, lds + wv + r * 4096);
     }
   }
   // K and V of key tile kt into the tiles at LDS byte addresses ldsK, ldsV
