@@ -2,7 +2,8 @@
 // trajectory instead of one per branch (Section 4.3, "Cost and deployment
 // splits").  Three passes, all recomputing P from the forward's LSE:
 //
-//  1. D_i = <dO_i, O_i> per row and head (HBM-bound, tiny).
+//  1. D_i = <dO_i, O_i> per row and head, and the row's LSE in base-2 units
+//     (HBM-bound, tiny).
 //  2. dQ: per 128-row query tile and head, over the forward's tile list:
 //     S^T = K Q^T, dP^T = V dO^T, dS^T = P^T o (dP^T - D), dQ^T += K^T dS^T.
 //  3. dK/dV: per 128-key tile and KV head, over the contiguous row range that
@@ -36,6 +37,7 @@ struct BwdArgs {
   u16* dk;
   u16* dv;
   float* Dd;       // [Hq, T]
+  float* L2;       // [Hq, T] LSE in base-2 units (LSE * log2 e), written by pass 1
   float* partial;  // [n_slots, Hkv, 2, 128, D]
   mv_mask_dev mask;
   int T, Hq, Hkv, n_qt, n_items;
@@ -70,6 +72,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
   if (ok && gid % LPV == 0) {
     const int i = int(vec / a.Hq), h = int(vec % a.Hq);
     a.Dd[size_t(h) * a.T + i] = acc;
+    a.L2[size_t(h) * a.T + i] = a.lse[size_t(h) * a.T + i] * kLog2e;
   }
 }
 
@@ -236,10 +239,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   constexpr int NBUF = 4;
   __shared__ __align__(1024) u16 sQbuf[NBUF * BQ * D];
   __shared__ __align__(1024) u16 sdObuf[NBUF * BQ * D];
-  __shared__ __align__(16) float sLbuf[NBUF * BQ];   // LSE (natural log)
+  __shared__ __align__(16) float sLbuf[NBUF * BQ];   // LSE * log2 e
   __shared__ __align__(16) float sDbuf[NBUF * BQ];
-  auto qtile = [&](int st) { return reinterpret_cast<const char*>(sQbuf + (st % NBUF) * BQ * D); };
-  auto dotile = [&](int st) { return reinterpret_cast<const char*>(sdObuf + (st % NBUF) * BQ * D); };
+  // block of step st in buffer st % NBUF (buf below)
+  auto qtile = [&](int buf) { return reinterpret_cast<const char*>(sQbuf + buf * BQ * D); };
+  auto dotile = [&](int buf) { return reinterpret_cast<const char*>(sdObuf + buf * BQ * D); };
 
   int xcd, local;
   xcd_split(xcd, local);
@@ -289,19 +293,20 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const KvTileLoader<D, BQ> ldr(tid);
   constexpr int LPS = 2 * KvTileLoader<D, BQ>::KLD + 1;
   static_assert(BQ == 64, "one LSE / D word per lane");
-  auto issue_step = [&](int st) {
-    const int hh = h0 + st / nqb, qb = qb0 + st % nqb, buf = st % NBUF;
+  auto issue_step = [&](int st, int buf) {   // a step past the last reloads the last block
+    const int sc_ = min(st, steps - 1);
+    const int hh = h0 + sc_ / nqb, qb = qb0 + sc_ % nqb;
     const uint32_t bytes = uint32_t(T) * q_row - uint32_t(hh) * D * 2;
     ldr.issue(make_rsrc(a.q + size_t(hh) * D, bytes), make_rsrc(a.dout + size_t(hh) * D, bytes), qb,
               T, q_row, lds_addr(sQbuf) + buf * BQ * D * 2, lds_addr(sdObuf) + buf * BQ * D * 2);
     const bool odd = __builtin_amdgcn_readfirstlane(wave) & 1;   // wave-uniform
-    const float* vec = (odd ? a.Dd : a.lse) + size_t(hh) * T;
+    const float* vec = (odd ? a.Dd : a.L2) + size_t(hh) * T;
     buf_lds4(make_rsrc(vec, uint32_t(T) * 4), uint32_t(min(qb * BQ + lane, T - 1)) * 4,
              (odd ? lds_addr(sDbuf) : lds_addr(sLbuf)) + buf * BQ * 4);
   };
   // before the barrier that ends step st: block st+2 landed (st+3 may fly)
-  auto wait_step = [&](int st) {
-    if (st + 3 < steps)
+  auto wait_step = [&](int st, int n_steps) {
+    if (st + 3 < n_steps)
       wait_vmcnt<LPS>();
     else
       wait_vmcnt<0>();
@@ -313,8 +318,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   // its share of dV^T += dO^T P and dK^T += Q^T dS.
   f32x16 s, dp;
   auto scores_mfma = [&](int st, int mb) {
-    const char* sQ = qtile(st);
-    const char* sdO = dotile(st);
+    const char* sQ = qtile(st % NBUF);
+    const char* sdO = dotile(st % NBUF);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       s[r] = 0.f;
@@ -342,7 +347,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       const int qo = mb * 32 + q4 * 8 + g * 4;
       const float4 l4 = *reinterpret_cast<const float4*>(&sL[qo]);
       const float4 d4 = *reinterpret_cast<const float4*>(&sD[qo]);
-      const float lv[4] = {l4.x * kLog2e, l4.y * kLog2e, l4.z * kLog2e, l4.w * kLog2e};
+      const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
       const float dd[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -363,8 +368,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     dsf[1] = to_operand(dp, 8);
   };
   auto accumulate = [&](int st, int mb, const bf16x8 (&pf)[2], const bf16x8 (&dsf)[2]) {
-    const char* sQ = qtile(st);
-    const char* sdO = dotile(st);
+    const char* sQ = qtile(st % NBUF);
+    const char* sdO = dotile(st % NBUF);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -386,23 +391,23 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   float lv[16], dd[16];
   int ui0 = 0, umb = 0;
   uint32_t urange = 0;
-  auto load_ctx = [&](int st, int mb) {
-    const int buf = st % NBUF;
+  auto load_ctx = [&](int st, int mb, int buf) {
     const float* sL = sLbuf + buf * BQ;
     const float* sD = sDbuf + buf * BQ;
     ui0 = (qb0 + st % nqb) * BQ;
     umb = mb;
     const bool full = (ui0 >= j1 - 1) && (ui0 + BQ <= om_min);
-    urange = full ? 0x7fffffffu : uint32_t(om - key);
+    // a padding step past the last (st >= steps) sees nothing
+    urange = st >= steps ? 0u : full ? 0x7fffffffu : uint32_t(om - key);
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       const int qo = mb * 32 + q4 * 8 + g * 4;
       const float4 l4 = *reinterpret_cast<const float4*>(&sL[qo]);
       const float4 d4 = *reinterpret_cast<const float4*>(&sD[qo]);
-      lv[q4 * 4 + 0] = l4.x * kLog2e;
-      lv[q4 * 4 + 1] = l4.y * kLog2e;
-      lv[q4 * 4 + 2] = l4.z * kLog2e;
-      lv[q4 * 4 + 3] = l4.w * kLog2e;
+      lv[q4 * 4 + 0] = l4.x;
+      lv[q4 * 4 + 1] = l4.y;
+      lv[q4 * 4 + 2] = l4.z;
+      lv[q4 * 4 + 3] = l4.w;
       dd[q4 * 4 + 0] = d4.x; dd[q4 * 4 + 1] = d4.y; dd[q4 * 4 + 2] = d4.z; dd[q4 * 4 + 3] = d4.w;
     }
   };
@@ -415,10 +420,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   };
   // phase X of the unit in set par: the next unit's (st, mb) S/dP MFMAs into
   // set par ^ 1 (if NEXT) with elements 8..15 of this unit, then its operands
-  auto phaseX = [&](auto next_tag, int par, int st, int mb, bf16x8 (&pfo)[2], bf16x8 (&dso)[2]) {
+  auto phaseX = [&](auto next_tag, int par, int st, int mb, bf16x8 (&pfo)[2], bf16x8 (&dso)[2],
+                    int buf) {
     constexpr bool NEXT = decltype(next_tag)::value;
-    const char* sQ = qtile(st);
-    const char* sdO = dotile(st);
+    const char* sQ = qtile(buf);
+    const char* sdO = dotile(buf);
     const int np = par ^ 1;
     auto opnd = [&](int j) {   // MFMA j: ks = j / 2, S (even) or dP (odd)
       return ld_row_swz<D>((j & 1) ? sdO : sQ, mb * 32 + c, (j >> 1) * 2 + g);
@@ -456,11 +462,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   // phase Y of unit (st, mb): its dV/dK MFMAs with elements 0..7 of the next
   // unit (st2, mb2) in set np, whose context is loaded first (if NEXT)
   auto phaseY = [&](auto next_tag, int st, int mb, const bf16x8 (&pfc)[2], const bf16x8 (&dsc)[2],
-                    int np, int st2, int mb2) {
+                    int np, int st2, int mb2, int buf, int buf2) {
     constexpr bool NEXT = decltype(next_tag)::value;
-    if constexpr (NEXT) load_ctx(st2, mb2);
-    const char* sQ = qtile(st);
-    const char* sdO = dotile(st);
+    if constexpr (NEXT) load_ctx(st2, mb2, buf2);
+    const char* sQ = qtile(buf);
+    const char* sdO = dotile(buf);
     // MFMA q: db = q / 4, kk = (q / 2) % 2, dV (even q) or dK (odd q)
     auto opnd = [&](int q) {
       return ld_tr_swz<D>((q & 1) ? sQ : sdO, (2 * mb + ((q >> 1) & 1)) * 16, (q >> 2) * 32);
@@ -494,24 +500,24 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   // the next unit's exponentials follow them.  Block st+3 is requested into
   // the buffer step st-1 used (every wave finished with it before the last
   // barrier).
-  issue_step(0);
-  if (steps > 1) issue_step(1);
-  if (steps > 2) issue_step(2);
-  wait_step(-1);   // blocks 0 and 1 landed
-  __syncthreads();
   bf16x8 pf[2], dsf[2];
   if constexpr (IV) {
+    issue_step(0, 0);
+    if (steps > 1) issue_step(1, 1);
+    if (steps > 2) issue_step(2, 2);
+    wait_step(-1, steps);   // blocks 0 and 1 landed
+    __syncthreads();
     scores_mfma(0, 0);
     scores_valu(0, 0, pf, dsf);
     for (int st = 0; st + 1 < steps; ++st) {
-      if (st + 3 < steps) issue_step(st + 3);
+      if (st + 3 < steps) issue_step(st + 3, (st + 3) % NBUF);
       scores_mfma(st, 1);
       accumulate(st, 0, pf, dsf);
       scores_valu(st, 1, pf, dsf);
       scores_mfma(st + 1, 0);
       accumulate(st, 1, pf, dsf);
       scores_valu(st + 1, 0, pf, dsf);
-      wait_step(st);
+      wait_step(st, steps);
       __syncthreads();
     }
     scores_mfma(steps - 1, 1);
@@ -519,10 +525,21 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     scores_valu(steps - 1, 1, pf, dsf);
     accumulate(steps - 1, 1, pf, dsf);
   } else {
+    // The step count is padded to a multiple of NBUF with steps that see
+    // nothing (they reload the last block, so every operand is finite), and
+    // the loop is unrolled NBUF times: every LDS buffer index is then a
+    // compile-time constant and the fragment reads use immediate offsets.
+    // The last step starts a unit past the end whose results are dropped.
     using yes = std::true_type;
-    using no = std::false_type;
+    const int steps_pad = (steps + NBUF - 1) / NBUF * NBUF;
+    static_assert(NBUF == 4, "unrolled four times");
+    issue_step(0, 0);
+    issue_step(1, 1);
+    issue_step(2, 2);
+    wait_step(-1, steps_pad);   // blocks 0 and 1 landed
+    __syncthreads();
     // unit (0, 0): S/dP into set 0, its context, elements 0..7
-    load_ctx(0, 0);
+    load_ctx(0, 0, 0);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       sc[0][r] = 0.f;
@@ -535,20 +552,21 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     }
 #pragma unroll
     for (int r = 0; r < 8; ++r) elem(0, r);
-    for (int st = 0; st + 1 < steps; ++st) {
-      if (st + 3 < steps) issue_step(st + 3);
-      phaseX(yes{}, 0, st, 1, pf, dsf);          // S/dP of (st, 1); finish (st, 0)
-      phaseY(yes{}, st, 0, pf, dsf, 1, st, 1);   // dV/dK of (st, 0); start (st, 1)
-      phaseX(yes{}, 1, st + 1, 0, pf, dsf);      // S/dP of (st+1, 0); finish (st, 1)
-      phaseY(yes{}, st, 1, pf, dsf, 0, st + 1, 0);
-      wait_step(st);
+    auto iter = [&](int st, int u) {   // u = st % NBUF, a constant at each call
+      if (st + 3 < steps_pad) issue_step(st + 3, (u + 3) & 3);
+      phaseX(yes{}, 0, st, 1, pf, dsf, u);                           // S/dP of (st, 1); finish (st, 0)
+      phaseY(yes{}, st, 0, pf, dsf, 1, st, 1, u, u);                 // dV/dK of (st, 0); start (st, 1)
+      phaseX(yes{}, 1, st + 1, 0, pf, dsf, (u + 1) & 3);             // S/dP of (st+1, 0); finish (st, 1)
+      phaseY(yes{}, st, 1, pf, dsf, 0, st + 1, 0, u, (u + 1) & 3);   // dV/dK of (st, 1); start (st+1, 0)
+      wait_step(st, steps_pad);
       __syncthreads();
+    };
+    for (int st = 0; st < steps_pad; st += NBUF) {
+      iter(st, 0);
+      iter(st + 1, 1);
+      iter(st + 2, 2);
+      iter(st + 3, 3);
     }
-    const int st = steps - 1;
-    phaseX(yes{}, 0, st, 1, pf, dsf);
-    phaseY(yes{}, st, 0, pf, dsf, 1, st, 1);
-    phaseX(no{}, 1, st, 1, pf, dsf);
-    phaseY(no{}, st, 1, pf, dsf, 0, st, 1);
   }
 
   if (!kok) return;
@@ -662,8 +680,9 @@ hipError_t attn_bwd_scratch(void** ptr) {
   return hipSuccess;
 }
 
+// D [Hq, T] | LSE * log2 e [Hq, T] | fp32 partials [n_slots, Hkv, 2, 128, D]
 size_t attn_bwd_ws_bytes(const mv_view_mask& m, int Hq, int Hkv, int D) {
-  return align256(size_t(Hq) * m.T * sizeof(float)) +
+  return 2 * align256(size_t(Hq) * m.T * sizeof(float)) +
          align256(size_t(m.n_slots) * Hkv * 2 * kBwdTileK * D * sizeof(float)) + 256;
 }
 
@@ -683,8 +702,10 @@ hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float 
   a.dv = static_cast<u16*>(dv);
   char* base = static_cast<char*>(ws);
   base = reinterpret_cast<char*>((reinterpret_cast<uintptr_t>(base) + 255) & ~uintptr_t(255));
+  const size_t row_stat = align256(size_t(Hq) * m.T * sizeof(float));
   a.Dd = reinterpret_cast<float*>(base);
-  a.partial = reinterpret_cast<float*>(base + align256(size_t(Hq) * m.T * sizeof(float)));
+  a.L2 = reinterpret_cast<float*>(base + row_stat);
+  a.partial = reinterpret_cast<float*>(base + 2 * row_stat);
   a.mask = m.d;
   a.T = m.T;
   a.Hq = Hq;
