@@ -244,15 +244,18 @@ def time_dweight(args, mv, h, w, ws):
             "frac_peak": round(tflops / PEAK_BF16_TFLOPS, 4)}
 
 
-def time_packed(args, mv, synth, trajs, wl, dev):
-    """One exact attention layer on the branch-replicated packed stream of the
-    same batch (the form that stays exact through a stack of layers): rotary
+def time_packed(args, mv, synth, trajs, wl, dev, shared):
+    """One exact attention layer on a packed stream of the same batch's branch
+    layers (the forms that stay exact through a stack of layers): rotary
     embedding of Q and K by per-branch positions, attention forward and
-    backward under the block-diagonal mask, the inverse rotation of dQ and dK.
-    Timed on its own after the step; useful FLOPs 14 d P Hq with P the packed
-    stream's causal pairs."""
+    backward under the stream's mask, the inverse rotation of dQ and dK.
+    shared = False: every branch replicates its trunk (LogitTree's branch
+    forwards); True: each branch stores only what it does not share with the
+    branch before it and reads the shared trunk's keys in place.  Timed on its
+    own after the step; useful FLOPs 14 d P Hq with P the stream's visible
+    pairs."""
     import torch
-    pk = mv.BranchPack(trajs).upload(dev)
+    pk = mv.BranchPack(trajs, shared_trunk=shared).upload(dev)
     st = pk.stats()
     N = st["n_packed"]
     gen = torch.Generator(device="cuda")
@@ -289,18 +292,72 @@ def time_packed(args, mv, synth, trajs, wl, dev):
         if cnt:
             kt[name] = round(tot / cnt, 3)
     mv.profile_enable(False)
+    attn_ms = sum(x for n, x in kt.items() if n != "rope")
     useful = 14.0 * wl.head_dim * st["causal_pairs"] * wl.n_heads_q
     tflops = useful / (ms * 1e-3) / 1e12
-    log(f"packed stream: N={N}, {ms:.2f} ms per exact layer fwd+bwd, {tflops:.0f} TFLOP/s")
+    del q, k, v, do, ws, qr, kr
+    torch.cuda.empty_cache()
+    log(f"{'shared-trunk' if shared else 'replicated'} stream: N={N}, {ms:.2f} ms per exact layer "
+        f"fwd+bwd ({attn_ms:.2f} ms attention kernels), {tflops:.0f} TFLOP/s")
     return {
+        "form": "shared trunk" if shared else "replicated trunk",
         "n_packed": N,
         "segments": st["n_segments"],
-        "causal_pairs": st["causal_pairs"],
+        "visible_pairs": st["causal_pairs"],
         "ms": round(ms, 3),
+        "attn_ms": round(attn_ms, 3),
         "useful_tflops": round(tflops, 2),
         "frac_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
         "kernels_ms": kt,
     }
+
+
+def time_naive_compressed(args, mv, synth, trajs, wl, dev):
+    """The Naive-Compressed baseline's attention (Section 3.3): each trajectory
+    scored once over its final compressed walk (the C tokens no edit removes),
+    plain causal, same heads; forward + backward."""
+    import torch
+    from paper_2609_00865_amd.synth import Trajectory
+    lens = []
+    for tr in trajs:
+        gone = set()
+        for e in tr.edits:
+            for b, x in e.evict:
+                gone.update(range(b, x))
+            for b, x in getattr(e, "restore", ()):
+                gone.difference_update(range(b, x))
+        lens.append(tr.end - tr.begin - len(gone))
+    comp, off = [], 0
+    for n in lens:
+        comp.append(Trajectory(off, off + n, ()))
+        off += n
+    m = mv.ViewMask(comp).upload(dev)
+    P = m.stats()["visible_pairs"]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(synth.tensor_seed("compressed", args.seed))
+    mk = lambda h: torch.randn((off, h, wl.head_dim), generator=gen, device="cuda").to(torch.bfloat16)
+    q, k, v, do = mk(wl.n_heads_q), mk(wl.n_heads_kv), mk(wl.n_heads_kv), mk(wl.n_heads_q)
+    ws = mv.attn_bwd_workspace(m, q, k)
+
+    def f():
+        o, lse = mv.attn_fwd(m, q, k, v)
+        mv.attn_bwd(m, q, k, v, o, do, lse, workspace=ws)
+
+    for _ in range(args.warmup):
+        f()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        f()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    del q, k, v, do, ws
+    torch.cuda.empty_cache()
+    log(f"naive-compressed: {off} tokens, {ms:.2f} ms attention fwd+bwd")
+    return {"tokens": off, "visible_pairs": P, "ms": round(ms, 3)}
 
 
 def time_attention(args, mv, synth, workload, seed, dev):
@@ -462,7 +519,11 @@ def main():
     sdcc = None if args.no_sdcc else time_sdcc(args, mv, synth, mask, wl, lmw, dev)
     del h, w, y, old, g, lp_ws, lpb_ws
     torch.cuda.empty_cache()
-    packed = None if args.no_packed else time_packed(args, mv, synth, trajs, wl, dev)
+    packed = shared = naive = None
+    if not args.no_packed:
+        packed = time_packed(args, mv, synth, trajs, wl, dev, shared=False)
+        shared = time_packed(args, mv, synth, trajs, wl, dev, shared=True)
+        naive = time_naive_compressed(args, mv, synth, trajs, wl, dev)
     others = []
     if not args.no_configs:
         del q, k, v, do, attn_ws
@@ -577,9 +638,25 @@ def main():
     if sdcc is not None:
         out["sdcc"] = sdcc
     if packed is not None:
-        packed["pairs_vs_union"] = round(packed["causal_pairs"] / P, 4)
-        packed["ms_vs_union_attention"] = round(packed["ms"] / attn_ms, 4)
+        for pk in (packed, shared):
+            pk["pairs_vs_union"] = round(pk["visible_pairs"] / P, 4)
+            pk["attn_ms_vs_union"] = round(pk["attn_ms"] / attn_ms, 4)
         out["branch_packed"] = packed
+        out["shared_trunk_packed"] = shared
+        nc = naive["ms"]
+        out["cost_ratios"] = {
+            "what": ("attention fwd+bwd of one layer over the 4 x 32K batch, each relative to "
+                     "the Naive-Compressed form (final compressed walk, plain causal)"),
+            "naive_compressed_ms": nc,
+            "naive_compressed_tokens": naive["tokens"],
+            "union_4d_mask": round(attn_ms / nc, 3),
+            "logittree_shared_trunk": round(shared["attn_ms"] / nc, 3),
+            "logittree_replicated_trunk": round(packed["attn_ms"] / nc, 3),
+            "paper_table_main_context": {"4D mask": 1.35, "LogitTree": 4.20,
+                                         "note": "whole training step multipliers over "
+                                                 "Naive-Compressed, Qwen3-4B, A100/H800-class; "
+                                                 "context, not this measurement"},
+        }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(trajs, wl, lmw, attn_useful, lm_useful)

@@ -223,11 +223,30 @@ typedef struct {
   int32_t n_packed;       /* packed slots N                                   */
   int32_t n_segments;     /* branch layers over all trajectories              */
   int32_t max_copies;     /* most copies of one physical token                */
-  int64_t causal_pairs;   /* sum over segments of l (l + 1) / 2               */
+  int64_t causal_pairs;   /* visible (row, key) pairs of the mask: for the
+                             replicated packing sum over segments of l (l+1)/2 */
 } mv_pack_stats;
 
 mv_status mv_build_branch_pack(const mv_trajectory* trajs, int32_t n_traj,
                                int32_t total_tokens, mv_branch_pack** out);
+
+/*
+ * LogitTree with shared-trunk KV (Section 4.1: the K+1 branch forwards, whose
+ * shared trunk is cached rather than replicated).  Consecutive branch
+ * sequences S_{k-1} and S_k agree on their first d_k tokens (up to the first
+ * token edit k removes), at the same positions, so those tokens' keys and
+ * values are the same at every layer.  Segment k of this packing holds only
+ * S_k[d_k:] (segment 0 all of S_0); its rows read the shared prefix from the
+ * slots of earlier segments.  The mask (mv_branch_pack_mask) gives every slot
+ * one lifetime: the record over the packed stream whose edit at the first
+ * slot of segment k evicts the slots holding S_{k-1}[d_k:].  pos is the
+ * token's index in its branch sequence (positions restart per branch), owner
+ * and target as above; causal_pairs holds the mask's visible pairs.  The
+ * result is exact through a stack of layers, like the replicated packing,
+ * with each shared prefix computed once.
+ */
+mv_status mv_build_shared_trunk_pack(const mv_trajectory* trajs, int32_t n_traj,
+                                     int32_t total_tokens, mv_branch_pack** out);
 mv_status mv_branch_pack_stats(const mv_branch_pack* p, mv_pack_stats* out);
 /* Host copies of the layout; every array is optional (null: skipped).
  * src, pos, target: int32 [n_packed]; owner: uint8 [n_packed];

@@ -27,6 +27,10 @@ Rotary embedding (reading: the rotate-half form with base theta, as the
 Qwen3 family uses): for i < d/2, f_i = theta^(-2i/d), a = pos * f_i,
   y_i = x_i cos a - x_{i+d/2} sin a,  y_{i+d/2} = x_{i+d/2} cos a + x_i sin a.
 
+Shared trunk (LogitTree with the trunk's keys and values cached, Section
+4.1): branch k stores only the suffix of S_k after the prefix it shares with
+S_{k-1}; its rows attend to that prefix where an earlier branch stored it.
+
 Toy model for the exactness check: n_layers of multi-head attention with RoPE
 on q and k and a residual, x <- x + Attn(x) Wo, no other sublayers.
 """
@@ -57,6 +61,54 @@ def branch_pack(trajs: Sequence) -> Dict[str, list]:
                 target.append(j + 1 if own and j + 1 < tr.end else -1)
             seg_begin.append(len(src))
     return {"src": src, "pos": pos, "owner": owner, "target": target, "seg_begin": seg_begin}
+
+
+def shared_trunk_pack(trajs: Sequence) -> Dict[str, list]:
+    """LogitTree with the shared trunk cached (Section 4.1): consecutive branch
+    sequences S_{k-1}, S_k agree on their first d_k tokens (the tokens before
+    the first one edit k removes), at the same positions; branch k stores only
+    S_k[d_k:] and reads its prefix from the slots of earlier branches.
+
+    Returns the layout of ``branch_pack`` plus ``views``: for every slot, the
+    slots holding S_k[0 .. pos] of its branch k (what its row attends to)."""
+    src: List[int] = []
+    pos: List[int] = []
+    owner: List[int] = []
+    target: List[int] = []
+    views: List[List[int]] = []
+    seg_begin: List[int] = [0]
+    for tr in trajs:
+        prev_seq: List[int] = []
+        prev_slots: List[int] = []
+        for k, (first, end, before) in enumerate(V.branch_layers(tr)):
+            seq = list(before) + list(range(first, end))
+            d = 0
+            if k > 0:
+                while d < min(len(seq), len(prev_seq)) and seq[d] == prev_seq[d]:
+                    d += 1
+            slots = prev_slots[:d]
+            for p in range(d, len(seq)):
+                j = seq[p]
+                slots.append(len(src))
+                src.append(j)
+                pos.append(p)
+                own = j >= first
+                owner.append(1 if own else 0)
+                target.append(j + 1 if own and j + 1 < tr.end else -1)
+                views.append(list(slots))
+            seg_begin.append(len(src))
+            prev_seq, prev_slots = seq, slots
+    return {"src": src, "pos": pos, "owner": owner, "target": target,
+            "seg_begin": seg_begin, "views": views}
+
+
+def views_mask(views: Sequence[Sequence[int]]) -> torch.Tensor:
+    """N x N: slot i sees slot j iff j is in views[i]."""
+    n = len(views)
+    M = torch.zeros(n, n, dtype=torch.bool)
+    for i, vs in enumerate(views):
+        M[i, list(vs)] = True
+    return M
 
 
 def block_causal_mask(seg_begin: Sequence[int]) -> torch.Tensor:
@@ -130,6 +182,21 @@ def toy_packed(trajs, x0, layers, n_heads, head_dim, theta) -> torch.Tensor:
     pk = branch_pack(trajs)
     x = x0.to(torch.float64)[pk["src"]]
     mask = block_causal_mask(pk["seg_begin"])
+    for prm in layers:
+        x = _attend(x, mask, pk["pos"], prm, n_heads, head_dim, theta)
+    out = torch.zeros(x0.shape, dtype=torch.float64)
+    own = torch.tensor(pk["owner"], dtype=torch.bool)
+    out[torch.tensor(pk["src"])[own]] = x[own]
+    return out
+
+
+def toy_shared_trunk(trajs, x0, layers, n_heads, head_dim, theta) -> torch.Tensor:
+    """The shared-trunk stream: each branch's new tokens gathered once, one
+    forward in which every slot attends to its branch prefix, owner rows
+    scattered back."""
+    pk = shared_trunk_pack(trajs)
+    x = x0.to(torch.float64)[pk["src"]]
+    mask = views_mask(pk["views"])
     for prm in layers:
         x = _attend(x, mask, pk["pos"], prm, n_heads, head_dim, theta)
     out = torch.zeros(x0.shape, dtype=torch.float64)

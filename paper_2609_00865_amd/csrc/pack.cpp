@@ -37,47 +37,97 @@ mv_status hip_ok(hipError_t e, const char* what) {
 
 }  // namespace
 
-extern "C" {
+namespace {
 
-mv_status mv_build_branch_pack(const mv_trajectory* trajs, int32_t n_traj, int32_t total_tokens,
-                               mv_branch_pack** out) {
+// Shared by both packings.  Replicated (shared = false): segment k holds the
+// whole branch sequence S_k = (keys live just before J_k, in physical order)
+// ++ (rows J_k .. J_{k+1}), under a block-diagonal causal mask.  Shared trunk
+// (shared = true): S_k begins with the d_k tokens it shares with S_{k-1} (the
+// tokens before the first one edit k removes, at the same positions, so
+// their keys and values are the same at every layer); segment k holds only
+// S_k[d_k:], and its rows read the shared prefix from the slots of earlier
+// segments.  That visibility is again one lifetime per slot: it is the record
+// over the packed stream whose edit at the start of segment k evicts the
+// slots holding S_{k-1}[d_k:].
+mv_status build_pack(const mv_trajectory* trajs, int32_t n_traj, int32_t total_tokens,
+                     bool shared, mv_branch_pack** out) {
   if (out == nullptr) return bad(MV_ERR_INVALID_ARG, "out is null");
   *out = nullptr;
   // validates the record and gives the key lifetimes
   mv_view_mask* live = nullptr;
   if (mv_status st = mv_build_view_mask(trajs, n_traj, total_tokens, &live); st != MV_OK)
     return st;
+  mv_branch_pack* p = nullptr;
   try {
-    auto* p = new mv_branch_pack();
+    p = new mv_branch_pack();
     p->T = total_tokens;
     p->seg_begin.push_back(0);
     int64_t pairs = 0;
+    // shared trunk: one record per trajectory over its packed slots
+    std::vector<mv_trajectory> rec;
+    std::vector<std::vector<mv_edit>> rec_edits;
+    std::vector<std::vector<mv_span>> rec_spans;
     for (int32_t t = 0; t < n_traj; ++t) {
       const mv_trajectory& tr = trajs[t];
       std::vector<int32_t> bounds{tr.begin};
       for (int32_t k = 0; k < tr.n_edits; ++k) bounds.push_back(tr.edits[k].junction);
       bounds.push_back(tr.end);
+      const int32_t traj_slot0 = int32_t(p->src.size());
+      std::vector<int32_t> prev_seq, prev_slots;   // S_{k-1} and the slots holding it
+      std::vector<std::pair<int32_t, std::vector<int32_t>>> evictions;   // (junction, slots)
       for (size_t k = 0; k + 1 < bounds.size(); ++k) {
         const int32_t first = bounds[k], end = bounds[k + 1];
-        int32_t p_in_seg = 0;
-        for (int32_t j = tr.begin; j < first; ++j) {
-          if (!live->visible(first, j)) continue;  // not in row `first`'s view
+        std::vector<int32_t> seq;
+        for (int32_t j = tr.begin; j < first; ++j)
+          if (live->visible(first, j)) seq.push_back(j);   // in row `first`'s view
+        const size_t n_before = seq.size();
+        for (int32_t r = first; r < end; ++r) seq.push_back(r);
+        size_t d = 0;   // common prefix with the previous branch
+        if (shared && k > 0)
+          while (d < prev_seq.size() && d < seq.size() && prev_seq[d] == seq[d]) ++d;
+        std::vector<int32_t> slots(prev_slots.begin(), prev_slots.begin() + d);
+        const int32_t seg0 = int32_t(p->src.size());
+        if (shared && k > 0 && d < prev_slots.size())
+          evictions.push_back({seg0, std::vector<int32_t>(prev_slots.begin() + d, prev_slots.end())});
+        for (size_t q = d; q < seq.size(); ++q) {
+          const int32_t j = seq[q];
+          slots.push_back(int32_t(p->src.size()));
           p->src.push_back(j);
-          p->pos.push_back(p_in_seg++);
-          p->owner.push_back(0);
-          p->target.push_back(-1);
+          p->pos.push_back(int32_t(q));
+          const bool own = q >= n_before;
+          p->owner.push_back(own ? 1 : 0);
+          p->target.push_back(own && j + 1 < tr.end ? j + 1 : -1);
         }
-        for (int32_t r = first; r < end; ++r) {
-          p->src.push_back(r);
-          p->pos.push_back(p_in_seg++);
-          p->owner.push_back(1);
-          p->target.push_back(r + 1 < tr.end ? r + 1 : -1);
-        }
-        pairs += int64_t(p_in_seg) * (p_in_seg + 1) / 2;
+        if (!shared) pairs += int64_t(seq.size()) * (int64_t(seq.size()) + 1) / 2;
         p->seg_begin.push_back(int32_t(p->src.size()));
+        prev_seq.swap(seq);
+        prev_slots.swap(slots);
+      }
+      if (shared) {
+        // the record of this trajectory's slots: each eviction as sorted spans
+        std::vector<mv_edit> edits;
+        for (auto& ev : evictions) {
+          std::vector<int32_t>& sl = ev.second;
+          std::sort(sl.begin(), sl.end());
+          rec_spans.emplace_back();
+          for (int32_t x : sl) {
+            if (!rec_spans.back().empty() && rec_spans.back().back().end == x)
+              rec_spans.back().back().end = x + 1;
+            else
+              rec_spans.back().push_back(mv_span{x, x + 1});
+          }
+          mv_edit e{};
+          e.junction = ev.first;
+          e.n_evict = int32_t(rec_spans.back().size());
+          e.summary = mv_span{0, 0};
+          edits.push_back(e);
+        }
+        rec_edits.push_back(std::move(edits));
+        rec.push_back(mv_trajectory{traj_slot0, int32_t(p->src.size()), 0, nullptr});
       }
     }
     mv_view_mask_free(live);
+    live = nullptr;
     if (p->src.size() > size_t(1) << 30) {
       delete p;
       return bad(MV_ERR_UNSUPPORTED, "packed stream longer than 2^30 slots");
@@ -94,12 +144,26 @@ mv_status mv_build_branch_pack(const mv_trajectory* trajs, int32_t n_traj, int32
     p->copy_slot.resize(p->N);
     std::vector<int32_t> fill(p->copy_ptr.begin(), p->copy_ptr.end() - 1);
     for (int32_t i = 0; i < p->N; ++i) p->copy_slot[fill[p->src[i]]++] = i;
-    // the block-diagonal causal mask: every segment a trajectory without edits
     const int32_t n_seg = int32_t(p->seg_begin.size()) - 1;
-    std::vector<mv_trajectory> segs(n_seg);
-    for (int32_t s = 0; s < n_seg; ++s)
-      segs[s] = mv_trajectory{p->seg_begin[s], p->seg_begin[s + 1], 0, nullptr};
-    if (mv_status st = mv_build_view_mask(segs.data(), n_seg, p->N, &p->mask); st != MV_OK) {
+    mv_status st = MV_OK;
+    if (shared) {
+      // (edit spans are attached only now: the span vectors no longer move)
+      size_t si = 0;
+      for (size_t t = 0; t < rec.size(); ++t) {
+        for (auto& e : rec_edits[t]) e.evict = rec_spans[si++].data();
+        rec[t].n_edits = int32_t(rec_edits[t].size());
+        rec[t].edits = rec_edits[t].data();
+      }
+      st = mv_build_view_mask(rec.data(), int32_t(rec.size()), p->N, &p->mask);
+      if (st == MV_OK) pairs = p->mask->stats.visible_pairs;
+    } else {
+      // the block-diagonal causal mask: every segment a trajectory without edits
+      std::vector<mv_trajectory> segs(n_seg);
+      for (int32_t s = 0; s < n_seg; ++s)
+        segs[s] = mv_trajectory{p->seg_begin[s], p->seg_begin[s + 1], 0, nullptr};
+      st = mv_build_view_mask(segs.data(), n_seg, p->N, &p->mask);
+    }
+    if (st != MV_OK) {
       delete p;
       return st;
     }
@@ -115,8 +179,23 @@ mv_status mv_build_branch_pack(const mv_trajectory* trajs, int32_t n_traj, int32
     return MV_OK;
   } catch (const std::exception& e) {
     mv_view_mask_free(live);
+    delete p;
     return bad(MV_ERR_INVALID_ARG, std::string("host allocation failed: ") + e.what());
   }
+}
+
+}  // namespace
+
+extern "C" {
+
+mv_status mv_build_branch_pack(const mv_trajectory* trajs, int32_t n_traj, int32_t total_tokens,
+                               mv_branch_pack** out) {
+  return build_pack(trajs, n_traj, total_tokens, false, out);
+}
+
+mv_status mv_build_shared_trunk_pack(const mv_trajectory* trajs, int32_t n_traj,
+                                     int32_t total_tokens, mv_branch_pack** out) {
+  return build_pack(trajs, n_traj, total_tokens, true, out);
 }
 
 mv_status mv_branch_pack_stats(const mv_branch_pack* p, mv_pack_stats* out) {

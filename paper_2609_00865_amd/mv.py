@@ -153,6 +153,8 @@ mv_ppo_clip_dlogp = _sig("mv_ppo_clip_dlogp", ctypes.c_int, _i32, _vp, _vp, _f32
                          _vp, _vp)
 mv_build_branch_pack = _sig("mv_build_branch_pack", ctypes.c_int, _P(TrajectoryC), _i32, _i32,
                             _P(_vp))
+mv_build_shared_trunk_pack = _sig("mv_build_shared_trunk_pack", ctypes.c_int, _P(TrajectoryC), _i32,
+                                  _i32, _P(_vp))
 mv_branch_pack_stats = _sig("mv_branch_pack_stats", ctypes.c_int, _vp, _P(PackStats))
 mv_branch_pack_layout = _sig("mv_branch_pack_layout", ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp)
 mv_branch_pack_mask = _sig("mv_branch_pack_mask", _vp, _vp)
@@ -190,6 +192,7 @@ EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_ma
             "mv_branch_pack_device_bytes", "mv_branch_pack_upload", "mv_branch_pack_free",
             "mv_pack_rows", "mv_unpack_rows_sum", "mv_rope", "mv_token_logprob_dweight",
             "mv_view_mask_intervals", "mv_token_logprob_bad_targets", "mv_attn_bwd_noalloc",
+            "mv_build_shared_trunk_pack",
             "mv_profile_enable", "mv_profile_read"]
 
 VIEW_LIVE, VIEW_FINAL = 0, 1
@@ -479,11 +482,13 @@ def ppo_clip_dlogp(ratio, adv, eps_low=0.2, eps_high=0.2, scale=1.0, stream=None
 class BranchPack:
     """Owns a libmv branch packing built from trajectories."""
 
-    def __init__(self, trajectories: Sequence, total_tokens: Optional[int] = None):
+    def __init__(self, trajectories: Sequence, total_tokens: Optional[int] = None,
+                 shared_trunk: bool = False):
         trajs, keep = _trajectories_c(trajectories)
         T = total_tokens if total_tokens is not None else int(trajectories[-1].end)
         handle = ctypes.c_void_p()
-        check(mv_build_branch_pack(trajs, len(trajectories), T, ctypes.byref(handle)))
+        build = mv_build_shared_trunk_pack if shared_trunk else mv_build_branch_pack
+        check(build(trajs, len(trajectories), T, ctypes.byref(handle)))
         self._h = handle
         self.total_tokens = T
         st = self.stats()

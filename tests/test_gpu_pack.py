@@ -1,7 +1,9 @@
-"""GPU parity of the branch-replicated packing (gather, its adjoint, rotary
-embedding by per-segment positions) and of attention over the packed stream,
-against the oracle, through the C ABI; plus a two-layer model run on the
-packed stream against per-branch forwards of the whole stack.
+"""GPU parity of both packings of the branch layers (replicated trunk, and
+shared trunk: each branch stores only what it does not share with the one
+before it) -- gather, its adjoint, rotary embedding by per-branch positions,
+attention over the packed stream -- against the oracle, through the C ABI;
+plus a two-layer model run on each packed stream against per-branch forwards
+of the whole stack.
 
 Gates: the gather is bit-exact; fp32 sums of the copies 1e-6 relative; bf16
 outputs as everywhere else (2e-2 + 2^-8 |ref| elementwise, 1e-2 relative
@@ -26,15 +28,27 @@ F64 = torch.float64
 BF = torch.bfloat16
 
 
+def _pack(trajs, shared):
+    return mv.BranchPack(trajs, shared_trunk=shared).upload()
+
+
+def _layout(trajs, shared):
+    return OP.shared_trunk_pack(trajs) if shared else OP.branch_pack(trajs)
+
+
+SHARED = pytest.mark.parametrize("shared", [False, True], ids=["replicated", "shared_trunk"])
+
+
 def _records(seed, lens=(300, 257, 180)):
     rng = np.random.default_rng(seed)
     return synth.random_trajectories(rng, list(lens), max_edits=6, max_span=40, summary_max=12)
 
 
-def test_pack_and_unpack():
+@SHARED
+def test_pack_and_unpack(shared):
     trajs = _records(1)
-    pk = mv.BranchPack(trajs).upload()
-    lay = OP.branch_pack(trajs)
+    pk = _pack(trajs, shared)
+    lay = _layout(trajs, shared)
     T, N = trajs[-1].end, pk.n_packed
     print(f"[gpu] pack rows T={T} N={N}", flush=True)
     gen = torch.Generator().manual_seed(3)
@@ -51,11 +65,12 @@ def test_pack_and_unpack():
     assert_bf16_close(s16, ref, "unpack bf16")
 
 
+@SHARED
 @pytest.mark.parametrize("d,theta", [(64, 1e4), (128, 1e6)])
-def test_rope(d, theta):
+def test_rope(d, theta, shared):
     trajs = _records(2, lens=(900, 400))
-    pk = mv.BranchPack(trajs).upload()
-    lay = OP.branch_pack(trajs)
+    pk = _pack(trajs, shared)
+    lay = _layout(trajs, shared)
     N = pk.n_packed
     print(f"[gpu] rope N={N} d={d}", flush=True)
     gen = torch.Generator().manual_seed(4)
@@ -73,14 +88,19 @@ def test_rope(d, theta):
     assert_bf16_close(back, x.double(), "rope round trip")
 
 
-def test_packed_attention_forward_backward():
+@SHARED
+@pytest.mark.parametrize("workload", ["tiny", "medium"])
+def test_packed_attention_forward_backward(shared, workload):
     """One layer over the packed stream: owner rows give every row's view
-    output; the copies' gradients summed back give the per-branch dK, dV."""
-    trajs = synth.make_trajectories("tiny", 0)
-    q, k, v, do = synth.make_attn_tensors("tiny", 0)
-    q = q.repeat(1, 2, 1).contiguous()
-    do = do.repeat(1, 2, 1).contiguous()
-    pk = mv.BranchPack(trajs).upload()
+    output; the copies' gradients summed back give the per-branch dK, dV
+    (with the shared trunk a trunk slot gathers the gradients of every branch
+    that reads it)."""
+    trajs = synth.make_trajectories(workload, 0)
+    q, k, v, do = synth.make_attn_tensors(workload, 0)
+    if workload == "tiny":
+        q = q.repeat(1, 2, 1).contiguous()
+        do = do.repeat(1, 2, 1).contiguous()
+    pk = _pack(trajs, shared)
     lay = pk.layout()
     own = lay["owner"].bool()
     print(f"[gpu] packed attention T={q.shape[0]} N={pk.n_packed}", flush=True)
@@ -92,7 +112,8 @@ def test_packed_attention_forward_backward():
     dK = mv.unpack_rows_sum(pk, dk, out_fp32=True).cpu()
     dV = mv.unpack_rows_sum(pk, dv, out_fp32=True).cpu()
     torch.cuda.synchronize()
-    O, L, dQ, rdK, rdV = OA.logittree(trajs, q.to(F64), k.to(F64), v.to(F64), dout=do.to(F64))
+    O, L, dQ, rdK, rdV = OA.logittree(trajs, q.to(F64), k.to(F64), v.to(F64), dout=do.to(F64),
+                                      row_chunk=1024)
     src = lay["src"].long()
     o_own = torch.zeros_like(O)
     o_own[src[own]] = o.cpu()[own].double()
@@ -105,7 +126,8 @@ def test_packed_attention_forward_backward():
     assert_bf16_close(dV, rdV, "packed dV summed over copies")
 
 
-def test_packed_attention_with_re_entering_keys():
+@SHARED
+def test_packed_attention_with_re_entering_keys(shared):
     """Packing a record whose keys leave and re-enter: every layer's segment
     copies the keys live at its start (restored ones at their own slots)."""
     rng = np.random.default_rng(41)
@@ -115,7 +137,7 @@ def test_packed_attention_with_re_entering_keys():
     gen = torch.Generator().manual_seed(41)
     q = torch.randn(T, 2, 64, generator=gen).to(BF)
     k, v = (torch.randn(T, 1, 64, generator=gen).to(BF) for _ in range(2))
-    pk = mv.BranchPack(trajs).upload()
+    pk = _pack(trajs, shared)
     lay = pk.layout()
     own = lay["owner"].bool()
     print(f"[gpu] packed attention with restores T={T} N={pk.n_packed}", flush=True)
@@ -131,7 +153,8 @@ def _bf(x):
     return x.to(BF)
 
 
-def test_two_layer_model_on_the_packed_stream():
+@SHARED
+def test_two_layer_model_on_the_packed_stream(shared):
     trajs = synth.make_trajectories("tiny", 1)
     T = trajs[-1].end
     W, H, d, theta, n_layers = 128, 2, 64, 1e4, 2
@@ -141,8 +164,8 @@ def test_two_layer_model_on_the_packed_stream():
     x0 = _bf(torch.randn(T, W, generator=gen)).double()
     ref = OP.toy_logittree(trajs, x0, layers, H, d, theta)
     uni = OP.toy_union(trajs, x0, layers, H, d, theta)
-    pk = mv.BranchPack(trajs).upload()
-    print(f"[gpu] two-layer model T={T} N={pk.n_packed}", flush=True)
+    pk = _pack(trajs, shared)
+    print(f"[gpu] two-layer model T={T} N={pk.n_packed} shared={shared}", flush=True)
     x = mv.pack_rows(pk, _bf(x0).cuda())
     for prm in layers:
         w = {n: t.float().cuda() for n, t in prm.items()}

@@ -146,3 +146,99 @@ def test_unpack_is_the_adjoint_of_the_gather():
     lhs = (x[pk["src"]] * g).sum()
     rhs = (x * OP.unpack_sum(pk, g, T)).sum()
     assert abs(float(lhs - rhs)) < 1e-10
+
+
+def test_shared_trunk_running_example():
+    """Hand-derived from Table "running-prefixes": branch 1 (rows y8..y10)
+    shares s, y1..y4 with branch 0 and stores y6 again (its position moves
+    from 6 to 5 once y5 is evicted), then its rows; branch 2 shares up to y7
+    and stores y10 again; branch 3 shares up to y10."""
+    fix = load("running_example.json")
+    traj, pos = trajectory_from(fix)
+    names = {i: n for n, i in pos.items()}
+    pk = OP.shared_trunk_pack([traj])
+    assert pk["seg_begin"] == [0, 7, 11, 14, 16]
+    assert pk["src"] == [0, 1, 2, 3, 4, 5, 6, 6, 7, 8, 9, 9, 10, 11, 12, 13]
+    assert pk["pos"] == [0, 1, 2, 3, 4, 5, 6, 5, 6, 7, 8, 7, 8, 9, 9, 10]
+    assert pk["owner"] == [1] * 7 + [0, 1, 1, 1, 0, 1, 1, 1, 1]
+    for e in fix["leaves"]:
+        r = pos[e["leaf"]] - 1
+        slot = [i for i in range(16) if pk["src"][i] == r and pk["owner"][i]]
+        assert len(slot) == 1
+        seen = [names[pk["src"][j]] for j in pk["views"][slot[0]] if pk["src"][j] != pos["s"]]
+        assert seen == e["live"]
+        assert pk["pos"][slot[0]] == len(e["live"])
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_shared_trunk_views(seed):
+    """Every slot's view is its branch prefix; owner slots see exactly their
+    row's view at its gap-free position; each branch stores only what its
+    predecessor does not share, so the stream is no longer than the
+    replicated one and each segment starts where the branches diverge."""
+    rng = np.random.default_rng(7000 + seed)
+    lens = [int(x) for x in rng.integers(1, 200, size=int(rng.integers(1, 4)))]
+    trajs = synth.random_trajectories(rng, lens, max_edits=6, max_span=30, summary_max=8,
+                                      restore_max=12 if seed % 2 else 0)
+    T = trajs[-1].end
+    pk = OP.shared_trunk_pack(trajs)
+    rep = OP.branch_pack(trajs)
+    N = pk["seg_begin"][-1]
+    assert T <= N <= rep["seg_begin"][-1]
+    own = [s for s, o in zip(pk["src"], pk["owner"]) if o]
+    assert sorted(own) == list(range(T))
+    M = OA.visibility(trajs)
+    sizes = {r: s for tr in trajs for r, s in zip(range(tr.begin, tr.end), V.view_sizes(tr))}
+    for i in range(N):
+        view_src = [pk["src"][j] for j in pk["views"][i]]
+        assert len(view_src) == pk["pos"][i] + 1
+        assert view_src[-1] == pk["src"][i] and pk["views"][i][-1] == i
+        if pk["owner"][i]:
+            r = pk["src"][i]
+            seen = torch.zeros(T, dtype=torch.bool)
+            seen[view_src] = True
+            assert torch.equal(seen, M[r])
+            assert pk["pos"][i] == sizes[r] - 1
+    # segment k begins where S_k leaves S_{k-1}: at position d_k, with the
+    # token S_k[d_k], and its length is |S_k| - d_k
+    seg = 0
+    for tr in trajs:
+        seqs = [list(b) + list(range(f, e)) for f, e, b in V.branch_layers(tr)]
+        for k, sq in enumerate(seqs):
+            d = 0
+            if k > 0:
+                prev = seqs[k - 1]
+                while d < min(len(sq), len(prev)) and sq[d] == prev[d]:
+                    d += 1
+            b, e = pk["seg_begin"][seg], pk["seg_begin"][seg + 1]
+            assert pk["pos"][b] == d and pk["src"][b] == sq[d] and e - b == len(sq) - d
+            seg += 1
+    assert seg == len(pk["seg_begin"]) - 1
+
+
+@pytest.mark.parametrize("n_layers", [1, 2, 3])
+def test_shared_trunk_stream_is_exact_over_layers(n_layers):
+    traj, _ = trajectory_from(load("running_example.json"))
+    rng = np.random.default_rng(8)
+    extra = synth.random_trajectories(rng, [90], max_edits=4, max_span=12)[0]
+    trajs = [traj, synth.Trajectory(14, 14 + 90, tuple(
+        synth.Edit(e.junction + 14, tuple((b + 14, x + 14) for b, x in e.evict),
+                   (e.summary[0] + 14, e.summary[1] + 14)) for e in extra.edits))]
+    T = trajs[-1].end
+    W, H = 16, 2
+    layers, d = _toy(10 + n_layers, W, H, n_layers)
+    x0 = torch.randn(T, W, generator=torch.Generator().manual_seed(3), dtype=F64)
+    for theta in (1e4, 0.0):
+        ref = OP.toy_logittree(trajs, x0, layers, H, d, theta)
+        got = OP.toy_shared_trunk(trajs, x0, layers, H, d, theta)
+        assert torch.allclose(got, ref, atol=1e-10)
+    # a planted mistake: sharing one token past the divergence point must fail
+    pk = OP.shared_trunk_pack(trajs)
+    bad_views = [list(v) for v in pk["views"]]
+    moved = 0
+    for i in range(len(bad_views)):
+        if not pk["owner"][i] and len(bad_views[i]) > 1:
+            bad_views[i] = bad_views[i][:-2] + bad_views[i][-1:]   # drop the previous slot
+            moved += 1
+    assert moved > 0
+    assert not torch.equal(OP.views_mask(bad_views), OP.views_mask(pk["views"]))

@@ -73,3 +73,39 @@ def test_errors_without_gpu():
     n = mv.mv_branch_pack_device_bytes(pk.handle)
     st = mv.mv_branch_pack_upload(pk.handle, fake, n - 1, None)
     assert mv.mv_status_string(st).decode() == "MV_ERR_WORKSPACE"
+
+
+def _check_shared(trajs):
+    pk = mv.BranchPack(trajs, shared_trunk=True)
+    want = OP.shared_trunk_pack(trajs)
+    got = pk.layout()
+    for k in ("src", "pos", "owner", "target", "seg_begin"):
+        assert got[k].tolist() == want[k], k
+    N = want["seg_begin"][-1]
+    st = pk.stats()
+    assert st["n_packed"] == N
+    bits = mv.unpack_bits(pk.mask.materialize_host(0, N), N)
+    ref = OP.views_mask(want["views"])
+    assert torch.equal(bits, ref)
+    assert st["causal_pairs"] == int(ref.sum())
+    return pk
+
+
+def test_shared_trunk_running_example():
+    traj, _ = trajectory_from(load("running_example.json"))
+    pk = _check_shared([traj])
+    assert pk.n_packed == 16 and pk.n_segments == 4
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_shared_trunk_random_records(seed):
+    rng = np.random.default_rng(6000 + seed)
+    lens = [int(x) for x in rng.integers(1, 400, size=int(rng.integers(1, 4)))]
+    _check_shared(synth.random_trajectories(rng, lens, max_edits=8, max_span=40, summary_max=10,
+                                            restore_max=25 if seed % 3 == 0 else 0))
+
+
+def test_shared_trunk_without_edits_is_the_physical_stream():
+    trajs = [synth.Trajectory(0, 50, ()), synth.Trajectory(50, 51, ())]
+    pk = _check_shared(trajs)
+    assert pk.layout()["src"].tolist() == list(range(51))
