@@ -244,61 +244,140 @@ def time_dweight(args, mv, h, w, ws):
             "frac_peak": round(tflops / PEAK_BF16_TFLOPS, 4)}
 
 
+def time_grpo(args, mv, synth, h, w, y, old):
+    """The forward with the GRPO loss and drift statistics fused into the
+    log-prob's combine pass, against the log-prob forward followed by the
+    stand-alone GRPO pass, on the step's LM-head inputs laid out as the
+    recipe's groups (64 trajectories of 512 tokens, groups of 16)."""
+    import torch
+    T = h.shape[0]
+    lengths = [512] * (T // 512)
+    ptr, r, _, _, _, mask = synth.make_grpo_inputs(lengths, args.seed)
+    gen = torch.Generator(device="cuda").manual_seed(synth.tensor_seed("grpo", args.seed))
+    ref = old + 0.05 * torch.randn(T, generator=gen, device="cuda")
+    pd, rd, md = ptr.cuda(), r.cuda(), mask.cuda()
+    ws = mv.token_logprob_grpo_workspace(h, w, len(lengths), 16)
+    lp_ws = mv.token_logprob_workspace(h, w)
+    gr_ws = None
+
+    def fused():
+        return mv.token_logprob_grpo(h, w, y, old, pd, rd, ref, md, group_size=16, beta=0.001,
+                                     workspace=ws)
+
+    def two_calls():
+        logp, ratio, clipped, lse = mv.token_logprob(h, w, y, old, 0.2, 0.28, workspace=lp_ws)
+        return mv.grpo_loss(pd, rd, logp, old, ref, md, group_size=16, beta=0.001,
+                            workspace=gr_ws)
+
+    def run(fn, tail):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        mv.profile_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        kt = {}
+        for name in ("lm_logits", "lm_combine") + tail:
+            tot, cnt = mv.profile_read(name)
+            if cnt:
+                kt[name] = round(tot / args.steps, 4)
+        mv.profile_enable(False)
+        return e0.elapsed_time(e1) / args.steps, kt
+
+    ms_f, kt_f = run(fused, ("grpo_prep", "grpo_finish"))
+    ms_2, kt_2 = run(two_calls, ("grpo",))
+    post_f = sum(v for n, v in kt_f.items() if n != "lm_logits")
+    post_2 = sum(v for n, v in kt_2.items() if n != "lm_logits")
+    del ws, lp_ws
+    log(f"log-prob + GRPO forward: fused {ms_f:.3f} ms, two calls {ms_2:.3f} ms "
+        f"(after the logits GEMM: {post_f:.3f} vs {post_2:.3f} ms)")
+    return {"fused_ms": round(ms_f, 3), "two_calls_ms": round(ms_2, 3),
+            "fused_kernels_ms": kt_f, "two_calls_kernels_ms": kt_2,
+            "after_gemm_ms": {"fused": round(post_f, 4), "two_calls": round(post_2, 4)}}
+
+
 def time_packed(args, mv, synth, trajs, wl, dev, shared):
     """One exact attention layer on a packed stream of the same batch's branch
-    layers (the forms that stay exact through a stack of layers): rotary
-    embedding of Q and K by per-branch positions, attention forward and
-    backward under the stream's mask, the inverse rotation of dQ and dK.
-    shared = False: every branch replicates its trunk (LogitTree's branch
-    forwards); True: each branch stores only what it does not share with the
-    branch before it and reads the shared trunk's keys in place.  Timed on its
-    own after the step; useful FLOPs 14 d P Hq with P the stream's visible
-    pairs."""
+    layers (the forms that stay exact through a stack of layers), from the
+    physical tokens' Q, K, V to their gradients: Q and K gathered into the
+    stream and rotated by per-branch positions in one pass each, V gathered,
+    attention forward and backward under the stream's mask, dQ and dK rotated
+    back and summed over their copies in one pass each, dV summed.  The same
+    layer with separate rotary passes (gather, rotate; rotate back, sum) is
+    timed beside it.  shared = False: every branch replicates its trunk
+    (LogitTree's branch forwards); True: each branch stores only what it does
+    not share with the branch before it and reads the shared trunk's keys in
+    place.  Timed on its own after the step; useful FLOPs 14 d P Hq with P
+    the stream's visible pairs."""
     import torch
     pk = mv.BranchPack(trajs, shared_trunk=shared).upload(dev)
     st = pk.stats()
     N = st["n_packed"]
+    q, k, v, _ = synth.make_attn_tensors(ATTN_WORKLOAD, args.seed, device="cuda")
     gen = torch.Generator(device="cuda")
     gen.manual_seed(synth.tensor_seed("packed", args.seed))
-    mk = lambda h: torch.randn((N, h, wl.head_dim), generator=gen, device="cuda").to(torch.bfloat16)
-    q, k, v, do = mk(wl.n_heads_q), mk(wl.n_heads_kv), mk(wl.n_heads_kv), mk(wl.n_heads_q)
-    ws = mv.attn_bwd_workspace(pk.mask, q, k)
-    qr, kr = torch.empty_like(q), torch.empty_like(k)
+    do = torch.randn((N, wl.n_heads_q, wl.head_dim), generator=gen, device="cuda").to(torch.bfloat16)
+    ws = mv.attn_bwd_workspace(pk.mask, do, torch.empty((N, wl.n_heads_kv, wl.head_dim),
+                                                        dtype=torch.bfloat16, device="cuda"))
+    theta = 1e6
 
-    def layer():
-        mv.rope(pk, q, 1e6, out=qr)
-        mv.rope(pk, k, 1e6, out=kr)
-        o, lse = mv.attn_fwd(pk.mask, qr, kr, v)
-        dq, dk, dv = mv.attn_bwd(pk.mask, qr, kr, v, o, do, lse, workspace=ws)
-        mv.rope(pk, dq, 1e6, inverse=True, out=dq)
-        mv.rope(pk, dk, 1e6, inverse=True, out=dk)
+    def layer_fused():
+        qr, kr = mv.pack_rows_rope(pk, q, theta), mv.pack_rows_rope(pk, k, theta)
+        vp = mv.pack_rows(pk, v)
+        o, lse = mv.attn_fwd(pk.mask, qr, kr, vp)
+        dq, dk, dv = mv.attn_bwd(pk.mask, qr, kr, vp, o, do, lse, workspace=ws)
+        return (mv.unpack_rows_sum_rope(pk, dq, theta), mv.unpack_rows_sum_rope(pk, dk, theta),
+                mv.unpack_rows_sum(pk, dv))
 
-    for _ in range(args.warmup):
-        layer()
-    torch.cuda.synchronize()
-    mv.profile_enable(True)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    stream = torch.cuda.current_stream()
-    e0.record(stream)
-    for _ in range(args.steps):
-        layer()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
-    kt = {}
-    for name in ("rope", "attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce",
-                 "attn_bwd_dq"):
-        tot, cnt = mv.profile_read(name)
-        if cnt:
-            kt[name] = round(tot / cnt, 3)
-    mv.profile_enable(False)
-    attn_ms = sum(x for n, x in kt.items() if n != "rope")
+    def layer_separate():
+        qr = mv.rope(pk, mv.pack_rows(pk, q), theta)
+        kr = mv.rope(pk, mv.pack_rows(pk, k), theta)
+        vp = mv.pack_rows(pk, v)
+        o, lse = mv.attn_fwd(pk.mask, qr, kr, vp)
+        dq, dk, dv = mv.attn_bwd(pk.mask, qr, kr, vp, o, do, lse, workspace=ws)
+        mv.rope(pk, dq, theta, inverse=True, out=dq)
+        mv.rope(pk, dk, theta, inverse=True, out=dk)
+        return (mv.unpack_rows_sum(pk, dq), mv.unpack_rows_sum(pk, dk),
+                mv.unpack_rows_sum(pk, dv))
+
+    names = ("pack", "pack_rope", "rope", "attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv",
+             "attn_bwd_reduce", "attn_bwd_dq", "unpack", "unpack_rope")
+
+    def run(layer):
+        for _ in range(args.warmup):
+            layer()
+        torch.cuda.synchronize()
+        mv.profile_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        stream = torch.cuda.current_stream()
+        e0.record(stream)
+        for _ in range(args.steps):
+            layer()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        kt = {}
+        for name in names:
+            tot, cnt = mv.profile_read(name)
+            if cnt:
+                kt[name] = round(tot / args.steps, 3)   # per layer (some run 2-3 times)
+        mv.profile_enable(False)
+        return ms, kt
+
+    ms, kt = run(layer_fused)
+    ms_sep, kt_sep = run(layer_separate)
+    attn_ms = sum(x for n, x in kt.items() if n.startswith("attn"))
     useful = 14.0 * wl.head_dim * st["causal_pairs"] * wl.n_heads_q
     tflops = useful / (ms * 1e-3) / 1e12
-    del q, k, v, do, ws, qr, kr
+    del q, k, v, do, ws
     torch.cuda.empty_cache()
     log(f"{'shared-trunk' if shared else 'replicated'} stream: N={N}, {ms:.2f} ms per exact layer "
-        f"fwd+bwd ({attn_ms:.2f} ms attention kernels), {tflops:.0f} TFLOP/s")
+        f"fwd+bwd incl. gathers ({attn_ms:.2f} ms attention kernels; {ms_sep:.2f} ms with "
+        f"separate rotary passes), {tflops:.0f} TFLOP/s")
     return {
         "form": "shared trunk" if shared else "replicated trunk",
         "n_packed": N,
@@ -308,7 +387,8 @@ def time_packed(args, mv, synth, trajs, wl, dev, shared):
         "attn_ms": round(attn_ms, 3),
         "useful_tflops": round(tflops, 2),
         "frac_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
-        "kernels_ms": kt,
+        "kernels_ms_per_layer": kt,
+        "separate_rope": {"ms": round(ms_sep, 3), "kernels_ms_per_layer": kt_sep},
     }
 
 
@@ -516,6 +596,7 @@ def main():
     log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step (host wall {wall_ms:.2f}), "
         f"attention {attn_ms:.2f} ms")
     dweight = time_dweight(args, mv, h, w, lpb_ws)
+    grpo = time_grpo(args, mv, synth, h, w, y, old)
     sdcc = None if args.no_sdcc else time_sdcc(args, mv, synth, mask, wl, lmw, dev)
     del h, w, y, old, g, lp_ws, lpb_ws
     torch.cuda.empty_cache()
@@ -618,6 +699,7 @@ def main():
             "frac_peak": round(lm_useful / (lm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
             "tokens_per_s": round(T_lm / (lm_ms * 1e-3), 1),
             "dweight": dweight,
+            "grpo_fused_forward": grpo,
         },
         "step": {
             "ms": round(ms_per_step, 3),

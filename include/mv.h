@@ -283,6 +283,25 @@ mv_status mv_unpack_rows_sum(const mv_branch_pack* p, const void* in, int32_t wi
 mv_status mv_rope(const mv_branch_pack* p, const void* x, int32_t n_heads, int32_t head_dim,
                   float theta, int32_t direction, void* out, hipStream_t stream);
 
+/* The gather with the rotary embedding fused into it (Appendix G: each
+ * branch's positions restart from its own prefix): out[slot] =
+ * R(pos[slot]) in[src[slot]], in bf16 [total_tokens, n_heads, head_dim], out
+ * bf16 [n_packed, n_heads, head_dim]; one pass instead of mv_pack_rows then
+ * mv_rope.  Angles in fp64 (reduced to [-pi, pi] there), their cosine and
+ * sine and the rotation in fp32, one rounding to bf16.  head_dim a multiple
+ * of 16, <= 256; out must not alias in. */
+mv_status mv_pack_rows_rope(const mv_branch_pack* p, const void* in, int32_t n_heads,
+                            int32_t head_dim, float theta, void* out, hipStream_t stream);
+/* The adjoint of mv_pack_rows_rope: out[t] = sum over the copies of token t,
+ * in increasing slot order, of R(pos[slot])^T in[slot] (the inverse rotation
+ * of each copy's gradient, summed in fp32, rounded once), stored as bf16
+ * (out_fp32 == 0) or fp32 [total_tokens, n_heads, head_dim]; one pass instead
+ * of mv_rope (direction -1) then mv_unpack_rows_sum.  Deterministic.
+ * head_dim a multiple of 16, <= 256; out must not alias in. */
+mv_status mv_unpack_rows_sum_rope(const mv_branch_pack* p, const void* in, int32_t n_heads,
+                                  int32_t head_dim, float theta, int32_t out_fp32, void* out,
+                                  hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * View-masked attention (Section 4.2, the packed single forward; its
  * equivalence with one causal forward per branch is Theorem "hard_equiv",
@@ -471,6 +490,36 @@ mv_status mv_grpo_loss(const mv_grpo_shape* shape, const int32_t* traj_ptr, cons
                        const uint8_t* loss_mask, float* advantage, float* dlogp,
                        mv_grpo_stats* stats, void* workspace, size_t workspace_bytes,
                        hipStream_t stream);
+
+/*
+ * mv_token_logprob and mv_grpo_loss in one forward: the GRPO loss terms, the
+ * gradient dlogp and the drift statistics are evaluated in the log-prob's
+ * combine pass, from its own logp, with no per-token array read back.
+ * Outputs as the two calls give them (logp, ratio, clipped, lse as
+ * mv_token_logprob with logp_old; advantage, dlogp, stats as mv_grpo_loss on
+ * that logp): logp, ratio, clipped, lse, advantage and dlogp are bit-identical
+ * to theirs; the statistics agree up to the order of their fp32 partial sums
+ * (per 4 tokens here), fixed, so still bitwise reproducible.  dlogp is ready
+ * for mv_token_logprob_bwd.  shape->eps_* clip the ratio output, grpo->eps_*
+ * the loss (normally the same pair); grpo->n_tokens must equal
+ * shape->n_tokens.  logp_old, logp, ratio, clipped, lse and dlogp are
+ * required (n_tokens > 0); advantage and loss_mask may be null; logp_ref may
+ * be null only with beta == 0.  A token on the loss mask whose target is -1
+ * enters the loss with logp 0, as in the two-call form.  The workspace
+ * (device, >= mv_token_logprob_grpo_workspace_bytes) also serves
+ * mv_token_logprob_bad_targets.
+ */
+size_t mv_token_logprob_grpo_workspace_bytes(const mv_logprob_shape* shape,
+                                             const mv_grpo_shape* grpo);
+
+mv_status mv_token_logprob_grpo(const mv_logprob_shape* shape, const mv_grpo_shape* grpo,
+                                const void* hidden, const void* weight, const int32_t* target,
+                                const float* logp_old, const int32_t* traj_ptr,
+                                const float* reward, const float* logp_ref,
+                                const uint8_t* loss_mask, float* logp, float* ratio,
+                                float* clipped, float* lse, float* advantage, float* dlogp,
+                                mv_grpo_stats* stats, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * SDCC junction KL (Section 5.1, Eq. "soft_loss"; forward KL, teacher first).

@@ -80,6 +80,15 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
 hipError_t launch_logprob_dweight(int T, int H, int V, const void* hidden, const void* ws,
                                   float* dw, hipStream_t stream);
 int* logprob_status_word(const void* ws);
+size_t logprob_grpo_ws_bytes(int T, int H, int V, int n_traj);
+hipError_t launch_logprob_grpo(int T, int H, int V, float eps_lo, float eps_hi,
+                               const void* hidden, const void* weight, const int32_t* target,
+                               const float* logp_old, int n_traj, int G, float g_eps_lo,
+                               float g_eps_hi, float beta, float adv_eps, const int32_t* traj_ptr,
+                               const float* reward, const float* logp_ref, const uint8_t* mask,
+                               float* logp, float* ratio, float* clipped, float* lse,
+                               float* adv_out, float* dlogp, float* stats, void* ws,
+                               hipStream_t stream);
 size_t grpo_ws_bytes(int T, int n_traj);
 hipError_t launch_grpo(int T, int n_traj, int G, float eps_lo, float eps_hi, float beta,
                        float adv_eps, const int32_t* traj_ptr, const float* reward,
@@ -302,6 +311,50 @@ mv_status mv_token_logprob(const mv_logprob_shape* s, const void* hidden, const 
                                            s->eps_high, hidden, weight, target, logp_old, logp,
                                            ratio, clipped, lse, ws, stream),
                     "log-prob forward launch");
+}
+
+size_t mv_token_logprob_grpo_workspace_bytes(const mv_logprob_shape* s,
+                                             const mv_grpo_shape* g) {
+  if (check_logprob(s) != MV_OK || check_grpo(g) != MV_OK) return 0;
+  return mv::logprob_grpo_ws_bytes(s->n_tokens, s->hidden, s->vocab, g->n_traj);
+}
+
+mv_status mv_token_logprob_grpo(const mv_logprob_shape* s, const mv_grpo_shape* g,
+                                const void* hidden, const void* weight, const int32_t* target,
+                                const float* logp_old, const int32_t* traj_ptr,
+                                const float* reward, const float* logp_ref,
+                                const uint8_t* loss_mask, float* logp, float* ratio,
+                                float* clipped, float* lse, float* advantage, float* dlogp,
+                                mv_grpo_stats* stats, void* ws, size_t ws_bytes,
+                                hipStream_t stream) {
+  if (mv_status st = check_logprob(s); st != MV_OK) return st;
+  if (mv_status st = check_grpo(g); st != MV_OK) return st;
+  if (g->n_tokens != s->n_tokens)
+    return fail(MV_ERR_SHAPE, "the GRPO shape's n_tokens must equal the log-prob shape's");
+  if (traj_ptr == nullptr || reward == nullptr || stats == nullptr || ws == nullptr)
+    return fail(MV_ERR_INVALID_ARG, "traj_ptr, reward, stats and workspace are required");
+  if (s->n_tokens > 0) {
+    if (mv_status st = check_ptrs({hidden, weight}); st != MV_OK) return st;
+    if (target == nullptr || logp_old == nullptr || logp == nullptr || ratio == nullptr ||
+        clipped == nullptr || lse == nullptr || dlogp == nullptr)
+      return fail(MV_ERR_INVALID_ARG,
+                  "target, logp_old, logp, ratio, clipped, lse and dlogp are required");
+  }
+  if (logp_ref == nullptr && g->beta != 0.f)
+    return fail(MV_ERR_INVALID_ARG, "beta > 0 needs logp_ref");
+  const size_t need = mv::logprob_grpo_ws_bytes(s->n_tokens, s->hidden, s->vocab, g->n_traj);
+  if (ws_bytes < need) {
+    std::ostringstream os;
+    os << "log-prob GRPO workspace has " << ws_bytes << " bytes, needs " << need;
+    return fail(MV_ERR_WORKSPACE, os.str());
+  }
+  return hip_status(
+      mv::launch_logprob_grpo(s->n_tokens, s->hidden, s->vocab, s->eps_low, s->eps_high, hidden,
+                              weight, target, logp_old, g->n_traj, g->group_size, g->eps_low,
+                              g->eps_high, g->beta, g->adv_eps, traj_ptr, reward, logp_ref,
+                              loss_mask, logp, ratio, clipped, lse, advantage, dlogp,
+                              reinterpret_cast<float*>(stats), ws, stream),
+      "log-prob GRPO forward launch");
 }
 
 size_t mv_token_logprob_bwd_workspace_bytes(const mv_logprob_shape* s) {

@@ -158,6 +158,9 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
     const char* sV = reinterpret_cast<const char*>(sVbuf + buf * BK * D);
     const int* sOm = sOmbuf + buf * BK;
     const int j0 = kt * BK;
+    // only a partial tile holding a key with several live intervals (masks
+    // with restoring edits) walks the interval lists
+    const bool tile_iv = IV && !full && __any(sOm[lane] < 0);
 
     // the tile's two 32-key halves one after the other: S^T and dP^T of a
     // half, its dS^T, then its share of dQ^T (half the live accumulators)
@@ -176,7 +179,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       }
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
-      if (!full) {  // block-uniform; per element a select, not a branch
+      if (tile_iv) {
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           const int4 om = *reinterpret_cast<const int4*>(&sOm[kb * 32 + q4 * 8 + g * 4]);
@@ -185,8 +188,19 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
           for (int u = 0; u < 4; ++u) {
             const int r = q4 * 4 + u;
             const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
-            const bool vis = mv_visible_k<IV>(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv);
-            s[r] = vis ? s[r] : 0.f;
+            s[r] = mv_visible_iv(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv) ? s[r] : 0.f;
+          }
+        }
+      } else if (!full) {  // block-uniform; per element a select, not a branch
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int4 om = *reinterpret_cast<const int4*>(&sOm[kb * 32 + q4 * 8 + g * 4]);
+          const int omv[4] = {om.x, om.y, om.z, om.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int r = q4 * 4 + u;
+            const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
+            s[r] = mv_visible(qrow, key, omv[u]) ? s[r] : 0.f;
           }
         }
       }
@@ -501,7 +515,12 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   // the buffer step st-1 used (every wave finished with it before the last
   // barrier).
   bf16x8 pf[2], dsf[2];
-  if constexpr (IV) {
+  // Masks with restoring edits: only a key tile that holds a key with several
+  // live intervals takes the plain loop with the interval walk; every other
+  // tile runs the pipelined loop of single-interval masks.
+  bool iv_tile = false;
+  if constexpr (IV) iv_tile = __syncthreads_or(kok && om < 0) != 0;
+  if (iv_tile) {
     issue_step(0, 0);
     if (steps > 1) issue_step(1, 1);
     if (steps > 2) issue_step(2, 2);

@@ -122,20 +122,29 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     if (!(ent & 1)) {   // block-uniform; per element a select, not a branch
       const int j0 = (ent >> 1) * BK;
       const int* sOm = sOmbuf + (t & 3) * BK;
+      // a tile holding a key with several live intervals (only masks with
+      // restoring edits have them) takes the out-of-line interval walk
+      if (IV && __any(sOm[lane] < 0)) {
+        const uint32_t vis = mv_visible_iv_bits(qrow, j0, g, sOm, a.mask.iv_ptr, a.mask.iv);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const int4 om = *reinterpret_cast<const int4*>(&sOm[kb * 32 + q4 * 8 + g * 4]);
-          const int omv[4] = {om.x, om.y, om.z, om.w};
+          for (int r = 0; r < 16; ++r) s[kb][r] = (vis >> (kb * 16 + r)) & 1u ? s[kb][r] : -INFINITY;
+      } else {
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int r = q4 * 4 + u;
-            const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
-            const bool vis = mv_visible_k<IV>(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv);
-            s[kb][r] = vis ? s[kb][r] : -INFINITY;
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const int4 om = *reinterpret_cast<const int4*>(&sOm[kb * 32 + q4 * 8 + g * 4]);
+            const int omv[4] = {om.x, om.y, om.z, om.w};
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int r = q4 * 4 + u;
+              const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
+              s[kb][r] = mv_visible(qrow, key, omv[u]) ? s[kb][r] : -INFINITY;
+            }
           }
-        }
+      }
     }
   };
   // element i (0..31) of a tile: block i / 16, accumulator row i % 16

@@ -1,8 +1,10 @@
 // GRPO token loss, its gradient into the per-token log-probs, and the drift
-// diagnostics, on the outputs of the fused LM head.
+// diagnostics, on the outputs of the fused LM head (the same loss also runs
+// inside the LM head's combine pass: mv_token_logprob_grpo; both use the
+// per-token arithmetic of mv_grpo_dev.h).
 //
 // Four small launches (all HBM-trivial next to the LM-head GEMMs):
-//   1. group-normalised advantage per trajectory (one thread per group);
+//   1. group-normalised advantage per trajectory;
 //   2. per token: the trajectory by binary search of the packed offsets, the
 //      ratio, the clipped surrogate and its gradient, the k3 reference KL and
 //      the drift |logp - logp_old|; unnormalised gradient out, per-block
@@ -10,15 +12,14 @@
 //   3. one block sums the partials in block order (fp64) into the statistics;
 //   4. the gradient is scaled by 1 / (number of loss tokens).
 // Every reduction has a fixed order, so results are bitwise reproducible.
-#include "mv_device.h"
+#include "mv_grpo_dev.h"
 
 namespace mv {
 
 namespace {
 constexpr int kTok = 256;          // threads (= tokens) per block of the token pass
-// per-block partials: count, loss, |drift|, clip low, clip high, k3, ratio
 constexpr int kRatioPart = 6;
-constexpr int kNP = 7;
+constexpr int kNP = kGrpoParts;
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
 }  // namespace
 
@@ -31,24 +32,16 @@ struct GrpoArgs {
   const uint8_t* mask;       // null: every token carries loss
   float* adv;                // [n_traj]
   float* dlogp;              // [T]
-  float* part;               // [n_blocks][kNP]
+  float* part;               // [kNP][n_blocks] (counter-major)
   float* stats;              // 8 floats
   int T, n_traj, G;
   float eps_lo, eps_hi, beta, adv_eps;
 };
 
 __global__ __launch_bounds__(256) void grpo_adv_kernel(GrpoArgs a) {
-  const int grp = blockIdx.x * 256 + threadIdx.x;
-  if (grp * a.G >= a.n_traj) return;
-  const float* r = a.reward + size_t(grp) * a.G;
-  double mean = 0.0;
-  for (int i = 0; i < a.G; ++i) mean += r[i];
-  mean /= a.G;
-  double var = 0.0;
-  for (int i = 0; i < a.G; ++i) var += (r[i] - mean) * (r[i] - mean);
-  const double sd = a.G > 1 ? sqrt(var / (a.G - 1)) : 0.0;
-  for (int i = 0; i < a.G; ++i)
-    a.adv[size_t(grp) * a.G + i] = float((r[i] - mean) / (sd + a.adv_eps));
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= a.n_traj) return;
+  a.adv[i] = grpo_advantage(a.reward, a.G, i, a.adv_eps);
 }
 
 __global__ __launch_bounds__(kTok) void grpo_token_kernel(GrpoArgs a) {
@@ -56,41 +49,13 @@ __global__ __launch_bounds__(kTok) void grpo_token_kernel(GrpoArgs a) {
   const int t = blockIdx.x * kTok + threadIdx.x;
   float v[kNP] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (t < a.T) {
-    // last trajectory whose first token is <= t
-    int lo = 0, hi = a.n_traj - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (a.traj_ptr[mid] <= t)
-        lo = mid;
-      else
-        hi = mid - 1;
-    }
+    const int tr = grpo_traj_of(a.traj_ptr, a.n_traj, t);
     const bool on = a.mask == nullptr || a.mask[t] != 0;
     float g = 0.f;
-    if (on) {
-      const float A = a.adv[lo];
-      const float lp = a.logp[t], old = a.logp_old[t];
-      const float rho = expf(lp - old);
-      const float lo_e = 1.f - a.eps_lo, hi_e = 1.f + a.eps_hi;
-      const float clipped = fminf(fmaxf(rho, lo_e), hi_e);
-      const float u = rho * A, c = clipped * A;
-      const bool clip_active = c < u;
-      float k3 = 0.f, dk3 = 0.f;
-      if (a.logp_ref != nullptr) {
-        const float x = a.logp_ref[t] - lp;
-        const float em1 = expm1f(x);   // exp(x) - 1 without cancellation near x = 0
-        k3 = em1 - x;
-        dk3 = -em1;
-      }
-      g = (clip_active ? 0.f : -u) + a.beta * dk3;
-      v[0] = 1.f;
-      v[1] = -fminf(u, c) + a.beta * k3;
-      v[2] = fabsf(lp - old);
-      v[3] = (clip_active && rho < lo_e) ? 1.f : 0.f;
-      v[4] = (clip_active && rho > hi_e) ? 1.f : 0.f;
-      v[5] = k3;
-      v[kRatioPart] = rho;
-    }
+    if (on)
+      g = grpo_token_terms(a.logp[t], a.logp_old[t],
+                           a.logp_ref != nullptr ? a.logp_ref + t : nullptr, a.adv[tr], a.eps_lo,
+                           a.eps_hi, a.beta, v);
     a.dlogp[t] = g;
   }
 #pragma unroll
@@ -103,20 +68,36 @@ __global__ __launch_bounds__(kTok) void grpo_token_kernel(GrpoArgs a) {
     }
     __syncthreads();
   }
-  if (threadIdx.x < kNP) a.part[size_t(blockIdx.x) * kNP + threadIdx.x] = red[threadIdx.x][0];
+  if (threadIdx.x < kNP) a.part[size_t(threadIdx.x) * gridDim.x + blockIdx.x] = red[threadIdx.x][0];
 }
 
-__global__ __launch_bounds__(256) void grpo_finish_kernel(GrpoArgs a, int n_blocks) {
-  __shared__ double red[kNP + 1][256];
+// One block: the per-block partials (counter-major: counter k of block b at
+// part[k * stride + b]) summed in fp64, thread-strided (16-byte loads where
+// the rows allow them) then a fixed tree, into the statistics.
+constexpr int kFinish = 512;
+__global__ __launch_bounds__(kFinish) void grpo_finish_kernel(GrpoArgs a, int n_blocks,
+                                                              int stride) {
+  __shared__ double red[kNP + 1][kFinish];
   double v[kNP + 1] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int b = threadIdx.x; b < n_blocks; b += 256)
+  const bool vec = (stride & 3) == 0 && (reinterpret_cast<uintptr_t>(a.part) & 15) == 0;
+  const int n4 = vec ? n_blocks / 4 : 0;
 #pragma unroll
-    for (int k = 0; k < kNP; ++k) v[k] += a.part[size_t(b) * kNP + k];
-  for (int i = threadIdx.x; i < a.n_traj; i += 256) v[kNP] += fabs(double(a.adv[i]));
+  for (int k = 0; k < kNP; ++k) {
+    const float* row = a.part + size_t(k) * stride;
+    for (int b = threadIdx.x; b < n4; b += kFinish) {
+      const float4 x = reinterpret_cast<const float4*>(row)[b];
+      v[k] += x.x;
+      v[k] += x.y;
+      v[k] += x.z;
+      v[k] += x.w;
+    }
+    for (int b = 4 * n4 + threadIdx.x; b < n_blocks; b += kFinish) v[k] += row[b];
+  }
+  for (int i = threadIdx.x; i < a.n_traj; i += kFinish) v[kNP] += fabs(double(a.adv[i]));
 #pragma unroll
   for (int k = 0; k <= kNP; ++k) red[k][threadIdx.x] = v[k];
   __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
+  for (int s = kFinish / 2; s > 0; s >>= 1) {
     if (threadIdx.x < s) {
 #pragma unroll
       for (int k = 0; k <= kNP; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + s];
@@ -176,13 +157,27 @@ hipError_t launch_grpo(int T, int n_traj, int G, float eps_lo, float eps_hi, flo
   a.beta = logp_ref != nullptr ? beta : 0.f;
   a.adv_eps = adv_eps;
   ProfScope prof("grpo", stream);
-  const int n_groups = n_traj / G;
-  hipLaunchKernelGGL(grpo_adv_kernel, dim3((n_groups + 255) / 256), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(grpo_adv_kernel, dim3((n_traj + 255) / 256), dim3(256), 0, stream, a);
   if (T > 0)
     hipLaunchKernelGGL(grpo_token_kernel, dim3(n_blocks), dim3(kTok), 0, stream, a);
-  hipLaunchKernelGGL(grpo_finish_kernel, dim3(1), dim3(256), 0, stream, a, n_blocks);
+  hipLaunchKernelGGL(grpo_finish_kernel, dim3(1), dim3(kFinish), 0, stream, a, n_blocks,
+                     n_blocks);
   if (T > 0)
     hipLaunchKernelGGL(grpo_scale_kernel, dim3((T + 255) / 256), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+// Statistics of the GRPO loss that the LM head's combine pass evaluated per
+// token (part: its per-block partials, counter k of block b at part[k *
+// stride + b]; adv: the advantages its preparation pass wrote).
+hipError_t launch_grpo_fused_finish(const float* part, int n_blocks, int stride, int n_traj,
+                                    const float* adv, float* stats, hipStream_t stream) {
+  GrpoArgs a{};
+  a.part = const_cast<float*>(part);
+  a.adv = const_cast<float*>(adv);
+  a.stats = stats;
+  a.n_traj = n_traj;
+  hipLaunchKernelGGL(grpo_finish_kernel, dim3(1), dim3(kFinish), 0, stream, a, n_blocks, stride);
   return hipGetLastError();
 }
 

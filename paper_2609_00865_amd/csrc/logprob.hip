@@ -2,10 +2,13 @@
 //
 // Forward: z = W h is produced 256 vocab rows x 256 tokens at a time by a bf16
 // MFMA tile engine and reduced in registers to a per-token (max, sum of exp)
-// over each wave's 128 vocab rows; the full logits are never stored.  The
-// target logit z_{t,y_t} comes from a per-token fp32 dot product, and a
-// combine pass merges the partials into logsumexp and writes logp, ratio and
-// the clipped ratio (the GRPO ratio of Appendix C, "Pitfall A, RL view").
+// over each wave's 128 vocab rows; the full logits are never stored.  A
+// combine pass (one wave per token) takes the target logit z_{t,y_t} as an
+// fp32 dot product, merges the partials into logsumexp and writes logp,
+// ratio and the clipped ratio (the GRPO ratio of Appendix C, "Pitfall A, RL
+// view"); its fused variant also evaluates the GRPO loss of each token and
+// its gradient, and reduces the drift statistics (Eq. "logdiff") in the same
+// pass.
 //
 // Backward: the logits tile is recomputed and turned into
 // G_tv = g_t (onehot(y_t)_v - softmax(z_t)_v), stored once in bf16 (the tile
@@ -30,7 +33,7 @@
 // XCD's L2.
 #include <algorithm>
 
-#include "mv_device.h"
+#include "mv_grpo_dev.h"
 
 namespace mv {
 
@@ -64,6 +67,9 @@ int vocab_pad(int V) { return (V + BA - 1) / BA * BA; }
 
 enum { kModeLogits = 0, kModeGrad = 1, kModeDh = 2, kModeKL = 3, kModeKLGrad = 4 };
 
+hipError_t launch_grpo_fused_finish(const float* part, int n_blocks, int stride, int n_traj,
+                                    const float* adv, float* stats, hipStream_t stream);
+
 struct LmArgs {
   const u16* h;       // [T, H]
   const u16* w;       // [V, H]
@@ -75,7 +81,6 @@ struct LmArgs {
   u16* Gout;          // [T, Vp] (grad modes)
   u16* dh;            // [T, H] (dH mode)
   float2* part;       // [T, n_chunks] (logits mode)
-  float* tlogit;      // [T] (target pass)
   // KL modes: token row 2i is leaf i's teacher row, 2i + 1 its student row
   const u16* zero_row; // [H] zeros: the row read for an out-of-range leaf row index
   const u16* hT;      // teacher hidden states [*, H]
@@ -556,26 +561,10 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void lm_dw_kernel(LmArgs a) {
   }
 }
 
-// Target logit z_{t,y_t} = h_t . W[y_t] in fp32, one wave per token.  Forward
-// (BWD = false): stored for the combine pass (0 for a token without loss).
-// Backward: rewrites G[t][y_t], which the grad tile left at -g_t p, to
-// g_t (1 - p) with p = softmax(z_t)_{y_t} from the forward's lse.
-// An id outside [-1, V) is never used as an index: the token is treated as
-// one without loss and counted in *bad_targets (this kernel sees every token
-// exactly once per call).
-template <bool BWD>
-__global__ __launch_bounds__(256) void lm_target_kernel(LmArgs a) {
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (t >= a.T) return;
-  const int y = a.tgt[t];
-  if (uint32_t(y) >= uint32_t(a.V)) {
-    if (lane == 0) {
-      if (!BWD) a.tlogit[t] = 0.f;
-      if (y != -1) atomicAdd(a.bad_targets, 1);
-    }
-    return;
-  }
+// Target logit z_{t,y_t} = h_t . W[y_t] in fp32 by one wave (lane k takes
+// 16-byte chunks k, k + 64, ...; a fixed shuffle tree sums the lanes), so
+// that the forward's combine and the backward's fix-up see the same value.
+__device__ __forceinline__ float target_dot(const LmArgs& a, int t, int y, int lane) {
   const u16* hp = a.h + size_t(t) * a.H;
   const u16* wp = a.w + size_t(y) * a.H;
   float s = 0.f;
@@ -590,11 +579,25 @@ __global__ __launch_bounds__(256) void lm_target_kernel(LmArgs a) {
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
-  if (lane != 0) return;
-  if (!BWD) {
-    a.tlogit[t] = s;
+  return s;
+}
+
+// Backward fix-up, one wave per token: rewrites G[t][y_t], which the grad
+// tile left at -g_t p, to g_t (1 - p) with p = softmax(z_t)_{y_t} from the
+// forward's lse.  An id outside [-1, V) is never used as an index: the token
+// is treated as one without loss and counted in *bad_targets (this kernel
+// sees every token exactly once per call).
+__global__ __launch_bounds__(256) void lm_target_kernel(LmArgs a) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= a.T) return;
+  const int y = a.tgt[t];
+  if (uint32_t(y) >= uint32_t(a.V)) {
+    if (lane == 0 && y != -1) atomicAdd(a.bad_targets, 1);
     return;
   }
+  const float s = target_dot(a, t, y, lane);
+  if (lane != 0) return;
   const float p = fast_exp2(fmaf(s, kLog2e, -a.lse[t] * kLog2e));
   a.Gout[panel_index(t, y, a.Vp)] = u16(bf16_bits(a.g[t] * (1.f - p)));
 }
@@ -626,33 +629,103 @@ __global__ __launch_bounds__(256) void transpose_w_kernel(const u16* w, u16* wT,
   }
 }
 
-// Merge the per-chunk (max, sum) pairs of one token and finish the epilogue.
-__global__ __launch_bounds__(256) void lm_combine_kernel(LmArgs a, const float* logp_old,
-                                                         float* logp, float* ratio,
-                                                         float* clipped, float* lse, float eps_lo,
-                                                         float eps_hi) {
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (t >= a.T) return;
-  const float2* p = a.part + size_t(t) * a.n_chunks;
-  float m = -INFINITY;
-  for (int i = lane; i < a.n_chunks; i += 64) m = fmaxf(m, p[i].x);
+// Outputs of the forward's combine pass; the GRPO fields are used only by the
+// fused variant (mv_token_logprob_grpo).
+struct CombineOut {
+  const float* logp_old;
+  float* logp;
+  float* ratio;
+  float* clipped;
+  float* lse;
+  float eps_lo, eps_hi;
+  // GRPO loss fused into the pass
+  const int32_t* traj_ptr;
+  const float* reward;
+  const float* logp_ref;     // null: no reference KL
+  const uint8_t* mask;       // null: every token carries loss
+  const float* adv;          // [n_traj] advantages from the preparation pass
+  const int* n_loss_count;   // loss tokens counted by the preparation pass (mask given)
+  int n_loss_fixed;          // the count when there is no mask (-1 otherwise)
+  float* dlogp;
+  float* part;               // [kGrpoParts][part_stride] (one column per block)
+  int part_stride;
+  int n_traj, G;
+  float g_eps_lo, g_eps_hi, beta, adv_eps;
+};
+
+// One wave per token: the target logit, the merge of the per-chunk (max,
+// sum) pairs into logsumexp, and the epilogue (logp, ratio, clip).  An id
+// outside [-1, V) is never used as an index: the token is treated as one
+// without loss and counted in *bad_targets.  GRPO: the wave finds the
+// token's trajectory, lane 0 evaluates the token's loss terms and its
+// gradient (already divided by the number of loss tokens), and the block's
+// four tokens are summed in wave order into one column of per-block
+// partials.
+template <bool GRPO>
+__global__ __launch_bounds__(256) void lm_combine_kernel(LmArgs a, CombineOut o) {
+  __shared__ float red[4][kGrpoParts];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int t = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + wave);   // wave-uniform
+  float v[kGrpoParts] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (t < a.T) {
+    // GRPO: the token's inputs and trajectory first, so that their loads
+    // land while the merge below runs
+    bool on = false;
+    float old_t = 0.f, ref_t = 0.f, adv_t = 0.f;
+    if (GRPO) {
+      on = o.mask == nullptr || o.mask[t] != 0;
+      old_t = o.logp_old[t];
+      if (o.logp_ref != nullptr) ref_t = o.logp_ref[t];
+      adv_t = o.adv[grpo_traj_of_wave(o.traj_ptr, o.n_traj, t, lane)];
+    }
+    const int y = a.tgt[t];
+    const bool scored = uint32_t(y) < uint32_t(a.V);
+    float tl = 0.f;
+    if (scored)
+      tl = target_dot(a, t, y, lane);
+    else if (lane == 0 && y != -1)
+      atomicAdd(a.bad_targets, 1);
+    const float2* p = a.part + size_t(t) * a.n_chunks;
+    float m = -INFINITY;
+    for (int i = lane; i < a.n_chunks; i += 64) m = fmaxf(m, p[i].x);
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
-  float s = 0.f;
-  for (int i = lane; i < a.n_chunks; i += 64) s += p[i].y * fast_exp2(p[i].x - m);
+    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+    float s = 0.f;
+    for (int i = lane; i < a.n_chunks; i += 64) s += p[i].y * fast_exp2(p[i].x - m);
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
-  if (lane != 0) return;
-  const float l = (m + __log2f(s)) * kLn2;
-  lse[t] = l;
-  const bool scored = uint32_t(a.tgt[t]) < uint32_t(a.V);
-  const float lp = scored ? a.tlogit[t] - l : 0.f;
-  logp[t] = lp;
-  if (logp_old != nullptr) {
-    const float r = scored ? expf(lp - logp_old[t]) : 1.f;
-    ratio[t] = r;
-    clipped[t] = fminf(fmaxf(r, 1.f - eps_lo), 1.f + eps_hi);
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    if (lane == 0) {
+      const float l = (m + __log2f(s)) * kLn2;
+      o.lse[t] = l;
+      const float lp = scored ? tl - l : 0.f;
+      o.logp[t] = lp;
+      if (o.logp_old != nullptr) {
+        const float r = scored ? expf(lp - o.logp_old[t]) : 1.f;
+        o.ratio[t] = r;
+        o.clipped[t] = fminf(fmaxf(r, 1.f - o.eps_lo), 1.f + o.eps_hi);
+      }
+      if (GRPO) {
+        float g = 0.f;
+        if (on) {
+          g = grpo_token_terms(lp, old_t, o.logp_ref != nullptr ? &ref_t : nullptr, adv_t,
+                               o.g_eps_lo, o.g_eps_hi, o.beta, v);
+          const float n = o.n_loss_fixed >= 0 ? float(o.n_loss_fixed) : float(*o.n_loss_count);
+          g = g / n;   // n >= 1: this token is a loss token
+        }
+        o.dlogp[t] = g;
+      }
+    }
+  }
+  if (GRPO) {
+    if (lane == 0)
+#pragma unroll
+      for (int k = 0; k < kGrpoParts; ++k) red[wave][k] = v[k];
+    __syncthreads();
+    if (threadIdx.x < kGrpoParts) {   // partials stored counter-major: [k][block]
+      const int k = threadIdx.x;
+      o.part[size_t(k) * o.part_stride + blockIdx.x] =
+          ((red[0][k] + red[1][k]) + red[2][k]) + red[3][k];
+    }
   }
 }
 
@@ -753,15 +826,26 @@ static hipError_t zero_row(u16* p, int H, hipStream_t stream) {
 
 // Both log-prob workspaces start (at their first 256-byte aligned address)
 // with a 256-byte status block: word 0 counts the target ids outside
-// [-1, V) the last call met.  The call's own buffers follow it.
+// [-1, V) the last call met, word 1 the loss tokens of a fused GRPO forward.
+// The call's own buffers follow it.
 constexpr size_t kStatusBytes = 256;
 
-// status | per-(token, chunk) (max, sum) | target logits
+// status | per-(token, chunk) (max, sum)
 size_t logprob_fwd_ws_bytes(int T, int H, int V) {
   (void)H;
   const int n_chunks = vocab_pad(V) / 128;
-  return kStatusBytes + align256(size_t(T) * n_chunks * sizeof(float2)) +
-         align256(size_t(T) * sizeof(float)) + 256;
+  return kStatusBytes + align256(size_t(T) * n_chunks * sizeof(float2)) + 256;
+}
+
+// the forward's workspace | GRPO per-block partials (4 tokens a block) |
+// advantages
+static int combine_blocks(int T) { return (T + 3) / 4; }
+// row stride of the counter-major partials (16-byte rows for the finish)
+static int part_stride(int T) { return (combine_blocks(T) + 3) / 4 * 4; }
+size_t logprob_grpo_ws_bytes(int T, int H, int V, int n_traj) {
+  return logprob_fwd_ws_bytes(T, H, V) +
+         align256(size_t(part_stride(T)) * kGrpoParts * sizeof(float)) +
+         align256(size_t(n_traj) * sizeof(float));
 }
 
 static int g_rows(int T) { return panel_rows(T); }
@@ -777,7 +861,7 @@ static char* align_ptr(void* p) {
 }
 
 __global__ __launch_bounds__(64) void clear_status_kernel(int* status) {
-  if (threadIdx.x == 0) status[0] = 0;
+  status[threadIdx.x] = 0;   // the whole 256-byte block
 }
 
 // The status block of a log-prob workspace, cleared on the stream (a kernel,
@@ -851,10 +935,63 @@ static hipError_t launch_dh(LmArgs b, float* part, const char* name, hipStream_t
   return hipGetLastError();
 }
 
-hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, const void* hidden,
-                              const void* weight, const int32_t* target, const float* logp_old,
-                              float* logp, float* ratio, float* clipped, float* lse, void* ws,
-                              hipStream_t stream) {
+// Preparation pass of the fused GRPO forward: the advantage of every
+// trajectory (thread i < n_traj) and the loss tokens (the mask's nonzero
+// entries, 1024 per block, added with one integer atomic per block: exact in
+// any order).
+__global__ __launch_bounds__(256) void grpo_prep_kernel(const uint8_t* mask, int T, int* count,
+                                                        const float* reward, int n_traj, int G,
+                                                        float adv_eps, float* adv) {
+  __shared__ int wsum[4];
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n_traj) adv[i] = grpo_advantage(reward, G, i, adv_eps);
+  if (mask == nullptr) return;   // block-uniform
+  const int i0 = i * 4;
+  int c = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) c += (i0 + k < T && mask[i0 + k] != 0) ? 1 : 0;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int tot = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    if (tot) atomicAdd(count, tot);
+  }
+}
+
+static hipError_t logprob_fwd_common(LmArgs& a, void* ws, const CombineOut& o, bool grpo,
+                                     const uint8_t* grpo_mask, hipStream_t stream) {
+  a.bad_targets = clear_status(ws, stream);
+  a.part = reinterpret_cast<float2*>(align_ptr(ws) + kStatusBytes);
+  a.nA = a.Vp / BA;
+  a.nT = (a.T + BT - 1) / BT;
+  if (grpo) {
+    const int blocks = std::max((a.T + 1023) / 1024, (o.n_traj + 255) / 256);
+    ProfScope p("grpo_prep", stream);
+    hipLaunchKernelGGL(grpo_prep_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, grpo_mask,
+                       a.T, a.bad_targets + 1, o.reward, o.n_traj, o.G, o.adv_eps,
+                       const_cast<float*>(o.adv));
+  }
+  if (a.T == 0) return hipGetLastError();
+  {
+    ProfScope p("lm_logits", stream);
+    hipLaunchKernelGGL(lm_tile_kernel<kModeLogits>, gemm_grid(a), dim3(NWAVES * 64), 0, stream, a);
+  }
+  {
+    ProfScope p("lm_combine", stream);
+    if (grpo)
+      hipLaunchKernelGGL(lm_combine_kernel<true>, dim3(combine_blocks(a.T)), dim3(256), 0, stream,
+                         a, o);
+    else
+      hipLaunchKernelGGL(lm_combine_kernel<false>, dim3(combine_blocks(a.T)), dim3(256), 0,
+                         stream, a, o);
+  }
+  return hipGetLastError();
+}
+
+static LmArgs fwd_args(int T, int H, int V, const void* hidden, const void* weight,
+                       const int32_t* target) {
   LmArgs a{};
   a.h = static_cast<const u16*>(hidden);
   a.w = static_cast<const u16*>(weight);
@@ -864,26 +1001,70 @@ hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, c
   a.V = V;
   a.Vp = vocab_pad(V);
   a.n_chunks = a.Vp / 128;
-  a.bad_targets = clear_status(ws, stream);
-  char* base = align_ptr(ws) + kStatusBytes;
-  a.part = reinterpret_cast<float2*>(base);
-  a.tlogit = reinterpret_cast<float*>(base + align256(size_t(T) * a.n_chunks * sizeof(float2)));
-  a.nA = a.Vp / BA;
-  a.nT = (T + BT - 1) / BT;
-  {
-    ProfScope p("lm_logits", stream);
-    hipLaunchKernelGGL(lm_tile_kernel<kModeLogits>, gemm_grid(a), dim3(NWAVES * 64), 0, stream, a);
-  }
-  {
-    ProfScope p("lm_target", stream);
-    hipLaunchKernelGGL(lm_target_kernel<false>, dim3((T + 3) / 4), dim3(256), 0, stream, a);
-  }
-  {
-    ProfScope p("lm_combine", stream);
-    hipLaunchKernelGGL(lm_combine_kernel, dim3((T + 3) / 4), dim3(256), 0, stream, a, logp_old,
-                       logp, ratio, clipped, lse, eps_lo, eps_hi);
-  }
-  return hipGetLastError();
+  return a;
+}
+
+hipError_t launch_logprob_fwd(int T, int H, int V, float eps_lo, float eps_hi, const void* hidden,
+                              const void* weight, const int32_t* target, const float* logp_old,
+                              float* logp, float* ratio, float* clipped, float* lse, void* ws,
+                              hipStream_t stream) {
+  LmArgs a = fwd_args(T, H, V, hidden, weight, target);
+  CombineOut o{};
+  o.logp_old = logp_old;
+  o.logp = logp;
+  o.ratio = ratio;
+  o.clipped = clipped;
+  o.lse = lse;
+  o.eps_lo = eps_lo;
+  o.eps_hi = eps_hi;
+  return logprob_fwd_common(a, ws, o, false, nullptr, stream);
+}
+
+// The forward with the GRPO loss fused into its combine pass: count the loss
+// tokens (mask given), the logits GEMM, the combine with the per-token loss
+// terms and gradient, one block for the statistics and advantages.
+hipError_t launch_logprob_grpo(int T, int H, int V, float eps_lo, float eps_hi,
+                               const void* hidden, const void* weight, const int32_t* target,
+                               const float* logp_old, int n_traj, int G, float g_eps_lo,
+                               float g_eps_hi, float beta, float adv_eps, const int32_t* traj_ptr,
+                               const float* reward, const float* logp_ref, const uint8_t* mask,
+                               float* logp, float* ratio, float* clipped, float* lse,
+                               float* adv_out, float* dlogp, float* stats, void* ws,
+                               hipStream_t stream) {
+  LmArgs a = fwd_args(T, H, V, hidden, weight, target);
+  CombineOut o{};
+  o.logp_old = logp_old;
+  o.logp = logp;
+  o.ratio = ratio;
+  o.clipped = clipped;
+  o.lse = lse;
+  o.eps_lo = eps_lo;
+  o.eps_hi = eps_hi;
+  o.traj_ptr = traj_ptr;
+  o.reward = reward;
+  o.logp_ref = logp_ref;
+  o.mask = mask;
+  o.n_loss_count = reinterpret_cast<const int*>(align_ptr(ws)) + 1;
+  o.n_loss_fixed = mask == nullptr ? T : -1;
+  o.dlogp = dlogp;
+  o.part = reinterpret_cast<float*>(align_ptr(ws) + kStatusBytes +
+                                    align256(size_t(T) * a.n_chunks * sizeof(float2)));
+  o.part_stride = part_stride(T);
+  o.adv = adv_out != nullptr
+              ? adv_out
+              : reinterpret_cast<float*>(reinterpret_cast<char*>(o.part) +
+                                         align256(size_t(part_stride(T)) * kGrpoParts *
+                                                  sizeof(float)));
+  o.n_traj = n_traj;
+  o.G = G;
+  o.g_eps_lo = g_eps_lo;
+  o.g_eps_hi = g_eps_hi;
+  o.beta = logp_ref != nullptr ? beta : 0.f;
+  o.adv_eps = adv_eps;
+  if (hipError_t e = logprob_fwd_common(a, ws, o, true, mask, stream); e != hipSuccess) return e;
+  ProfScope p("grpo_finish", stream);
+  return launch_grpo_fused_finish(o.part, combine_blocks(T), o.part_stride, n_traj, o.adv, stats,
+                                  stream);
 }
 
 hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const void* weight,
@@ -918,7 +1099,7 @@ hipError_t launch_logprob_bwd(int T, int H, int V, const void* hidden, const voi
   }
   {
     ProfScope p("lm_target", stream);
-    hipLaunchKernelGGL(lm_target_kernel<true>, dim3((T + 3) / 4), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(lm_target_kernel, dim3((T + 3) / 4), dim3(256), 0, stream, a);
   }
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   return launch_dh(a, part, "lm_dh", stream);

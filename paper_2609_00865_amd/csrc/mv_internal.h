@@ -106,4 +106,8 @@ hipError_t launch_unpack_sum(const mv_branch_pack& p, const void* in, int W, boo
                              void* out, hipStream_t stream);
 hipError_t launch_rope(const mv_branch_pack& p, const void* x, int H, int d, float theta,
                        int direction, void* out, hipStream_t stream);
+hipError_t launch_pack_rope(const mv_branch_pack& p, const void* in, int H, int d, float theta,
+                            void* out, hipStream_t stream);
+hipError_t launch_unpack_rope(const mv_branch_pack& p, const void* in, int H, int d, float theta,
+                              bool out_fp32, void* out, hipStream_t stream);
 }  // namespace mv

@@ -37,3 +37,21 @@ template <bool IV>
 MV_HD bool mv_visible_k(int i, int j, int omega_j, const int* iv_ptr, const int* iv) {
   return IV ? mv_visible_iv(i, j, omega_j, iv_ptr, iv) : mv_visible(i, j, omega_j);
 }
+
+#if defined(__HIPCC__)
+// The visibility bits of one lane's 32 score elements of a 64-key tile whose
+// keys may have several live intervals, in the attention kernels' layout:
+// element e (bit e) is key j0 + (e / 16) * 32 + ((e % 16) / 4) * 8 + g * 4 +
+// e % 4 for query row i; omega of the tile's key k at om[k].  Out of line: the
+// interval walk stays off the register budget of the kernels' pipelined
+// loops, which call it only for tiles that hold such a key.
+[[maybe_unused]] static __device__ __noinline__ uint32_t
+mv_visible_iv_bits(int i, int j0, int g, const int* om, const int* iv_ptr, const int* iv) {
+  uint32_t bits = 0;
+  for (int e = 0; e < 32; ++e) {
+    const int k = (e >> 4) * 32 + ((e & 15) >> 2) * 8 + g * 4 + (e & 3);
+    if (mv_visible_iv(i, j0 + k, om[k], iv_ptr, iv)) bits |= 1u << e;
+  }
+  return bits;
+}
+#endif

@@ -288,4 +288,32 @@ mv_status mv_rope(const mv_branch_pack* p, const void* x, int32_t n_heads, int32
                 "rope launch");
 }
 
+mv_status mv_pack_rows_rope(const mv_branch_pack* p, const void* in, int32_t n_heads,
+                            int32_t head_dim, float theta, void* out, hipStream_t stream) {
+  if (mv_status st = check_ready(p); st != MV_OK) return st;
+  if (n_heads <= 0 || head_dim <= 0 || head_dim % 16 != 0 || head_dim > 256)
+    return bad(MV_ERR_UNSUPPORTED, "n_heads > 0 and head_dim a multiple of 16, <= 256 required");
+  if (!(theta > 1.f)) return bad(MV_ERR_INVALID_ARG, "theta must be > 1");
+  if (in == nullptr || out == nullptr || !aligned16(in) || !aligned16(out))
+    return bad(MV_ERR_INVALID_ARG, "null or misaligned tensor");
+  if (in == out) return bad(MV_ERR_INVALID_ARG, "out must not alias in");
+  return hip_ok(mv::launch_pack_rope(*p, in, n_heads, head_dim, theta, out, stream),
+                "pack+rope launch");
+}
+
+mv_status mv_unpack_rows_sum_rope(const mv_branch_pack* p, const void* in, int32_t n_heads,
+                                  int32_t head_dim, float theta, int32_t out_fp32, void* out,
+                                  hipStream_t stream) {
+  if (mv_status st = check_ready(p); st != MV_OK) return st;
+  if (n_heads <= 0 || head_dim <= 0 || head_dim % 16 != 0 || head_dim > 256)
+    return bad(MV_ERR_UNSUPPORTED, "n_heads > 0 and head_dim a multiple of 16, <= 256 required");
+  if (!(theta > 1.f)) return bad(MV_ERR_INVALID_ARG, "theta must be > 1");
+  if (in == nullptr || out == nullptr || !aligned16(in) || !aligned16(out))
+    return bad(MV_ERR_INVALID_ARG, "null or misaligned tensor");
+  if (in == out) return bad(MV_ERR_INVALID_ARG, "out must not alias in");
+  return hip_ok(mv::launch_unpack_rope(*p, in, n_heads, head_dim, theta, out_fp32 != 0, out,
+                                       stream),
+                "unpack+rope launch");
+}
+
 }  // extern "C"

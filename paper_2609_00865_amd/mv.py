@@ -164,9 +164,17 @@ mv_branch_pack_free = _sig("mv_branch_pack_free", None, _vp)
 mv_pack_rows = _sig("mv_pack_rows", ctypes.c_int, _vp, _vp, _i32, _vp, _vp)
 mv_unpack_rows_sum = _sig("mv_unpack_rows_sum", ctypes.c_int, _vp, _vp, _i32, _i32, _vp, _vp)
 mv_rope = _sig("mv_rope", ctypes.c_int, _vp, _vp, _i32, _i32, _f32, _i32, _vp, _vp)
+mv_pack_rows_rope = _sig("mv_pack_rows_rope", ctypes.c_int, _vp, _vp, _i32, _i32, _f32, _vp, _vp)
+mv_unpack_rows_sum_rope = _sig("mv_unpack_rows_sum_rope", ctypes.c_int, _vp, _vp, _i32, _i32,
+                               _f32, _i32, _vp, _vp)
 mv_grpo_loss_workspace_bytes = _sig("mv_grpo_loss_workspace_bytes", _sz, _P(GrpoShape))
 mv_grpo_loss = _sig("mv_grpo_loss", ctypes.c_int, _P(GrpoShape), _vp, _vp, _vp, _vp, _vp, _vp,
                     _vp, _vp, _vp, _vp, _sz, _vp)
+mv_token_logprob_grpo_workspace_bytes = _sig("mv_token_logprob_grpo_workspace_bytes", _sz,
+                                             _P(LogprobShape), _P(GrpoShape))
+mv_token_logprob_grpo = _sig("mv_token_logprob_grpo", ctypes.c_int, _P(LogprobShape),
+                             _P(GrpoShape), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                             _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp)
 mv_sdcc_kl_workspace_bytes = _sig("mv_sdcc_kl_workspace_bytes", _sz, _P(KLShape))
 mv_sdcc_kl = _sig("mv_sdcc_kl", ctypes.c_int, _P(KLShape), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                   _vp, _sz, _vp)
@@ -192,7 +200,8 @@ EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_ma
             "mv_branch_pack_device_bytes", "mv_branch_pack_upload", "mv_branch_pack_free",
             "mv_pack_rows", "mv_unpack_rows_sum", "mv_rope", "mv_token_logprob_dweight",
             "mv_view_mask_intervals", "mv_token_logprob_bad_targets", "mv_attn_bwd_noalloc",
-            "mv_build_shared_trunk_pack",
+            "mv_build_shared_trunk_pack", "mv_token_logprob_grpo_workspace_bytes",
+            "mv_token_logprob_grpo", "mv_pack_rows_rope", "mv_unpack_rows_sum_rope",
             "mv_profile_enable", "mv_profile_read"]
 
 VIEW_LIVE, VIEW_FINAL = 0, 1
@@ -561,6 +570,28 @@ def rope(pack: BranchPack, x, theta: float = 1e6, inverse: bool = False, out=Non
     return out
 
 
+def pack_rows_rope(pack: BranchPack, x, theta: float = 1e6, stream=None):
+    """x [T, H, d] bf16 -> [n_packed, H, d]: gathered by each slot's physical
+    token and rotated by the slot's position id in the same pass."""
+    _need_bf16_cuda(x)
+    out = torch.empty((pack.n_packed,) + tuple(x.shape[1:]), dtype=x.dtype, device=x.device)
+    check(mv_pack_rows_rope(pack.handle, _ptr(x), x.shape[1], x.shape[2], float(theta),
+                            _ptr(out), _stream(stream)))
+    return out
+
+
+def unpack_rows_sum_rope(pack: BranchPack, g, theta: float = 1e6, out_fp32: bool = False,
+                         stream=None):
+    """g [n_packed, H, d] bf16 -> [T, H, d]: each copy rotated back by its
+    slot's position and the copies of a token summed (fp32), in one pass."""
+    _need_bf16_cuda(g)
+    out = torch.empty((pack.total_tokens,) + tuple(g.shape[1:]),
+                      dtype=torch.float32 if out_fp32 else g.dtype, device=g.device)
+    check(mv_unpack_rows_sum_rope(pack.handle, _ptr(g), g.shape[1], g.shape[2], float(theta),
+                                  1 if out_fp32 else 0, _ptr(out), _stream(stream)))
+    return out
+
+
 # ---------------------------------------------------------------------------
 # GRPO loss and drift diagnostics
 # ---------------------------------------------------------------------------
@@ -581,6 +612,41 @@ def grpo_loss(traj_ptr, reward, logp, logp_old, logp_ref=None, loss_mask=None, g
                        _ptr(logp_old), _ptr(logp_ref), _ptr(loss_mask), _ptr(adv), _ptr(dlogp),
                        _ptr(stats), _ptr(workspace), workspace.numel(), _stream(stream)))
     return adv, dlogp, stats
+
+
+def token_logprob_grpo_workspace(hidden, weight, n_traj, group_size=16) -> torch.Tensor:
+    s = _lp_shape(hidden, weight, 0.2, 0.2)
+    g = GrpoShape(hidden.shape[0], int(n_traj), int(group_size), 0.2, 0.2, 0.0, 1e-6)
+    n = int(mv_token_logprob_grpo_workspace_bytes(ctypes.byref(s), ctypes.byref(g)))
+    return torch.empty(n, dtype=torch.uint8, device=hidden.device)
+
+
+def token_logprob_grpo(hidden, weight, target, logp_old, traj_ptr, reward, logp_ref=None,
+                       loss_mask=None, group_size=16, eps_low=0.2, eps_high=0.28, beta=0.0,
+                       adv_eps=1e-6, workspace=None, stream=None):
+    """token_logprob and grpo_loss in one forward (the loss fused into the
+    log-prob's combine pass): (logp, ratio, clipped, lse, advantage, dlogp,
+    stats fp32 [8] in GRPO_STATS order), all on device.  The same clip pair
+    serves the ratio output and the loss."""
+    _need_bf16_cuda(hidden, weight)
+    T, n_traj = hidden.shape[0], reward.numel()
+    s = _lp_shape(hidden, weight, eps_low, eps_high)
+    g = GrpoShape(T, n_traj, int(group_size), float(eps_low), float(eps_high), float(beta),
+                  float(adv_eps))
+    dev = hidden.device
+    f = lambda n: torch.empty(n, dtype=torch.float32, device=dev)
+    logp, ratio, clipped, lse, dlogp = f(T), f(T), f(T), f(T), f(T)
+    adv, stats = f(n_traj), f(8)
+    if workspace is None:
+        workspace = torch.empty(
+            int(mv_token_logprob_grpo_workspace_bytes(ctypes.byref(s), ctypes.byref(g))),
+            dtype=torch.uint8, device=dev)
+    check(mv_token_logprob_grpo(ctypes.byref(s), ctypes.byref(g), _ptr(hidden), _ptr(weight),
+                                _ptr(target), _ptr(logp_old), _ptr(traj_ptr), _ptr(reward),
+                                _ptr(logp_ref), _ptr(loss_mask), _ptr(logp), _ptr(ratio),
+                                _ptr(clipped), _ptr(lse), _ptr(adv), _ptr(dlogp), _ptr(stats),
+                                _ptr(workspace), workspace.numel(), _stream(stream)))
+    return logp, ratio, clipped, lse, adv, dlogp, stats
 
 
 # ---------------------------------------------------------------------------
@@ -643,7 +709,8 @@ def sdcc_lambda(step: int, total_steps: int, lambda_max: float = 0.1,
 KERNELS = ["attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq",
            "lm_logits", "lm_target", "lm_combine", "lm_wt", "lm_grad", "lm_dh", "lm_dw",
            "kl_logits", "kl_combine", "kl_wt", "kl_grad", "kl_dh",
-           "grpo", "pack", "unpack", "rope",
+           "grpo", "grpo_prep", "grpo_finish", "pack", "unpack", "rope", "pack_rope",
+           "unpack_rope",
            "materialize", "ppo_clip"]
 
 

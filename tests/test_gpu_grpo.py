@@ -80,3 +80,144 @@ def test_single_token_and_wide_ratios():
 def test_bench_shape():
     """The recipe's shape: 4 prompts x 16 samples, 512 tokens each (32768)."""
     _check(*_run([512] * 64, 16, 5), "grpo-64x512")
+
+
+# ---------------------------------------------------------------------------
+# The loss fused into the LM head's combine pass (mv_token_logprob_grpo)
+# ---------------------------------------------------------------------------
+from oracle import logprob as OL  # noqa: E402
+
+
+def _fused_inputs(lengths, H, V, G, seed, bad_every=0, skip_every=0):
+    """LM-head inputs whose rollout and reference log-probs sit near the
+    oracle's log-prob of each token (both clip edges and the interior occur)."""
+    ptr, r, _, _, _, mask = synth.make_grpo_inputs(lengths, seed)
+    T = int(ptr[-1])
+    h, w, y, _, _ = synth.make_logprob_inputs(T, H, V, seed)
+    if skip_every:
+        y[skip_every - 1::skip_every] = -1
+    lp_true = OL.token_logprob(h, w, y)[0]
+    gen = torch.Generator().manual_seed(synth.tensor_seed("grpo-fused", seed))
+    old = (lp_true + 0.1 * torch.randn(T, generator=gen, dtype=F64)).float()
+    ref = (lp_true + 0.05 * torch.randn(T, generator=gen, dtype=F64)).float()
+    y_dev = y.clone()
+    if bad_every:
+        y_dev[bad_every - 1::bad_every] = V + 3     # out of range: skipped and counted
+    return h, w, y, y_dev, old, ptr, r, ref, mask, lp_true
+
+
+def _run_fused_vs_two_calls(lengths, H, V, G, seed, use_ref=True, use_mask=True, beta=0.001,
+                            eps=(0.2, 0.28), bad_every=0, skip_every=0):
+    h, w, y, y_dev, old, ptr, r, ref, mask, lp_true = _fused_inputs(lengths, H, V, G, seed,
+                                                                     bad_every, skip_every)
+    T = h.shape[0]
+    print(f"[gpu] fused grpo T={T} H={H} V={V} n_traj={len(lengths)} G={G} "
+          f"ref={use_ref} mask={use_mask} bad_every={bad_every}", flush=True)
+    ref = ref if use_ref else None
+    mask = mask if use_mask else None
+    b = beta if use_ref else 0.0
+    cu = lambda x: None if x is None else x.cuda()
+    hd, wd, yd, od, pd, rd, refd, md = map(cu, (h, w, y_dev, old, ptr, r, ref, mask))
+    ws = mv.token_logprob_grpo_workspace(hd, wd, len(lengths), G)
+    fused = mv.token_logprob_grpo(hd, wd, yd, od, pd, rd, refd, md, group_size=G,
+                                  eps_low=eps[0], eps_high=eps[1], beta=b, workspace=ws)
+    bad = mv.token_logprob_bad_targets(ws)
+    again = mv.token_logprob_grpo(hd, wd, yd, od, pd, rd, refd, md, group_size=G,
+                                  eps_low=eps[0], eps_high=eps[1], beta=b)
+    logp, ratio, clipped, lse = mv.token_logprob(hd, wd, yd, od, eps[0], eps[1])
+    adv, dlogp, stats = mv.grpo_loss(pd, rd, logp, od, refd, md, group_size=G, eps_low=eps[0],
+                                     eps_high=eps[1], beta=b)
+    torch.cuda.synchronize()
+    for x, z in zip(fused, again):
+        assert torch.equal(x, z)                  # fixed-order reductions
+    names = ("logp", "ratio", "clipped", "lse", "advantage", "dlogp")
+    for n, x, z in zip(names, fused[:6], (logp, ratio, clipped, lse, adv, dlogp)):
+        assert torch.equal(x, z), f"fused {n} differs from the two-call form"
+    fs, ts = fused[6].cpu().double(), stats.cpu().double()
+    print("fused stats", fs.tolist(), "two-call", ts.tolist(), flush=True)
+    assert torch.allclose(fs, ts, rtol=1e-6, atol=1e-7)
+    expect_bad = len(range(bad_every - 1, T, bad_every)) if bad_every else 0
+    assert bad == expect_bad
+    return fused, (y, old, ptr, r, ref, mask, lp_true, b, eps)
+
+
+def _check_fused_oracle(fused, ctx, G):
+    """The fused outputs against the oracle run on the oracle's own log-probs.
+    The gates follow from the measured log-prob error d (max |logp_gpu -
+    logp_oracle|): each ratio moves by a factor within exp(+-d), so a clip
+    decision may flip only where the oracle's ratio lies within 2 d of an
+    edge, and each per-token term moves by at most ~2 d of its own size."""
+    y, old, ptr, r, ref, mask, lp_true, beta, eps = ctx
+    logp, _, _, _, adv, dlogp, stats = (x.cpu() for x in fused)
+    scored = y >= 0
+    d = float((logp.double() - lp_true).abs().max())
+    print(f"max |logp - oracle| = {d:.3e}", flush=True)
+    assert d <= 1e-3
+    o = OG.grpo_loss(ptr.tolist(), r, lp_true, old, ref, mask, G, eps[0], eps[1], beta)
+    assert torch.allclose(adv.double(), o["advantage"], rtol=1e-5, atol=1e-5)
+    rho = o["ratio"]
+    amb = ((rho - (1 - eps[0])).abs() <= 2 * d * rho + 1e-6) | \
+          ((rho - (1 + eps[1])).abs() <= 2 * d * rho + 1e-6)
+    scale = float(o["dlogp"].abs().max()) or 1.0
+    err = (dlogp.double() - o["dlogp"]).abs()
+    assert bool((err[~amb] <= (2 * d + 1e-5) * scale).all()), float(err[~amb].max())
+    st = o["stats"]
+    got = dict(zip(mv.GRPO_STATS, stats.tolist()))
+    n = float(st["n_loss_tokens"])
+    assert got["n_loss_tokens"] == n
+    slack = float(amb.sum()) / max(n, 1.0) + 1e-6
+    for k in ("clip_frac_low", "clip_frac_high"):
+        assert abs(got[k] - float(st[k])) <= slack, (k, got[k], float(st[k]))
+    amax = float(o["advantage"].abs().max())
+    rmax = float(rho.max())
+    # |d k3 / d logp| = |exp(x) - 1| with x = ref - logp
+    kmax = float((ref.double() - lp_true).abs().max() + d).__abs__() if ref is not None else 0.0
+    kslope = float(np.expm1(kmax)) if ref is not None else 0.0
+    tol = {"loss": 2 * d * amax * rmax + beta * kslope * d + 1e-5 * max(1.0, abs(float(st["loss"]))),
+           "logdiff": d + 1e-5, "ratio_mean": 2 * d * rmax + 1e-5,
+           "kl_ref": 2 * d * kslope + 1e-6, "adv_abs_mean": 1e-5}
+    for k, t in tol.items():
+        assert abs(got[k] - float(st[k])) <= t, (k, got[k], float(st[k]), t)
+    assert bool((scored | (logp == 0)).all())
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_fused_ragged_groups(seed):
+    rng = np.random.default_rng(seed)
+    lengths = [int(x) for x in rng.integers(0, 60, size=16)]     # includes empty ones
+    fused, ctx = _run_fused_vs_two_calls(lengths, 256, 1000, 8, seed, skip_every=11)
+    _check_fused_oracle(fused, ctx, 8)
+
+
+def test_fused_no_reference_no_mask_group_of_one():
+    fused, ctx = _run_fused_vs_two_calls([5, 30, 1, 57], 128, 600, 1, 3, use_ref=False,
+                                         use_mask=False)
+    _check_fused_oracle(fused, ctx, 1)
+
+
+def test_fused_out_of_range_targets():
+    """Ids outside [-1, vocab) are skipped and counted in the fused pass too
+    (both forms see the same ids; the oracle is not asked about them)."""
+    _run_fused_vs_two_calls([40, 23, 17, 64], 192, 300, 2, 6, bad_every=9)
+
+
+def test_fused_bench_shape_sampled_against_two_calls():
+    """The recipe's 64 x 512 token layout on a 3584-hidden, 152064-vocab head:
+    fused and two-call forms agree bit for bit (the two-call form's parity at
+    this size is covered by the log-prob and GRPO tests)."""
+    lengths = [512] * 64
+    ptr, r, _, _, _, mask = synth.make_grpo_inputs(lengths, 7)
+    T = int(ptr[-1])
+    h, w, y, old, _ = synth.make_logprob_inputs(T, 3584, 152064, 7, device="cuda")
+    old = old - 10.0       # near the head's log-probs at random init (~ -log V)
+    gen = torch.Generator(device="cuda").manual_seed(synth.tensor_seed("grpo-fused", 7))
+    ref = old + 0.05 * torch.randn(T, generator=gen, device="cuda")
+    print(f"[gpu] fused grpo bench shape T={T}", flush=True)
+    pd, rd, md = ptr.cuda(), r.cuda(), mask.cuda()
+    fused = mv.token_logprob_grpo(h, w, y, old, pd, rd, ref, md, group_size=16, beta=0.001)
+    logp, ratio, clipped, lse = mv.token_logprob(h, w, y, old, 0.2, 0.28)
+    adv, dlogp, stats = mv.grpo_loss(pd, rd, logp, old, ref, md, group_size=16, beta=0.001)
+    torch.cuda.synchronize()
+    for x, z in zip(fused[:6], (logp, ratio, clipped, lse, adv, dlogp)):
+        assert torch.equal(x, z)
+    assert torch.allclose(fused[6].double(), stats.double(), rtol=1e-6, atol=1e-7)

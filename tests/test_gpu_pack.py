@@ -89,6 +89,38 @@ def test_rope(d, theta, shared):
 
 
 @SHARED
+@pytest.mark.parametrize("d,theta,H", [(64, 1e4, 3), (128, 1e6, 5)])
+def test_fused_gather_rope_and_adjoint(d, theta, H, shared):
+    """The gather with the rotation fused into it against the oracle's gather
+    then rotation; its adjoint (inverse rotation of each copy, summed) against
+    the oracle's inverse rotation then sum over copies.  The head count is not
+    a multiple of the kernel's 4-head blocks."""
+    trajs = _records(5, lens=(700, 333))
+    pk = _pack(trajs, shared)
+    lay = _layout(trajs, shared)
+    T, N = trajs[-1].end, pk.n_packed
+    print(f"[gpu] fused gather+rope T={T} N={N} H={H} d={d}", flush=True)
+    gen = torch.Generator().manual_seed(6)
+    x = torch.randn(T, H, d, generator=gen).to(BF)
+    got = mv.pack_rows_rope(pk, x.cuda(), theta).cpu()
+    ref = OP.rope(x[lay["src"]], lay["pos"], theta)
+    excess = float(((got.double() - ref).abs() - 2.0 ** -8 * ref.abs()).max())
+    assert excess <= 1e-5 * float(x.abs().max()), excess
+    g = torch.randn(N, H, d, generator=gen).to(BF)
+    gd = g.cuda()
+    s32 = mv.unpack_rows_sum_rope(pk, gd, theta, out_fp32=True).cpu()
+    s16 = mv.unpack_rows_sum_rope(pk, gd, theta).cpu()
+    again = mv.unpack_rows_sum_rope(pk, gd, theta, out_fp32=True).cpu()
+    torch.cuda.synchronize()
+    assert torch.equal(s32, again)
+    back = OP.unpack_sum(lay, OP.rope(g, lay["pos"], theta, inverse=True), T)
+    # fp32 rotation and sums: error well under 1e-5 of the largest term
+    err = float((s32.double() - back).abs().max())
+    assert err <= 1e-5 * float(g.abs().max()) * max(int(np.bincount(lay["src"]).max()), 1), err
+    assert_bf16_close(s16, back, "unpack+rope bf16")
+
+
+@SHARED
 @pytest.mark.parametrize("workload", ["tiny", "medium"])
 def test_packed_attention_forward_backward(shared, workload):
     """One layer over the packed stream: owner rows give every row's view
