@@ -240,22 +240,33 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
 // ---------------------------------------------------------------------------
 // 3. dK / dV
 // ---------------------------------------------------------------------------
+// One workgroup per (128-key tile, KV head) work item, 8 waves: on each SIMD a
+// score wave (waves 0-3) and an accumulating wave (waves 4-7) share 32 keys.
+// For each 32-row unit of each 64-row query block (all query heads of the
+// group), the score wave computes S = Q K^T and dP = dO V^T from its keys' K
+// and V fragments (kept in registers), then P and dS = P (dP - D), and hands
+// both to the accumulating wave as bf16 MFMA operands through LDS (16 bytes
+// per lane and operand, in the lane order both waves use); the accumulating
+// wave runs dV += dO^T P and dK += Q^T dS with the transposing LDS read.
+// The score wave works one unit ahead, so one wave's softmax arithmetic runs
+// beside the other's MFMAs, and each wave holds only half of the state (K/V
+// fragments, or the dK/dV accumulators): that is what lets two waves share a
+// SIMD.  One barrier per unit.  The accumulating waves also stream the query
+// blocks (Q, dO, their rows' LSE and D) from raw buffers straight into LDS,
+// three buffers: the block being accumulated, the block being scored, and
+// one landing.
 template <int D, bool IV>
-__global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
+__global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a) {
   constexpr int BK = kBwdTileK, BQ = kBwdBlockQ;
   constexpr int KS = D / 16, DB = D / 32;
-  // Q and dO blocks, with the rows' LSE and D, go from raw buffers straight
-  // into LDS; Q and dO rows are unpadded and swizzled (kv_swz), read along
-  // their rows and with the transposing read.  Four buffers: while step st
-  // accumulates dV, dK from its block, step st+1 computes S and dP from the
-  // next one, and blocks st+2 and st+3 are in flight (each has two steps to
-  // land).
-  constexpr int NBUF = 4;
+  constexpr int NBUF = 3;
   __shared__ __align__(1024) u16 sQbuf[NBUF * BQ * D];
   __shared__ __align__(1024) u16 sdObuf[NBUF * BQ * D];
   __shared__ __align__(16) float sLbuf[NBUF * BQ];   // LSE * log2 e
   __shared__ __align__(16) float sDbuf[NBUF * BQ];
-  // block of step st in buffer st % NBUF (buf below)
+  // P and dS operands of unit u in half u & 1: [half][pair][operand][lane]
+  __shared__ __align__(16) bf16x8 sXbuf[2][4][4][64];
+  // block of step st in buffer st % NBUF
   auto qtile = [&](int buf) { return reinterpret_cast<const char*>(sQbuf + buf * BQ * D); };
   auto dotile = [&](int buf) { return reinterpret_cast<const char*>(sdObuf + buf * BQ * D); };
 
@@ -271,12 +282,164 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const int om_min = a.mask.bwd_tiles[4 * kt + 0];
   const int T = a.T, G = a.Hq / a.Hkv;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int pair = wave & 3;
+  const bool scorer = __builtin_amdgcn_readfirstlane(wave) < 4;   // wave-uniform
   const int c = lane & 31, g = lane >> 5;
   const int j0 = kt * BK, j1 = min(T, j0 + BK);
-  const int key = j0 + wave * 32 + c;
+  const int key = j0 + pair * 32 + c;
   const bool kok = key < T;
   const int om = kok ? a.mask.omega[key] : 0;
+  // masks with restoring edits: only a key tile holding a key with several
+  // live intervals walks the interval lists
+  bool iv_tile = false;
+  if constexpr (IV) iv_tile = __syncthreads_or(kok && om < 0) != 0;
 
+  const int nqb = qb1 - qb0;
+  const int steps = nqb * G;
+  const int h0 = hk * G;
+  const int n_units = 2 * steps;   // unit u: step u / 2, rows (u % 2) * 32 .. of its block
+  // Step st covers query block qb0 + st % nqb of head h0 + st / nqb.  Rows
+  // past T read row T - 1 (finite values; no key is visible to them).  Every
+  // accumulating wave issues the same number of loads per step (LPS): its
+  // share of Q and dO, and the block's LSE (even waves) or D (odd waves; the
+  // second pair of waves writes the same words again).
+  const uint32_t q_row = uint32_t(a.Hq) * D * 2;     // bytes per query row
+  constexpr int LPS = 2 * KvTileLoader<D, BQ>::KLD + 1;
+  static_assert(BQ == 64, "one LSE / D word per lane");
+
+  if (!scorer) {   // ---- accumulating waves: loads of steps 0 and 1
+    const KvTileLoader<D, BQ> ldr(tid - 256);
+    auto issue_step = [&](int st) {
+      const int buf = st % NBUF;
+      const int hh = h0 + st / nqb, qb = qb0 + st % nqb;
+      const uint32_t bytes = uint32_t(T) * q_row - uint32_t(hh) * D * 2;
+      ldr.issue(make_rsrc(a.q + size_t(hh) * D, bytes), make_rsrc(a.dout + size_t(hh) * D, bytes),
+                qb, T, q_row, lds_addr(sQbuf) + buf * BQ * D * 2,
+                lds_addr(sdObuf) + buf * BQ * D * 2);
+      const bool odd = pair & 1;
+      const float* vec = (odd ? a.Dd : a.L2) + size_t(hh) * T;
+      buf_lds4(make_rsrc(vec, uint32_t(T) * 4), uint32_t(min(qb * BQ + lane, T - 1)) * 4,
+               (odd ? lds_addr(sDbuf) : lds_addr(sLbuf)) + buf * BQ * 4);
+    };
+    issue_step(0);
+    if (steps > 1) {
+      issue_step(1);
+      wait_vmcnt<LPS>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    __syncthreads();   // block 0 landed
+
+    f32x16 dk[DB], dv[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        dk[db][r] = 0.f;
+        dv[db][r] = 0.f;
+      }
+    // interval u (between the barriers that end units u - 1 and u): unit u's
+    // dV/dK here, unit u + 1 in the score wave.  Before the barrier that
+    // ends it, the block the score waves read next (unit u + 2) has landed:
+    // only the block issued after it may still be in flight.
+    auto wait_for = [&](int u) {
+      const int r = (u + 2) >> 1;
+      const int last = min(steps - 1, u >= 0 ? (u >> 1) + 2 : 1);   // last block issued
+      if (r < steps) {
+        if (last > r)
+          wait_vmcnt<LPS>();
+        else
+          wait_vmcnt<0>();
+      }
+    };
+    wait_for(-1);
+    __syncthreads();
+    // unit u = 6 i + UM: its block's buffer (u / 2) % 3 = UM / 2, its rows
+    // and operand half are compile-time constants, so every LDS address is a
+    // per-lane base plus an immediate offset
+    auto unit = [&](auto um_tag, int u) {
+      constexpr int UM = decltype(um_tag)::value;
+      constexpr int mb = UM & 1, buf = UM / 2;
+      const int st = u >> 1;
+      // block st+2 into the buffer block st-1 used (every wave is done with it)
+      if (mb == 0 && st + 2 < steps) issue_step(st + 2);
+      const bf16x8* x = &sXbuf[UM & 1][pair][0][lane];
+      const bf16x8 pf[2] = {x[0], x[64]}, dsf[2] = {x[128], x[192]};
+      const char* sQ = qtile(buf);
+      const char* sdO = dotile(buf);
+      // MFMA q: db = q / 4, kk = (q / 2) % 2, dV (even q) or dK (odd q);
+      // operands read two MFMAs ahead
+      auto opnd = [&](int q) {
+        return ld_tr_swz<D>((q & 1) ? sQ : sdO, (2 * mb + ((q >> 1) & 1)) * 16, (q >> 2) * 32);
+      };
+      constexpr int NQ = 4 * DB;
+      bf16x8 op[3];
+      op[0] = opnd(0);
+      op[1] = opnd(1);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        if (q + 2 < NQ) op[(q + 2) % 3] = opnd(q + 2);
+        const int db = q >> 2, kk = (q >> 1) & 1;
+        if (q & 1)
+          dk[db] = mfma32(op[q % 3], dsf[kk], dk[db]);
+        else
+          dv[db] = mfma32(op[q % 3], pf[kk], dv[db]);
+      }
+      wait_for(u);
+      __syncthreads();
+    };
+    using std::integral_constant;
+    for (int u0 = 0; u0 < n_units; u0 += 6) {
+      unit(integral_constant<int, 0>{}, u0);
+      unit(integral_constant<int, 1>{}, u0 + 1);   // n_units is even
+      if (u0 + 2 < n_units) {
+        unit(integral_constant<int, 2>{}, u0 + 2);
+        unit(integral_constant<int, 3>{}, u0 + 3);
+      }
+      if (u0 + 4 < n_units) {
+        unit(integral_constant<int, 4>{}, u0 + 4);
+        unit(integral_constant<int, 5>{}, u0 + 5);
+      }
+    }
+
+    if (!kok) return;
+    if (slot < 0) {
+      u16* pk = a.dk + (size_t(key) * a.Hkv + hk) * D;
+      u16* pv = a.dv + (size_t(key) * a.Hkv + hk) * D;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int d0 = db * 32 + q4 * 8 + g * 4;
+          uint2 wk, wv;
+          wk.x = pack2(dk[db][q4 * 4 + 0] * a.scale, dk[db][q4 * 4 + 1] * a.scale);
+          wk.y = pack2(dk[db][q4 * 4 + 2] * a.scale, dk[db][q4 * 4 + 3] * a.scale);
+          wv.x = pack2(dv[db][q4 * 4 + 0], dv[db][q4 * 4 + 1]);
+          wv.y = pack2(dv[db][q4 * 4 + 2], dv[db][q4 * 4 + 3]);
+          *reinterpret_cast<uint2*>(pk + d0) = wk;
+          *reinterpret_cast<uint2*>(pv + d0) = wv;
+        }
+    } else {
+      float* base = a.partial + (size_t(slot) * a.Hkv + hk) * 2 * BK * D;
+      float* pk = base + size_t(pair * 32 + c) * D;
+      float* pv = base + size_t(BK) * D + size_t(pair * 32 + c) * D;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int d0 = db * 32 + q4 * 8 + g * 4;
+          *reinterpret_cast<float4*>(pk + d0) =
+              make_float4(dk[db][q4 * 4 + 0] * a.scale, dk[db][q4 * 4 + 1] * a.scale,
+                          dk[db][q4 * 4 + 2] * a.scale, dk[db][q4 * 4 + 3] * a.scale);
+          *reinterpret_cast<float4*>(pv + d0) =
+              make_float4(dv[db][q4 * 4 + 0], dv[db][q4 * 4 + 1], dv[db][q4 * 4 + 2],
+                          dv[db][q4 * 4 + 3]);
+        }
+    }
+    return;
+  }
+
+  // ---- score waves
   bf16x8 kf[KS], vf[KS];
   {
     const size_t off = (size_t(kok ? key : 0) * a.Hkv + hk) * D + g * 8;
@@ -286,76 +449,41 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       vf[ks] = as_bf16x8(kok ? ld16(a.v + off + ks * 16) : make_uint4(0, 0, 0, 0));
     }
   }
-  f32x16 dk[DB], dv[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      dk[db][r] = 0.f;
-      dv[db][r] = 0.f;
-    }
-
-  const int nqb = qb1 - qb0;
-  const int steps = nqb * G;
-  const int h0 = hk * G;
-  // Step st covers query block qb0 + st % nqb of head h0 + st / nqb.  Rows
-  // past T read row T - 1 (finite values; no key is visible to them).  Every
-  // wave issues the same number of loads per step (LPS): its share of Q and
-  // dO, and the block's LSE (even waves) or D (odd waves; the second pair of
-  // waves writes the same words again).
-  const uint32_t q_row = uint32_t(a.Hq) * D * 2;     // bytes per query row
-  const KvTileLoader<D, BQ> ldr(tid);
-  constexpr int LPS = 2 * KvTileLoader<D, BQ>::KLD + 1;
-  static_assert(BQ == 64, "one LSE / D word per lane");
-  auto issue_step = [&](int st, int buf) {   // a step past the last reloads the last block
-    const int sc_ = min(st, steps - 1);
-    const int hh = h0 + sc_ / nqb, qb = qb0 + sc_ % nqb;
-    const uint32_t bytes = uint32_t(T) * q_row - uint32_t(hh) * D * 2;
-    ldr.issue(make_rsrc(a.q + size_t(hh) * D, bytes), make_rsrc(a.dout + size_t(hh) * D, bytes), qb,
-              T, q_row, lds_addr(sQbuf) + buf * BQ * D * 2, lds_addr(sdObuf) + buf * BQ * D * 2);
-    const bool odd = __builtin_amdgcn_readfirstlane(wave) & 1;   // wave-uniform
-    const float* vec = (odd ? a.Dd : a.L2) + size_t(hh) * T;
-    buf_lds4(make_rsrc(vec, uint32_t(T) * 4), uint32_t(min(qb * BQ + lane, T - 1)) * 4,
-             (odd ? lds_addr(sDbuf) : lds_addr(sLbuf)) + buf * BQ * 4);
-  };
-  // before the barrier that ends step st: block st+2 landed (st+3 may fly)
-  auto wait_step = [&](int st, int n_steps) {
-    if (st + 3 < n_steps)
-      wait_vmcnt<LPS>();
-    else
-      wait_vmcnt<0>();
-  };
-
-  // The work of a step runs in two halves (unit 2 st + mb: the block's
-  // query rows mb*32 ..): S = Q K^T and dP = dO V^T of the half (rows: its
-  // queries, lanes: this wave's keys), then P and dS as bf16 operands, then
-  // its share of dV^T += dO^T P and dK^T += Q^T dS.
-  f32x16 s, dp;
-  auto scores_mfma = [&](int st, int mb) {
-    const char* sQ = qtile(st % NBUF);
-    const char* sdO = dotile(st % NBUF);
+  __syncthreads();   // block 0 landed
+  // unit v = 6 i + VM (computed in the interval before the accumulating
+  // wave takes it): buffer VM / 2, rows and operand half constant
+  auto unit = [&](auto vm_tag, int v) {
+    constexpr int VM = decltype(vm_tag)::value;
+    constexpr int mb = VM & 1, buf = VM / 2;
+    const int st = v >> 1;
+    const char* sQ = qtile(buf);
+    const char* sdO = dotile(buf);
+    // S^T and dP^T of the unit: rows are this wave's keys, lanes' columns
+    // the unit's queries mb*32 + q4*8 + g*4 + e; operands two MFMAs ahead
+    f32x16 s, dp;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       s[r] = 0.f;
       dp[r] = 0.f;
     }
+    auto opnd = [&](int j) {   // MFMA j: ks = j / 2, S (even) or dP (odd)
+      return ld_row_swz<D>((j & 1) ? sdO : sQ, mb * 32 + c, (j >> 1) * 2 + g);
+    };
+    bf16x8 op[3];
+    op[0] = opnd(0);
+    op[1] = opnd(1);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      s = mfma32(ld_row_swz<D>(sQ, mb * 32 + c, ks * 2 + g), kf[ks], s);
-      dp = mfma32(ld_row_swz<D>(sdO, mb * 32 + c, ks * 2 + g), vf[ks], dp);
+    for (int j = 0; j < 2 * KS; ++j) {
+      if (j + 2 < 2 * KS) op[(j + 2) % 3] = opnd(j + 2);
+      if (j & 1)
+        dp = mfma32(op[j % 3], vf[j >> 1], dp);
+      else
+        s = mfma32(op[j % 3], kf[j >> 1], s);
     }
-  };
-  // rows of s/dp are queries mb*32 + q4*8 + g*4 + u of the block
-  auto scores_valu = [&](int st, int mb, bf16x8 (&pf)[2], bf16x8 (&dsf)[2]) {
-    const int buf = st % NBUF;
     const float* sL = sLbuf + buf * BQ;
     const float* sD = sDbuf + buf * BQ;
     const int i0 = (qb0 + st % nqb) * BQ;
-    const bool full = (i0 >= j1 - 1) && (i0 + BQ <= om_min);
-    // single-interval keys: row i sees this lane's key iff 0 <= i - key < om - key,
-    // every row of a full step does (a select, not a branch, keeps the step
-    // one scheduling region)
-    const uint32_t range = full ? 0x7fffffffu : uint32_t(om - key);
+    const bool full = (i0 >= j1 - 1) && (i0 + BQ <= om_min);   // block-uniform
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       const int qo = mb * 32 + q4 * 8 + g * 4;
@@ -364,264 +492,42 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
       const float dd[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int r = q4 * 4 + u;
-        float p = fast_exp2(fmaf(s[r], a.scale_log2, -lv[u]));
-        if (IV) {
-          if (!full && !mv_visible_iv(i0 + qo + u, key, om, a.mask.iv_ptr, a.mask.iv)) p = 0.f;
-        } else {
-          p = uint32_t(i0 + qo + u - key) < range ? p : 0.f;
+      for (int e = 0; e < 4; ++e) s[q4 * 4 + e] = fast_exp2(fmaf(s[q4 * 4 + e], a.scale_log2, -lv[e]));
+      if (!full) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int i = i0 + qo + e;
+          // single-interval keys: row i sees this lane's key iff 0 <= i -
+          // key < om - key
+          const bool vis = (IV && iv_tile) ? mv_visible_iv(i, key, om, a.mask.iv_ptr, a.mask.iv)
+                                           : uint32_t(i - key) < uint32_t(om - key);
+          s[q4 * 4 + e] = vis ? s[q4 * 4 + e] : 0.f;
         }
-        s[r] = p;
-        dp[r] = p * (dp[r] - dd[u]);
       }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dp[q4 * 4 + e] = s[q4 * 4 + e] * (dp[q4 * 4 + e] - dd[e]);
     }
-    pf[0] = to_operand(s, 0);
-    pf[1] = to_operand(s, 8);
-    dsf[0] = to_operand(dp, 0);
-    dsf[1] = to_operand(dp, 8);
-  };
-  auto accumulate = [&](int st, int mb, const bf16x8 (&pf)[2], const bf16x8 (&dsf)[2]) {
-    const char* sQ = qtile(st % NBUF);
-    const char* sdO = dotile(st % NBUF);
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        // dO^T and Q^T operands: columns db*32.. of rows (2 mb + kk)*16.. in accumulator order
-        dv[db] = mfma32(ld_tr_swz<D>(sdO, (2 * mb + kk) * 16, db * 32), pf[kk], dv[db]);
-        dk[db] = mfma32(ld_tr_swz<D>(sQ, (2 * mb + kk) * 16, db * 32), dsf[kk], dk[db]);
-      }
-  };
-
-  // Single-interval masks (IV = false): the same units, with every MFMA
-  // interleaved with softmax work in a fixed issue order (a scheduling fence
-  // after each group).  Unit n's S/dP (run in phase X of unit n-1) feed its
-  // softmax elements 0..7 in phase Y of unit n-1 and 8..15 in its own phase
-  // X; phase X issues unit n+1's S/dP MFMAs, phase Y unit n's dV/dK MFMAs;
-  // operands are read two MFMAs ahead.  Score registers alternate by unit
-  // parity; the row LSE, D and mask range of the unit in flight are kept.
-  f32x16 sc[2], dc[2];
-  float lv[16], dd[16];
-  int ui0 = 0, umb = 0;
-  uint32_t urange = 0;
-  auto load_ctx = [&](int st, int mb, int buf) {
-    const float* sL = sLbuf + buf * BQ;
-    const float* sD = sDbuf + buf * BQ;
-    ui0 = (qb0 + st % nqb) * BQ;
-    umb = mb;
-    const bool full = (ui0 >= j1 - 1) && (ui0 + BQ <= om_min);
-    // a padding step past the last (st >= steps) sees nothing
-    urange = st >= steps ? 0u : full ? 0x7fffffffu : uint32_t(om - key);
-#pragma unroll
-    for (int q4 = 0; q4 < 4; ++q4) {
-      const int qo = mb * 32 + q4 * 8 + g * 4;
-      const float4 l4 = *reinterpret_cast<const float4*>(&sL[qo]);
-      const float4 d4 = *reinterpret_cast<const float4*>(&sD[qo]);
-      lv[q4 * 4 + 0] = l4.x;
-      lv[q4 * 4 + 1] = l4.y;
-      lv[q4 * 4 + 2] = l4.z;
-      lv[q4 * 4 + 3] = l4.w;
-      dd[q4 * 4 + 0] = d4.x; dd[q4 * 4 + 1] = d4.y; dd[q4 * 4 + 2] = d4.z; dd[q4 * 4 + 3] = d4.w;
-    }
-  };
-  // softmax element r (row umb*32 + (r/4)*8 + g*4 + r%4) of the unit in flight
-  auto elem = [&](int par, int r) {
-    float p = fast_exp2(fmaf(sc[par][r], a.scale_log2, -lv[r]));
-    p = uint32_t(ui0 + umb * 32 + (r >> 2) * 8 + g * 4 + (r & 3) - key) < urange ? p : 0.f;
-    sc[par][r] = p;
-    dc[par][r] = p * (dc[par][r] - dd[r]);
-  };
-  // phase X of the unit in set par: the next unit's (st, mb) S/dP MFMAs into
-  // set par ^ 1 (if NEXT) with elements 8..15 of this unit, then its operands
-  auto phaseX = [&](auto next_tag, int par, int st, int mb, bf16x8 (&pfo)[2], bf16x8 (&dso)[2],
-                    int buf) {
-    constexpr bool NEXT = decltype(next_tag)::value;
-    const char* sQ = qtile(buf);
-    const char* sdO = dotile(buf);
-    const int np = par ^ 1;
-    auto opnd = [&](int j) {   // MFMA j: ks = j / 2, S (even) or dP (odd)
-      return ld_row_swz<D>((j & 1) ? sdO : sQ, mb * 32 + c, (j >> 1) * 2 + g);
-    };
-    bf16x8 op[3];
-    if constexpr (NEXT) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        sc[np][r] = 0.f;
-        dc[np][r] = 0.f;
-      }
-      op[0] = opnd(0);
-      op[1] = opnd(1);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int j = 0; j < 2 * KS; ++j) {
-      if constexpr (NEXT) {
-        if (j + 2 < 2 * KS) op[(j + 2) % 3] = opnd(j + 2);
-        if (j & 1)
-          dc[np] = mfma32(op[j % 3], vf[j >> 1], dc[np]);
-        else
-          sc[np] = mfma32(op[j % 3], kf[j >> 1], sc[np]);
-      }
-      if ((j & 1) && 8 + (j >> 1) < 16) elem(par, 8 + (j >> 1));
-      __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int r = 8 + KS; r < 16; ++r) elem(par, r);   // D = 64: the rest
-    pfo[0] = to_operand(sc[par], 0);
-    pfo[1] = to_operand(sc[par], 8);
-    dso[0] = to_operand(dc[par], 0);
-    dso[1] = to_operand(dc[par], 8);
-  };
-  // phase Y of unit (st, mb): its dV/dK MFMAs with elements 0..7 of the next
-  // unit (st2, mb2) in set np, whose context is loaded first (if NEXT)
-  auto phaseY = [&](auto next_tag, int st, int mb, const bf16x8 (&pfc)[2], const bf16x8 (&dsc)[2],
-                    int np, int st2, int mb2, int buf, int buf2) {
-    constexpr bool NEXT = decltype(next_tag)::value;
-    if constexpr (NEXT) load_ctx(st2, mb2, buf2);
-    const char* sQ = qtile(buf);
-    const char* sdO = dotile(buf);
-    // MFMA q: db = q / 4, kk = (q / 2) % 2, dV (even q) or dK (odd q)
-    auto opnd = [&](int q) {
-      return ld_tr_swz<D>((q & 1) ? sQ : sdO, (2 * mb + ((q >> 1) & 1)) * 16, (q >> 2) * 32);
-    };
-    constexpr int NQ = 4 * DB;
-    bf16x8 op[3];
-    op[0] = opnd(0);
-    op[1] = opnd(1);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      if (q + 2 < NQ) op[(q + 2) % 3] = opnd(q + 2);
-      const int db = q >> 2, kk = (q >> 1) & 1;
-      if (q & 1)
-        dk[db] = mfma32(op[q % 3], dsc[kk], dk[db]);
-      else
-        dv[db] = mfma32(op[q % 3], pfc[kk], dv[db]);
-      if constexpr (NEXT) {
-        if ((q & 1) && (q >> 1) < 8) elem(np, q >> 1);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if constexpr (NEXT) {
-#pragma unroll
-      for (int r = NQ / 2; r < 8; ++r) elem(np, r);   // D = 64: the rest
-    }
-  };
-
-  // Software pipeline over half-step units, one barrier per step: the next
-  // unit's S and dP MFMAs are issued before this unit's dV and dK MFMAs, and
-  // the next unit's exponentials follow them.  Block st+3 is requested into
-  // the buffer step st-1 used (every wave finished with it before the last
-  // barrier).
-  bf16x8 pf[2], dsf[2];
-  // Masks with restoring edits: only a key tile that holds a key with several
-  // live intervals takes the plain loop with the interval walk; every other
-  // tile runs the pipelined loop of single-interval masks.
-  bool iv_tile = false;
-  if constexpr (IV) iv_tile = __syncthreads_or(kok && om < 0) != 0;
-  if (iv_tile) {
-    issue_step(0, 0);
-    if (steps > 1) issue_step(1, 1);
-    if (steps > 2) issue_step(2, 2);
-    wait_step(-1, steps);   // blocks 0 and 1 landed
+    bf16x8* x = &sXbuf[VM & 1][pair][0][lane];
+    x[0] = to_operand(s, 0);
+    x[64] = to_operand(s, 8);
+    x[128] = to_operand(dp, 0);
+    x[192] = to_operand(dp, 8);
     __syncthreads();
-    scores_mfma(0, 0);
-    scores_valu(0, 0, pf, dsf);
-    for (int st = 0; st + 1 < steps; ++st) {
-      if (st + 3 < steps) issue_step(st + 3, (st + 3) % NBUF);
-      scores_mfma(st, 1);
-      accumulate(st, 0, pf, dsf);
-      scores_valu(st, 1, pf, dsf);
-      scores_mfma(st + 1, 0);
-      accumulate(st, 1, pf, dsf);
-      scores_valu(st + 1, 0, pf, dsf);
-      wait_step(st, steps);
-      __syncthreads();
+  };
+  using std::integral_constant;
+  for (int v0 = 0; v0 < n_units; v0 += 6) {
+    unit(integral_constant<int, 0>{}, v0);
+    unit(integral_constant<int, 1>{}, v0 + 1);
+    if (v0 + 2 < n_units) {
+      unit(integral_constant<int, 2>{}, v0 + 2);
+      unit(integral_constant<int, 3>{}, v0 + 3);
     }
-    scores_mfma(steps - 1, 1);
-    accumulate(steps - 1, 0, pf, dsf);
-    scores_valu(steps - 1, 1, pf, dsf);
-    accumulate(steps - 1, 1, pf, dsf);
-  } else {
-    // The step count is padded to a multiple of NBUF with steps that see
-    // nothing (they reload the last block, so every operand is finite), and
-    // the loop is unrolled NBUF times: every LDS buffer index is then a
-    // compile-time constant and the fragment reads use immediate offsets.
-    // The last step starts a unit past the end whose results are dropped.
-    using yes = std::true_type;
-    const int steps_pad = (steps + NBUF - 1) / NBUF * NBUF;
-    static_assert(NBUF == 4, "unrolled four times");
-    issue_step(0, 0);
-    issue_step(1, 1);
-    issue_step(2, 2);
-    wait_step(-1, steps_pad);   // blocks 0 and 1 landed
-    __syncthreads();
-    // unit (0, 0): S/dP into set 0, its context, elements 0..7
-    load_ctx(0, 0, 0);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      sc[0][r] = 0.f;
-      dc[0][r] = 0.f;
-    }
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      sc[0] = mfma32(ld_row_swz<D>(qtile(0), c, ks * 2 + g), kf[ks], sc[0]);
-      dc[0] = mfma32(ld_row_swz<D>(dotile(0), c, ks * 2 + g), vf[ks], dc[0]);
-    }
-#pragma unroll
-    for (int r = 0; r < 8; ++r) elem(0, r);
-    auto iter = [&](int st, int u) {   // u = st % NBUF, a constant at each call
-      if (st + 3 < steps_pad) issue_step(st + 3, (u + 3) & 3);
-      phaseX(yes{}, 0, st, 1, pf, dsf, u);                           // S/dP of (st, 1); finish (st, 0)
-      phaseY(yes{}, st, 0, pf, dsf, 1, st, 1, u, u);                 // dV/dK of (st, 0); start (st, 1)
-      phaseX(yes{}, 1, st + 1, 0, pf, dsf, (u + 1) & 3);             // S/dP of (st+1, 0); finish (st, 1)
-      phaseY(yes{}, st, 1, pf, dsf, 0, st + 1, 0, u, (u + 1) & 3);   // dV/dK of (st, 1); start (st+1, 0)
-      wait_step(st, steps_pad);
-      __syncthreads();
-    };
-    for (int st = 0; st < steps_pad; st += NBUF) {
-      iter(st, 0);
-      iter(st + 1, 1);
-      iter(st + 2, 2);
-      iter(st + 3, 3);
+    if (v0 + 4 < n_units) {
+      unit(integral_constant<int, 4>{}, v0 + 4);
+      unit(integral_constant<int, 5>{}, v0 + 5);
     }
   }
-
-  if (!kok) return;
-  if (slot < 0) {
-    u16* pk = a.dk + (size_t(key) * a.Hkv + hk) * D;
-    u16* pv = a.dv + (size_t(key) * a.Hkv + hk) * D;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int d0 = db * 32 + q4 * 8 + g * 4;
-        uint2 wk, wv;
-        wk.x = pack2(dk[db][q4 * 4 + 0] * a.scale, dk[db][q4 * 4 + 1] * a.scale);
-        wk.y = pack2(dk[db][q4 * 4 + 2] * a.scale, dk[db][q4 * 4 + 3] * a.scale);
-        wv.x = pack2(dv[db][q4 * 4 + 0], dv[db][q4 * 4 + 1]);
-        wv.y = pack2(dv[db][q4 * 4 + 2], dv[db][q4 * 4 + 3]);
-        *reinterpret_cast<uint2*>(pk + d0) = wk;
-        *reinterpret_cast<uint2*>(pv + d0) = wv;
-      }
-  } else {
-    float* base = a.partial + (size_t(slot) * a.Hkv + hk) * 2 * BK * D;
-    float* pk = base + size_t(wave * 32 + c) * D;
-    float* pv = base + size_t(BK) * D + size_t(wave * 32 + c) * D;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int d0 = db * 32 + q4 * 8 + g * 4;
-        *reinterpret_cast<float4*>(pk + d0) =
-            make_float4(dk[db][q4 * 4 + 0] * a.scale, dk[db][q4 * 4 + 1] * a.scale,
-                        dk[db][q4 * 4 + 2] * a.scale, dk[db][q4 * 4 + 3] * a.scale);
-        *reinterpret_cast<float4*>(pv + d0) =
-            make_float4(dv[db][q4 * 4 + 0], dv[db][q4 * 4 + 1], dv[db][q4 * 4 + 2],
-                        dv[db][q4 * 4 + 3]);
-      }
-  }
+  __syncthreads();   // the interval of the last unit's dV/dK
 }
 
 // Sum the fp32 partial tiles of every split key tile in slot order.
@@ -749,7 +655,7 @@ hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float 
     { ProfScope p("attn_bwd_pre", stream, profile);
       hipLaunchKernelGGL(pre, g_pre, b256, 0, stream, a); }
     { ProfScope p("attn_bwd_dkdv", stream, profile);
-      hipLaunchKernelGGL(dkdv, g_kv, b256, 0, stream, a); }
+      hipLaunchKernelGGL(dkdv, g_kv, dim3(512), 0, stream, a); }
     if (n_red) {
       ProfScope p("attn_bwd_reduce", stream, profile);
       hipLaunchKernelGGL(red, g_red, b256, 0, stream, a, n_red);

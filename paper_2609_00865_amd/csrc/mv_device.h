@@ -221,7 +221,9 @@ struct KvTileLoader {
   static_assert(KLD >= 1, "tile too small for 256 threads");
   int row[KLD];
   uint32_t col[KLD];   // byte offset of the loaded chunk within its row
-  __device__ __forceinline__ explicit KvTileLoader(int tid) {
+  uint32_t wv;         // LDS byte offset of this thread's wave within a tile
+  // tid: the thread's index among the 256 that load (0..255)
+  __device__ __forceinline__ explicit KvTileLoader(int tid) : wv(uint32_t(tid >> 6) * 1024) {
 #pragma unroll
     for (int r = 0; r < KLD; ++r) {
       const int P = (r * 4 + (tid >> 6)) * 64 + (tid & 63);
@@ -233,7 +235,6 @@ struct KvTileLoader {
   // loads per thread)
   __device__ __forceinline__ void issue_one(rsrc_t rs, int kt, int T, uint32_t kv_row,
                                             uint32_t lds) const {
-    const uint32_t wv = uint32_t(threadIdx.x >> 6) * 1024;
 #pragma unroll
     for (int r = 0; r < KLD; ++r) {
       const uint32_t off = uint32_t(min(kt * BK + row[r], T - 1)) * kv_row + col[r];
@@ -243,7 +244,6 @@ struct KvTileLoader {
   // K and V of key tile kt into the tiles at LDS byte addresses ldsK, ldsV
   __device__ __forceinline__ void issue(rsrc_t krs, rsrc_t vrs, int kt, int T, uint32_t kv_row,
                                         uint32_t ldsK, uint32_t ldsV) const {
-    const uint32_t wv = uint32_t(threadIdx.x >> 6) * 1024;
 #pragma unroll
     for (int r = 0; r < KLD; ++r) {
       const uint32_t off = uint32_t(min(kt * BK + row[r], T - 1)) * kv_row + col[r];
