@@ -149,11 +149,13 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
   sOmbuf[tid % BK] = omreg;   // identical copies
   if (e0 + 1 < e1) issue_tile(sload_i32(a.mask.k_list + e0 + 1) >> 1, 1);
   __syncthreads();
-  for (int e = e0; e < e1; ++e) {
+  // tile e in buffer BUF = (e - e0) & 1, a compile-time constant in each
+  // half of the loop below (LDS addresses fold into immediate offsets)
+  auto tile = [&](auto buf_tag, int e) {
+    constexpr int buf = decltype(buf_tag)::value;
     const int ent = sload_i32(a.mask.k_list + e);
     const int kt = ent >> 1;
     const bool full = ent & 1;
-    const int buf = (e - e0) & 1;
     const char* sK = reinterpret_cast<const char*>(sKbuf + buf * BK * D);
     const char* sV = reinterpret_cast<const char*>(sVbuf + buf * BK * D);
     const int* sOm = sOmbuf + buf * BK;
@@ -221,6 +223,10 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
     if (e + 1 < e1) sOmbuf[(buf ^ 1) * BK + tid % BK] = omreg;
     __syncthreads();
     if (e + 2 < e1) issue_tile(sload_i32(a.mask.k_list + e + 2) >> 1, buf);
+  };
+  for (int e = e0; e < e1; e += 2) {
+    tile(std::integral_constant<int, 0>{}, e);
+    if (e + 1 < e1) tile(std::integral_constant<int, 1>{}, e + 1);
   }
 
   if (!qok) return;
