@@ -138,6 +138,19 @@ enum {
 mv_status mv_build_view_mask(const mv_trajectory* trajs, int32_t n_traj,
                              int32_t total_tokens, mv_view_mask** out);
 
+/*
+ * As mv_build_view_mask, with the tile shape of the forward / dQ schedule
+ * named: tile_q query rows x tile_k keys.  The kernels are compiled for
+ * MV_TILE_Q x MV_TILE_K (the dK/dV pass walks 128-key tiles in 64-row
+ * blocks); any other shape is refused with MV_ERR_UNSUPPORTED before anything
+ * is built, so a caller that assumes a tiling learns at once that it differs.
+ */
+#define MV_TILE_Q 128
+#define MV_TILE_K 64
+mv_status mv_build_view_mask_tiled(const mv_trajectory* trajs, int32_t n_traj,
+                                   int32_t total_tokens, int32_t tile_q, int32_t tile_k,
+                                   mv_view_mask** out);
+
 /* As mv_build_view_mask, for kind MV_VIEW_LIVE or MV_VIEW_FINAL. */
 mv_status mv_build_view_mask_kind(const mv_trajectory* trajs, int32_t n_traj,
                                   int32_t total_tokens, int32_t kind, mv_view_mask** out);

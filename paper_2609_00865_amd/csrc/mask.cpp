@@ -429,6 +429,20 @@ mv_status mv_build_view_mask(const mv_trajectory* trajs, int32_t n_traj, int32_t
   return mv_build_view_mask_kind(trajs, n_traj, total_tokens, MV_VIEW_LIVE, out);
 }
 
+mv_status mv_build_view_mask_tiled(const mv_trajectory* trajs, int32_t n_traj,
+                                   int32_t total_tokens, int32_t tile_q, int32_t tile_k,
+                                   mv_view_mask** out) {
+  static_assert(MV_TILE_Q == mv::kFwdTileQ && MV_TILE_K == mv::kFwdTileK,
+                "the header's tile shape is the kernels'");
+  if (tile_q != MV_TILE_Q || tile_k != MV_TILE_K) {
+    std::ostringstream os;
+    os << "tile shape " << tile_q << " x " << tile_k << " unsupported: the kernels are built for "
+       << MV_TILE_Q << " x " << MV_TILE_K;
+    return bad(MV_ERR_UNSUPPORTED, os.str());
+  }
+  return mv_build_view_mask(trajs, n_traj, total_tokens, out);
+}
+
 mv_status mv_view_mask_leaves(const mv_view_mask* m, int32_t* tokens, int32_t* teacher_rows,
                               int32_t* student_rows, int32_t capacity, int32_t* n_out) {
   if (m == nullptr || n_out == nullptr) return bad(MV_ERR_INVALID_ARG, "null argument");

@@ -115,6 +115,9 @@ mv_last_error = _sig("mv_last_error", ctypes.c_char_p)
 mv_version = _sig("mv_version", _i32)
 mv_build_view_mask = _sig("mv_build_view_mask", ctypes.c_int, _P(TrajectoryC), _i32, _i32,
                           _P(_vp))
+mv_build_view_mask_tiled = _sig("mv_build_view_mask_tiled", ctypes.c_int, _P(TrajectoryC), _i32,
+                                _i32, _i32, _i32, _P(_vp))
+TILE_Q, TILE_K = 128, 64   # the forward / dQ tile shape the kernels are built for
 mv_build_view_mask_kind = _sig("mv_build_view_mask_kind", ctypes.c_int, _P(TrajectoryC), _i32,
                                _i32, _i32, _P(_vp))
 mv_view_mask_leaves = _sig("mv_view_mask_leaves", ctypes.c_int, _vp, _vp, _vp, _vp, _i32,
@@ -202,6 +205,7 @@ EXPORTED = ["mv_status_string", "mv_last_error", "mv_version", "mv_build_view_ma
             "mv_view_mask_intervals", "mv_token_logprob_bad_targets", "mv_attn_bwd_noalloc",
             "mv_build_shared_trunk_pack", "mv_token_logprob_grpo_workspace_bytes",
             "mv_token_logprob_grpo", "mv_pack_rows_rope", "mv_unpack_rows_sum_rope",
+            "mv_build_view_mask_tiled",
             "mv_profile_enable", "mv_profile_read"]
 
 VIEW_LIVE, VIEW_FINAL = 0, 1

@@ -156,6 +156,27 @@ def test_mask_buffer_errors():
     assert _status(mv.mv_build_view_mask(None, 0, 10, ctypes.byref(h))) == "MV_ERR_INVALID_ARG"
 
 
+def test_tiled_builder_accepts_only_the_kernels_tiles():
+    """The builder that names a tile shape builds the same mask for the
+    kernels' own shape and refuses any other before building anything."""
+    trajs = synth.make_trajectories("tiny", 0)
+    tc, keep = mv._trajectories_c(trajs)
+    T = trajs[-1].end
+    h = ctypes.c_void_p()
+    assert _status(mv.mv_build_view_mask_tiled(tc, len(trajs), T, mv.TILE_Q, mv.TILE_K,
+                                               ctypes.byref(h))) == "MV_OK"
+    st = mv.MaskStats()
+    assert _status(mv.mv_view_mask_stats(h, ctypes.byref(st))) == "MV_OK"
+    assert st.visible_pairs == mv.ViewMask(trajs).stats()["visible_pairs"]
+    mv.mv_view_mask_free(h)
+    for tq, tk in ((64, 64), (128, 128), (256, 64), (0, 0)):
+        h2 = ctypes.c_void_p()
+        assert _status(mv.mv_build_view_mask_tiled(tc, len(trajs), T, tq, tk,
+                                                   ctypes.byref(h2))) == "MV_ERR_UNSUPPORTED"
+        assert not h2.value
+        assert b"unsupported" in mv.mv_last_error()
+
+
 def test_binding_has_no_fallback():
     """The binding is marshalling only: it never imports the oracle."""
     src = open(os.path.join(ROOT, "paper_2609_00865_amd", "mv.py")).read()
