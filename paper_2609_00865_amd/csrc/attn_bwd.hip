@@ -164,23 +164,32 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
     // with restoring edits) walks the interval lists
     const bool tile_iv = IV && !full && __any(sOm[lane] < 0);
 
-    // the tile's two 32-key halves one after the other: S^T and dP^T of a
-    // half, its dS^T, then its share of dQ^T (half the live accumulators)
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x16 s, dp;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] = 0.f;
-        dp[r] = 0.f;
+    // The tile's MFMAs in one fixed sequence: S^T and dP^T of key half 0,
+    // of half 1, then dQ^T += K^T dS^T of both halves.  The vector work of
+    // a half runs beside the MFMAs that follow it: the exponentials of S
+    // beside its dP MFMAs, half 0's dS beside half 1's S MFMAs, half 1's dS
+    // beside half 0's dQ MFMAs; only the mask of a partial tile runs alone.
+    constexpr int NS = 2 * KS;            // S and dP MFMAs of one half
+    constexpr int NM = 2 * NS + 4 * DB;   // MFMAs of the tile
+    f32x16 s[2], dp[2];
+    bf16x8 dsf[2][2];
+    auto opnd = [&](int m) {   // A operand of MFMA m
+      if (m < 2 * NS) {
+        const int kb = m / NS, j = m % NS;
+        return ld_row_swz<D>(j < KS ? sK : sV, kb * 32 + c, (j % KS) * 2 + g);
       }
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        s = mfma32(ld_row_swz<D>(sK, kb * 32 + c, ks * 2 + g), qf[ks], s);
-        dp = mfma32(ld_row_swz<D>(sV, kb * 32 + c, ks * 2 + g), df[ks], dp);
+      const int q = m - 2 * NS, kb = q / (2 * DB), db = (q % (2 * DB)) >> 1, kk = q & 1;
+      return ld_tr_swz<D>(sK, (2 * kb + kk) * 16, db * 32);   // K^T, keys (2 kb + kk) * 16..
+    };
+    auto expo = [&](int kb, int i) { s[kb][i] = fast_exp2(fmaf(s[kb][i], a.scale_log2, -lse2)); };
+    auto dso = [&](int kb, int i) {
+      dp[kb][i] = s[kb][i] * (dp[kb][i] - Di);
+      if ((i & 7) == 7) {
+        dsf[kb][i >> 3] = to_operand(dp[kb], i & 8);
+        asm volatile("" : "+v"(dsf[kb][i >> 3]));   // keeps it in its slot
       }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
+    };
+    auto mask = [&](int kb) {   // partial tiles only (block-uniform)
       if (tile_iv) {
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
@@ -190,10 +199,11 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
           for (int u = 0; u < 4; ++u) {
             const int r = q4 * 4 + u;
             const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
-            s[r] = mv_visible_iv(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv) ? s[r] : 0.f;
+            s[kb][r] = mv_visible_iv(qrow, key, omv[u], a.mask.iv_ptr, a.mask.iv) ? s[kb][r] : 0.f;
           }
         }
-      } else if (!full) {  // block-uniform; per element a select, not a branch
+      } else {   // per element a select, not a branch
+        const int di = qrow - (j0 + g * 4);   // keys relative to the lane's first
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           const int4 om = *reinterpret_cast<const int4*>(&sOm[kb * 32 + q4 * 8 + g * 4]);
@@ -201,22 +211,51 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
             const int r = q4 * 4 + u;
-            const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
-            s[r] = mv_visible(qrow, key, omv[u]) ? s[r] : 0.f;
+            const int jo = kb * 32 + q4 * 8 + u;   // key j0 + g * 4 + jo
+            s[kb][r] = mv_visible_rel(di, jo, qrow, omv[u]) ? s[kb][r] : 0.f;
           }
         }
       }
+    };
+    // vector work of slot m: elements [16 (m - b) / n, 16 (m - b + 1) / n)
+    // of a stretch of n slots starting at b
+    auto spread = [&](int m, int b, int n, auto&& f) {
+      if (m >= b && m < b + n) {
+        const int i0 = 16 * (m - b) / n, i1 = 16 * (m - b + 1) / n;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = s[r] * (dp[r] - Di);
-      const bf16x8 dsf[2] = {to_operand(s, 0), to_operand(s, 8)};
+        for (int i = i0; i < i1; ++i) f(i);
+      }
+    };
+    bf16x8 op[3];
+    op[0] = opnd(0);
+    op[1] = opnd(1);
+    __builtin_amdgcn_sched_barrier(0);
+    auto slot = [&](int m) {
+      if (m + 2 < NM) op[(m + 2) % 3] = opnd(m + 2);
+      if (m < 2 * NS) {
+        const int kb = m / NS, j = m % NS;
+        if (j < KS)
+          s[kb] = mfma32(op[m % 3], qf[j], j == 0 ? f32x16{} : s[kb]);
+        else
+          dp[kb] = mfma32(op[m % 3], df[j - KS], j == KS ? f32x16{} : dp[kb]);
+      } else {
+        const int q = m - 2 * NS, kb = q / (2 * DB), db = (q % (2 * DB)) >> 1, kk = q & 1;
+        acc[db] = mfma32(op[m % 3], dsf[kb][kk], acc[db]);
+      }
+      spread(m, KS + 1, KS - 1, [&](int i) { expo(0, i); });
+      spread(m, NS + 1, KS - 1, [&](int i) { dso(0, i); });
+      spread(m, NS + KS + 1, KS - 1, [&](int i) { expo(1, i); });
+      spread(m, 2 * NS + 1, 2 * DB - 1, [&](int i) { dso(1, i); });
+      __builtin_amdgcn_sched_barrier(0);
+    };
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
+    for (int m = 0; m < NS; ++m) slot(m);
+    if (!full) mask(0);
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          // K^T operand: column block db of keys (2 kb + kk)*16.. in accumulator order
-          acc[db] = mfma32(ld_tr_swz<D>(sK, (2 * kb + kk) * 16, db * 32), dsf[kk], acc[db]);
-        }
-    }
+    for (int m = NS; m < 2 * NS; ++m) slot(m);
+    if (!full) mask(1);
+#pragma unroll
+    for (int m = 2 * NS; m < NM; ++m) slot(m);
     // tile e+1 has landed (and its omega values are written) before the
     // barrier that publishes it; then tile e's buffer takes tile e+2
     wait_vmcnt<0>();

@@ -131,6 +131,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) s[kb][r] = (vis >> (kb * 16 + r)) & 1u ? s[kb][r] : -INFINITY;
       } else {
+        const int di = qrow - (j0 + g * 4);   // keys relative to the lane's first
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -140,8 +141,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
               const int r = q4 * 4 + u;
-              const int key = j0 + kb * 32 + q4 * 8 + g * 4 + u;
-              s[kb][r] = mv_visible(qrow, key, omv[u]) ? s[kb][r] : -INFINITY;
+              const int jo = kb * 32 + q4 * 8 + u;   // key j0 + g * 4 + jo
+              s[kb][r] = mv_visible_rel(di, jo, qrow, omv[u]) ? s[kb][r] : -INFINITY;
             }
           }
       }
@@ -286,6 +287,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
           const int i0 = 32 * (st - 1) / NS, i1 = 32 * st / NS;
 #pragma unroll
           for (int i = i0; i < i1; ++i) mx = fmaxf(mx, nxt[i >> 4][i & 15]);
+          // keeps the max in its slot: it is only read under the branch
+          // below, into which the compiler would otherwise sink the whole
+          // chain, after the last MFMA
+          asm volatile("" : "+v"(mx));
         }
         __builtin_amdgcn_sched_barrier(0);
       }

@@ -16,6 +16,14 @@
 // instead of branching per element)
 MV_HD bool mv_visible(int i, int j, int omega_j) { return (j <= i) & (i < omega_j); }
 
+// The same test with the key given by its offset from a base key b: jo = j -
+// b and di = i - b (j <= i iff jo <= di).  Kernels take b per lane and tile,
+// so that jo is a compile-time constant per score element and the diagonal
+// test compares against an immediate.
+MV_HD bool mv_visible_rel(int di, int jo, int i, int omega_j) {
+  return (jo <= di) & (i < omega_j);
+}
+
 // A key that a later edit restores has further live intervals.  Such a key is
 // stored with the sign bit of omega set (the low 31 bits keep the end of its
 // first interval) and its other intervals [b, e) in a per-key list: iv[2k],
