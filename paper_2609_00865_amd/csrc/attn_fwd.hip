@@ -13,9 +13,9 @@
 // Each wave runs a two-stage software pipeline over the tile list: while the
 // score MFMAs of tile t+1 run, the vector ALU turns tile t's scores into
 // probabilities; while the PV MFMAs of tile t run, it masks tile t+1 and
-// takes its row maxima.  K and V have separate double buffers with their own
-// turns (two barriers per tile), so each load has about one and a half tiles
-// to land.  Query tiles are visited heaviest first and the heads of one query
+// takes its row maxima.  K and V have double buffers and one barrier per
+// step: after it, tile t+2's K and tile t+1's V go into the buffers the
+// previous step finished with, so each load has one step to land.  Query tiles are visited heaviest first and the heads of one query
 // tile are kept on one XCD so that GQA heads share K/V in that XCD's L2.
 #include <type_traits>
 
@@ -90,8 +90,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   const rsrc_t vrs = make_rsrc(a.v + size_t(hk) * D, kv_bytes);
   const rsrc_t omrs = make_rsrc(a.mask.omega, uint32_t(T) * 4);
   const KvTileLoader<D, BK> ldr(tid);
-  // (block-uniform: the tile list is read with scalar loads, only right
-  // after barriers, where no LDS read is outstanding)
+  // (block-uniform: the tile list is read with scalar loads, where no LDS
+  // read is outstanding: such a load waits on lgkmcnt, which counts both)
   const int e0 = __builtin_amdgcn_readfirstlane(a.mask.q_ptr[qt]);
   const int n = __builtin_amdgcn_readfirstlane(a.mask.q_ptr[qt + 1]) - e0;   // >= 1
   const int* klist = a.mask.k_list + e0;
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     }
   };
 
-  // ---- prologue: K0, K1, V0 (the issue order the pipeline's waits assume)
+  // ---- prologue: K0, K1, V0 (the issue order the first wait assumes)
   issue_k(0);
   if (n > 1) issue_k(1);
   issue_v(0);
@@ -190,8 +190,6 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   }
   mask_tile(sc[0], 0);
   rescale(tile_max(sc[0]));
-  __syncthreads();                      // every wave is done with K0's buffer
-  if (n > 2) issue_k(2);
 
   // ---- one pipeline step: tile t (scores in set P) and tile t+1 (scores
   // into set P ^ 1).  On the last tile (no t+1) the score MFMAs still run,
@@ -203,13 +201,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     f32x16 (&nxt)[2] = sc[P ^ 1];
     const bool next = t + 1 < n;   // block-uniform
 
-    // barrier 1: K[t+1] landed (loads issued after it: V[t], K[t+2])
-    if (t + 2 < n)
-      wait_vmcnt<NL + NLK>();
-    else if (next)
-      wait_vmcnt<NL>();
+    // one barrier per step: K[t+1] and V[t] landed, every wave done with
+    // K[t] and V[t-1]; then K[t+2] and V[t+1] go into their buffers
+    wait_vmcnt<0>();
     __syncthreads();
-    if (next) issue_v(t + 1);   // into V[t-1]'s buffer (read before this barrier)
+    if (t + 2 < n) issue_k(t + 2);
+    if (next) issue_v(t + 1);
 
     // phase 1: S^T of tile t+1 (16 MFMAs) with the exponentials of tile t's
     // elements 0..23 (spread evenly over the MFMA slots) and their bf16
@@ -251,15 +248,6 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     }
     asm volatile("" : "+v"(psum));
 
-    // barrier 2: V[t] landed (loads issued after it: K[t+2], V[t+1])
-    if (t + 2 < n)
-      wait_vmcnt<NLK + NL>();
-    else if (next)
-      wait_vmcnt<NL>();
-    else
-      wait_vmcnt<0>();
-    __syncthreads();
-    if (t + 3 < n) issue_k(t + 3);   // into K[t+1]'s buffer (read in phase 1)
     if (next) mask_tile(nxt, t + 1);
 
     // phase 2: O^T += V^T P^T of tile t (16 MFMAs, V^T read four ahead) with
