@@ -178,7 +178,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
         const int kb = m / NS, j = m % NS;
         return ld_row_swz<D>(j < KS ? sK : sV, kb * 32 + c, (j % KS) * 2 + g);
       }
-      const int q = m - 2 * NS, kb = q / (2 * DB), db = (q % (2 * DB)) >> 1, kk = q & 1;
+      const int q = m - 2 * NS, kb = q / (2 * DB), kk = (q % (2 * DB)) / DB, db = q % DB;
       return ld_tr_swz<D>(sK, (2 * kb + kk) * 16, db * 32);   // K^T, keys (2 kb + kk) * 16..
     };
     auto expo = [&](int kb, int i) { s[kb][i] = fast_exp2(fmaf(s[kb][i], a.scale_log2, -lse2)); };
@@ -239,7 +239,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
         else
           dp[kb] = mfma32(op[m % 3], df[j - KS], j == KS ? f32x16{} : dp[kb]);
       } else {
-        const int q = m - 2 * NS, kb = q / (2 * DB), db = (q % (2 * DB)) >> 1, kk = q & 1;
+        const int q = m - 2 * NS, kb = q / (2 * DB), kk = (q % (2 * DB)) / DB, db = q % DB;
         acc[db] = mfma32(op[m % 3], dsf[kb][kk], acc[db]);
       }
       spread(m, KS + 1, KS - 1, [&](int i) { expo(0, i); });
@@ -412,10 +412,11 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a) {
       const bf16x8 pf[2] = {x[0], x[64]}, dsf[2] = {x[128], x[192]};
       const char* sQ = qtile(buf);
       const char* sdO = dotile(buf);
-      // MFMA q: db = q / 4, kk = (q / 2) % 2, dV (even q) or dK (odd q);
-      // operands read two MFMAs ahead
+      // MFMA q: dV (even q) or dK (odd q) of db = (q / 2) % DB, operand kk =
+      // q / (2 DB) (db before kk, so that no two neighbouring MFMAs of one
+      // kind share an accumulator); operands read two MFMAs ahead
       auto opnd = [&](int q) {
-        return ld_tr_swz<D>((q & 1) ? sQ : sdO, (2 * mb + ((q >> 1) & 1)) * 16, (q >> 2) * 32);
+        return ld_tr_swz<D>((q & 1) ? sQ : sdO, (2 * mb + q / (2 * DB)) * 16, ((q >> 1) % DB) * 32);
       };
       constexpr int NQ = 4 * DB;
       bf16x8 op[3];
@@ -424,7 +425,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a) {
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
         if (q + 2 < NQ) op[(q + 2) % 3] = opnd(q + 2);
-        const int db = q >> 2, kk = (q >> 1) & 1;
+        const int db = (q >> 1) % DB, kk = q / (2 * DB);
         if (q & 1)
           dk[db] = mfma32(op[q % 3], dsf[kk], dk[db]);
         else
