@@ -2,7 +2,8 @@
 // trajectory instead of one per branch (Section 4.3, "Cost and deployment
 // splits").  Three passes, all recomputing P from the forward's LSE:
 //
-//  1. D_i = <dO_i, O_i> per row and head, and the row's LSE in base-2 units
+//  1. -D_i = -<dO_i, O_i> per row and head (the value dQ's dP chains start
+//     from, so its MFMAs deliver dP - D) and the row's LSE in base-2 units
 //     (HBM-bound, tiny).
 //  2. dQ: per 128-row query tile and head, over the forward's tile list:
 //     S^T = K Q^T, dP^T = V dO^T, dS^T = P^T o (dP^T - D), dQ^T += K^T dS^T.
@@ -36,7 +37,7 @@ struct BwdArgs {
   u16* dq;
   u16* dk;
   u16* dv;
-  float* Dd;       // [Hq, T]
+  float* Dd;       // [Hq, T] -D = -rowsum(dO o O)
   float* L2;       // [Hq, T] LSE in base-2 units (LSE * log2 e), written by pass 1
   float* partial;  // [n_slots, Hkv, 2, 128, D]
   mv_mask_dev mask;
@@ -45,7 +46,7 @@ struct BwdArgs {
 };
 
 // ---------------------------------------------------------------------------
-// 1. D = rowsum(dO * O)
+// 1. -D = -rowsum(dO * O)
 // ---------------------------------------------------------------------------
 // D/8 consecutive lanes share one (row, head) vector, 16 bytes each, so a
 // wave reads whole contiguous rows; the partial dot products are summed
@@ -71,7 +72,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
   for (int m = LPV / 2; m > 0; m >>= 1) acc += __shfl_xor(acc, m);
   if (ok && gid % LPV == 0) {
     const int i = int(vec / a.Hq), h = int(vec % a.Hq);
-    a.Dd[size_t(h) * a.T + i] = acc;
+    a.Dd[size_t(h) * a.T + i] = -acc;
     a.L2[size_t(h) * a.T + i] = a.lse[size_t(h) * a.T + i] * kLog2e;
   }
 }
@@ -114,7 +115,12 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
     }
   }
   const float lse2 = qok ? a.lse[size_t(h) * T + qrow] * kLog2e : 0.f;
-  const float Di = qok ? a.Dd[size_t(h) * T + qrow] : 0.f;
+  // -D_i in every element: the dP^T chain starts from it, so its MFMAs
+  // deliver dP - D (lane = query row) and dS = P o (dP - D) is one multiply
+  const float nDi = qok ? a.Dd[size_t(h) * T + qrow] : 0.f;
+  f32x16 negD;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) negD[r] = nDi;
 
   f32x16 acc[DB];
 #pragma unroll
@@ -182,8 +188,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       return ld_tr_swz<D>(sK, (2 * kb + kk) * 16, db * 32);   // K^T, keys (2 kb + kk) * 16..
     };
     auto expo = [&](int kb, int i) { s[kb][i] = fast_exp2(fmaf(s[kb][i], a.scale_log2, -lse2)); };
-    auto dso = [&](int kb, int i) {
-      dp[kb][i] = s[kb][i] * (dp[kb][i] - Di);
+    auto dso = [&](int kb, int i) {   // dp already holds dP - D
+      dp[kb][i] = s[kb][i] * dp[kb][i];
       if ((i & 7) == 7) {
         dsf[kb][i >> 3] = to_operand(dp[kb], i & 8);
         asm volatile("" : "+v"(dsf[kb][i >> 3]));   // keeps it in its slot
@@ -237,7 +243,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
         if (j < KS)
           s[kb] = mfma32(op[m % 3], qf[j], j == 0 ? f32x16{} : s[kb]);
         else
-          dp[kb] = mfma32(op[m % 3], df[j - KS], j == KS ? f32x16{} : dp[kb]);
+          dp[kb] = mfma32(op[m % 3], df[j - KS], j == KS ? negD : dp[kb]);
       } else {
         const int q = m - 2 * NS, kb = q / (2 * DB), kk = (q % (2 * DB)) / DB, db = q % DB;
         acc[db] = mfma32(op[m % 3], dsf[kb][kk], acc[db]);
@@ -527,7 +533,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a) {
         s = mfma32(op[j % 3], kf[j >> 1], s);
     }
     const float* sL = sLbuf + buf * BQ;
-    const float* sD = sDbuf + buf * BQ;
+    const float* sD = sDbuf + buf * BQ;   // -D
     const int i0 = (qb0 + st % nqb) * BQ;
     const bool full = (i0 >= j1 - 1) && (i0 + BQ <= om_min);   // block-uniform
 #pragma unroll
@@ -536,7 +542,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a) {
       const float4 l4 = *reinterpret_cast<const float4*>(&sL[qo]);
       const float4 d4 = *reinterpret_cast<const float4*>(&sD[qo]);
       const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-      const float dd[4] = {d4.x, d4.y, d4.z, d4.w};
+      const float nd[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) s[q4 * 4 + e] = fast_exp2(fmaf(s[q4 * 4 + e], a.scale_log2, -lv[e]));
       if (!full) {
@@ -551,7 +557,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a) {
         }
       }
 #pragma unroll
-      for (int e = 0; e < 4; ++e) dp[q4 * 4 + e] = s[q4 * 4 + e] * (dp[q4 * 4 + e] - dd[e]);
+      for (int e = 0; e < 4; ++e) dp[q4 * 4 + e] = s[q4 * 4 + e] * (dp[q4 * 4 + e] + nd[e]);
     }
     bf16x8* x = &sXbuf[VM & 1][pair][0][lane];
     x[0] = to_operand(s, 0);

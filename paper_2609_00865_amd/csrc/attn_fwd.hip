@@ -11,9 +11,12 @@
 // operand is read with the transposing LDS read.
 //
 // Each wave runs a two-stage software pipeline over the tile list: while the
-// score MFMAs of tile t+1 run, the vector ALU turns tile t's scores into
-// probabilities; while the PV MFMAs of tile t run, it masks tile t+1 and
-// takes its row maxima.  K and V have double buffers and one barrier per
+// score MFMAs of tile t+1 run, the vector ALU turns the second half of tile
+// t's scores into probabilities; while the PV MFMAs of tile t run, it turns
+// the first half of tile t+1's.  Tiles take no row maxima: probabilities are
+// taken against a score the row has already seen, and only a tile whose
+// probabilities would grow past 2^16 takes its exact maximum and rescales
+// (a slow path).  K and V have double buffers and one barrier per
 // step: after it, tile t+2's K and tile t+1's V go into the buffers the
 // previous step finished with, so each load has one step to land.  Query tiles are visited heaviest first and the heads of one query
 // tile are kept on one XCD so that GQA heads share K/V in that XCD's L2.
@@ -115,8 +118,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   auto kfrag = [&](const char* sK, int j) {
     return ld_row_swz<D>(sK, (j & 1) * 32 + c, (j >> 1) * 2 + g);
   };
-  // Mask (partial tiles) and row max of tile t's scores in set P: returns
-  // the tile's max in base-2 units (-inf for a row that sees none of it).
+  // Mask of tile t's scores in set s (partial tiles only): invisible scores
+  // become -inf.
   auto mask_tile = [&](f32x16 (&s)[2], int t) {
     const int ent = sload_i32(klist + t);
     if (!(ent & 1)) {   // block-uniform; per element a select, not a branch
@@ -157,19 +160,48 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
     return max_halves(mx) * a.scale_log2;
   };
-  // Lazy rescaling: the running max moves only when a tile's max exceeds it
-  // by more than 8 (base 2); until then p = exp2(x - m_run) <= 2^8, well
-  // inside fp32 and the bf16 operand range, and O and l keep their scale.
-  auto rescale = [&](float m_tile) {
-    const bool grow = m_tile > m_run + 8.f;
-    if (__any(grow)) {
-      const float alpha = grow ? fast_exp2(m_run - m_tile) : 1.f;
-      if (grow) m_run = m_tile;
+  // Probabilities are p = exp2(s * scale_log2 - m_run), where m_run is the
+  // exact maximum of a tile this row has already scored (-inf until the row
+  // has seen a key: then the offset is 0).  Tiles do not take their row
+  // maxima: a tile whose probabilities reach 2^16 in some lane (its lane sum
+  // of p exceeds that), or that a row meets with no key seen yet, takes the
+  // slow path below.  So every p stays <= 2^16, far inside fp32 and the bf16
+  // operand range, and the offset cancels in O = sum p v / sum p.
+  auto m_off = [&]() { return m_run == -INFINITY ? 0.f : m_run; };
+  auto pexp = [&](const f32x16 (&s)[2], int i, float mu) {
+    return fast_exp2(fmaf(s[i >> 4][i & 15], a.scale_log2, -mu));
+  };
+  // Slow path for the tile with scores s: its exact maximum; if that is above
+  // the row's offset, O and l are rescaled to it; then the tile's 32
+  // probabilities are recomputed from the scores (kept unchanged until the
+  // tile's PV products are issued) into the four operands and the lane sum.
+  auto slow_tile = [&](const f32x16 (&s)[2], bf16x8 (&pf)[4], float& psum) {
+    const float m_tile = tile_max(s);
+    if (m_tile > m_run) {
+      const float alpha = fast_exp2(m_run - m_tile);   // 0 when m_run is -inf
+      m_run = m_tile;
       l_run *= alpha;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+    }
+    const float mu = m_off();
+    psum = 0.f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float p[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        p[u] = pexp(s, 8 * k + u, mu);
+        psum += p[u];
+      }
+      uint4 w;
+      w.x = pack2(p[0], p[1]);
+      w.y = pack2(p[2], p[3]);
+      w.z = pack2(p[4], p[5]);
+      w.w = pack2(p[6], p[7]);
+      pf[k] = as_bf16x8(w);
     }
   };
 
@@ -189,12 +221,36 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
       sc[0][j & 1] = mfma32(kfrag(sK, j), qf[j >> 1], j < 2 ? f32x16{} : sc[0][j & 1]);
   }
   mask_tile(sc[0], 0);
-  rescale(tile_max(sc[0]));
+  m_run = tile_max(sc[0]);
+  // operands of a tile, elements 8k .. 8k+7 in pf[k]; elements 0..15 of the
+  // next tile are computed during the current tile's PV products, with their
+  // lane sum in psum_a
+  bf16x8 pf[4];
+  float psum_a = 0.f;
+  {
+    const float mu = m_off();
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      float p[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        p[u] = pexp(sc[0], 8 * k + u, mu);
+        psum_a += p[u];
+      }
+      uint4 w;
+      w.x = pack2(p[0], p[1]);
+      w.y = pack2(p[2], p[3]);
+      w.z = pack2(p[4], p[5]);
+      w.w = pack2(p[6], p[7]);
+      pf[k] = as_bf16x8(w);
+    }
+  }
 
-  // ---- one pipeline step: tile t (scores in set P) and tile t+1 (scores
-  // into set P ^ 1).  On the last tile (no t+1) the score MFMAs still run,
-  // on stale LDS, and their results are dropped: the interleaved phases
-  // stay free of branches.
+  // ---- one pipeline step: tile t (scores in set P, operands 0 and 1 of its
+  // probabilities already in pf) and tile t+1 (scores into set P ^ 1).  On
+  // the last tile (no t+1) the score MFMAs still run, on stale LDS, and their
+  // results and probabilities are dropped: the interleaved phases stay free
+  // of branches.
   auto step = [&](auto par_tag, int t) {
     constexpr int P = decltype(par_tag)::value;
     f32x16 (&cur)[2] = sc[P];
@@ -208,82 +264,89 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     if (t + 2 < n) issue_k(t + 2);
     if (next) issue_v(t + 1);
 
-    // phase 1: S^T of tile t+1 (16 MFMAs) with the exponentials of tile t's
-    // elements 0..23 (spread evenly over the MFMA slots) and their bf16
-    // operands
-    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-    float psum = 0.f;
-    bf16x8 pf[4];
-    auto celem = [&](int i) {
-      const float x = fast_exp2(fmaf(cur[i >> 4][i & 15], a.scale_log2, -m_use));
-      cur[i >> 4][i & 15] = x;
-      psum += x;
-    };
+    // phase 1: S^T of tile t+1 (2 KS MFMAs) with tile t's elements 16..31
+    // (spread evenly over the MFMA slots) and their bf16 operands
+    const float mu = m_off();
+    float psum = psum_a;
     {
       const char* sK = ktile(t + 1);
       bf16x8 kr[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) kr[j] = kfrag(sK, j);
+      float p[16];
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int j = 0; j < 2 * KS; ++j) {
         nxt[j & 1] = mfma32(kr[j & 3], qf[j >> 1], j < 2 ? f32x16{} : nxt[j & 1]);
         if (j + 4 < 2 * KS) kr[j & 3] = kfrag(sK, j + 4);
-        // elements [24 j / NS, 24 (j + 1) / NS) in slot j; operand k (elements
-        // 8k .. 8k+7) packed in the slot that finishes it
         constexpr int NS = 2 * KS;
-        const int i0 = 24 * j / NS, i1 = 24 * (j + 1) / NS;
+        const int i0 = 16 * j / NS, i1 = 16 * (j + 1) / NS;
 #pragma unroll
-        for (int i = i0; i < i1; ++i) celem(i);
-        if (i1 / 8 != i0 / 8) {
+        for (int i = i0; i < i1; ++i) {
+          p[i] = pexp(cur, 16 + i, mu);
+          psum += p[i];
+        }
+        if (i1 / 8 != i0 / 8) {   // operand 2 + k (elements 16 + 8k ..) complete
           const int k = i1 / 8 - 1;
-          pf[k] = to_operand(cur[k >> 1], (k & 1) * 8);
+          uint4 w;
+          w.x = pack2(p[8 * k + 0], p[8 * k + 1]);
+          w.y = pack2(p[8 * k + 2], p[8 * k + 3]);
+          w.z = pack2(p[8 * k + 4], p[8 * k + 5]);
+          w.w = pack2(p[8 * k + 6], p[8 * k + 7]);
+          pf[2 + k] = as_bf16x8(w);
           // an empty asm that consumes the operand keeps its computation in
           // this phase (the compiler would otherwise sink it past the
           // barrier, next to the MFMAs that read it)
-          asm volatile("" : "+v"(pf[k]));
+          asm volatile("" : "+v"(pf[2 + k]));
         }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    asm volatile("" : "+v"(psum));
+    // rows past T never see a key and never ask for the slow path
+    if (__any(!(psum <= 65536.f) || (qok && m_run == -INFINITY))) slow_tile(cur, pf, psum);
+    l_run += psum;
 
     if (next) mask_tile(nxt, t + 1);
 
-    // phase 2: O^T += V^T P^T of tile t (16 MFMAs, V^T read four ahead) with
-    // tile t's elements 24..31 first, then tile t+1's row max
+    // phase 2: O^T += V^T P^T of tile t (4 DB MFMAs, V^T read four ahead)
+    // with tile t+1's elements 0..15; operand k of tile t+1 replaces tile
+    // t's operand k once the MFMAs that read the latter are issued
     {
+      const float mu1 = m_off();
       const char* sV = vtile(t);
       auto vfrag = [&](int st) { return ld_tr_swz<D>(sV, (st / DB) * 16, (st % DB) * 32); };
       bf16x8 vr[4];
 #pragma unroll
       for (int st = 0; st < 4; ++st) vr[st] = vfrag(st);
-      float mx = -INFINITY;
+      float p[16];
+      psum_a = 0.f;
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int st = 0; st < 4 * DB; ++st) {
-        if (st == 0) {
-#pragma unroll
-          for (int i = 24; i < 32; ++i) celem(i);
-          pf[3] = to_operand(cur[1], 8);
-        }
         oacc[st % DB] = mfma32(vr[st & 3], pf[st / DB], oacc[st % DB]);
         if (st + 4 < 4 * DB) vr[st & 3] = vfrag(st + 4);
-        // the next tile's elements, spread over the slots after the first
-        constexpr int NS = 4 * DB - 1;
-        if (st >= 1) {
-          const int i0 = 32 * (st - 1) / NS, i1 = 32 * st / NS;
+        constexpr int NS = 4 * DB;
+        const int i0 = 16 * st / NS, i1 = 16 * (st + 1) / NS;
 #pragma unroll
-          for (int i = i0; i < i1; ++i) mx = fmaxf(mx, nxt[i >> 4][i & 15]);
-          // keeps the max in its slot: it is only read under the branch
-          // below, into which the compiler would otherwise sink the whole
-          // chain, after the last MFMA
-          asm volatile("" : "+v"(mx));
+        for (int i = i0; i < i1; ++i) {
+          p[i] = pexp(nxt, i, mu1);
+          psum_a += p[i];
+        }
+        // operand k of tile t+1 (elements 8k ..) once complete and once the
+        // MFMAs reading tile t's operand k (slots DB k .. DB k + DB - 1) are out
+        if (i1 / 8 != i0 / 8) {
+          const int k = i1 / 8 - 1;
+          uint4 w;
+          w.x = pack2(p[8 * k + 0], p[8 * k + 1]);
+          w.y = pack2(p[8 * k + 2], p[8 * k + 3]);
+          w.z = pack2(p[8 * k + 4], p[8 * k + 5]);
+          w.w = pack2(p[8 * k + 6], p[8 * k + 7]);
+          pf[k] = as_bf16x8(w);
+          asm volatile("" : "+v"(pf[k]));
         }
         __builtin_amdgcn_sched_barrier(0);
       }
-      l_run += psum;
-      if (next) rescale(max_halves(mx) * a.scale_log2);
+      asm volatile("" : "+v"(psum_a));
     }
   };
 

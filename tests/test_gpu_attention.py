@@ -113,6 +113,36 @@ def test_keys_that_re_enter(d, lens, seed):
     assert torch.equal(dev, OA.visibility(trajs))
 
 
+@pytest.mark.parametrize("jump", [False, True])
+def test_scores_far_above_earlier_tiles(jump):
+    """One key every 64 positions scores 20 base-2 units above the previous
+    such key, so that most tiles exceed every score their rows have seen by
+    more than 16 and take the forward's slow path (exact maximum, rescale);
+    with jump, one of those keys scores another 200 units higher, so its
+    probability overflows fp32 unless the slow path recomputes it from the
+    score.  (A steady ramp of all keys would make dQ ill-conditioned: a
+    large key component common to the few keys of each softmax, under dS
+    rows that sum to zero.)"""
+    d, hq, hkv, lens, seed = 128, 2, 1, [700, 300], 41
+    rng = np.random.default_rng(seed)
+    trajs = synth.random_trajectories(rng, lens, max_edits=5, max_span=60, summary_max=20)
+    T = trajs[-1].end
+    gen = torch.Generator().manual_seed(seed)
+    u = torch.randn(d, generator=gen)
+    u = u / u.norm()
+    q = (torch.randn(T, hq, d, generator=gen) * 0.25 + 8.0 * u).to(torch.bfloat16)
+    k = torch.randn(T, hkv, d, generator=gen)
+    c = d ** -0.5 * 1.4426950408889634   # base-2 units per unit of q.k
+    for t in trajs:
+        for m, p in enumerate(range(t.begin + 17, t.end, 64)):
+            x = 20.0 * (m + 1) + (200.0 if jump and m == 4 else 0.0)   # target base-2 score
+            k[p] = k[p] * 0.25 + (x / (8.0 * c)) * u
+    k = k.to(torch.bfloat16)
+    v, do = torch.randn(T, hkv, d, generator=gen), torch.randn(T, hq, d, generator=gen)
+    _check_full(trajs, q, k, v.to(torch.bfloat16), do.to(torch.bfloat16),
+                f"growing scores (jump={jump})")
+
+
 def test_no_compression_is_causal():
     T, hq, hkv, d = 700, 4, 1, 128
     gen = torch.Generator().manual_seed(11)
