@@ -344,7 +344,7 @@ def time_packed(args, mv, synth, trajs, wl, dev, shared):
         return (mv.unpack_rows_sum(pk, dq), mv.unpack_rows_sum(pk, dk),
                 mv.unpack_rows_sum(pk, dv))
 
-    names = ("pack", "pack_rope", "rope", "attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv",
+    names = ("pack", "pack_rope", "rope", "attn_fwd", "attn_bwd_dkdv",
              "attn_bwd_reduce", "attn_bwd_dq", "unpack", "unpack_rope")
 
     def run(layer):
@@ -472,7 +472,7 @@ def time_attention(args, mv, synth, workload, seed, dev):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
     kt = {}
-    for name in ("attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq"):
+    for name in ("attn_fwd", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq"):
         tot, cnt = mv.profile_read(name)
         if cnt:
             kt[name] = round(tot / cnt, 3)

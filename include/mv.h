@@ -594,7 +594,7 @@ float mv_sdcc_lambda(int32_t step, int32_t total_steps, float lambda_max, float 
  * HIP events recorded on the launch stream.  mv_profile_enable(1) clears the
  * previous records; mv_profile_read waits for the recorded events and returns
  * the summed duration (ms) and launch count of the kernels named `kernel`
- * (one of "attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce",
+ * (one of "attn_fwd", "attn_bwd_dkdv", "attn_bwd_reduce",
  * "attn_bwd_dq", "lm_logits", "lm_combine", "lm_grad", "lm_dh", "lm_dw", "kl_logits",
  * "kl_combine", "kl_grad", "kl_dh", "grpo", "pack", "unpack", "rope", "materialize",
  * "ppo_clip").  Not for use

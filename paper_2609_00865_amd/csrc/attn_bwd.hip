@@ -1,13 +1,14 @@
 // View-masked attention backward on gfx950: one backward for the packed
 // trajectory instead of one per branch (Section 4.3, "Cost and deployment
-// splits").  Three passes, all recomputing P from the forward's LSE:
+// splits").  Two passes (and a reduce), all recomputing P from the
+// forward's LSE:
 //
-//  1. -D_i = -<dO_i, O_i> per row and head (the value dQ's dP chains start
-//     from, so its MFMAs deliver dP - D) and the row's LSE in base-2 units
-//     (HBM-bound, tiny).
-//  2. dQ: per 128-row query tile and head, over the forward's tile list:
+//  1. dQ: per 128-row query tile and head, over the forward's tile list:
 //     S^T = K Q^T, dP^T = V dO^T, dS^T = P^T o (dP^T - D), dQ^T += K^T dS^T.
-//  3. dK/dV: per 128-key tile and KV head, over the contiguous row range that
+//     Each row's D = <dO_i, O_i> is taken in the prologue (every row and
+//     head belongs to exactly one block) and stored negated, beside the
+//     row's LSE in base-2 units, for the next pass.
+//  2. dK/dV: per 128-key tile and KV head, over the contiguous row range that
 //     sees some key of the tile, for every query head of the GQA group:
 //     S = Q K^T, dV^T += dO^T P, dP = dO V^T, dK^T += Q^T dS.
 //     Long ranges are cut into items that write fp32 partial tiles; a reduce
@@ -37,8 +38,8 @@ struct BwdArgs {
   u16* dq;
   u16* dk;
   u16* dv;
-  float* Dd;       // [Hq, T] -D = -rowsum(dO o O)
-  float* L2;       // [Hq, T] LSE in base-2 units (LSE * log2 e), written by pass 1
+  float* Dd;       // [Hq, T] -D = -rowsum(dO o O), written by the dQ pass
+  float* L2;       // [Hq, T] LSE in base-2 units (LSE * log2 e), written by the dQ pass
   float* partial;  // [n_slots, Hkv, 2, 128, D]
   mv_mask_dev mask;
   int T, Hq, Hkv, n_qt, n_items;
@@ -46,39 +47,7 @@ struct BwdArgs {
 };
 
 // ---------------------------------------------------------------------------
-// 1. -D = -rowsum(dO * O)
-// ---------------------------------------------------------------------------
-// D/8 consecutive lanes share one (row, head) vector, 16 bytes each, so a
-// wave reads whole contiguous rows; the partial dot products are summed
-// across those lanes.
-template <int D>
-__global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
-  constexpr int LPV = D / 8;   // lanes per vector
-  const int64_t gid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  const int64_t vec = gid / LPV;   // row * Hq + head
-  const bool ok = vec < int64_t(a.T) * a.Hq;
-  float acc = 0.f;
-  if (ok) {
-    const size_t off = size_t(gid) * 8;   // = vec * D + (gid % LPV) * 8
-    const uint4 x = ld16(a.o + off), y = ld16(a.dout + off);
-    const uint32_t xs[4] = {x.x, x.y, x.z, x.w}, ys[4] = {y.x, y.y, y.z, y.w};
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      acc = fmaf(bf16_to_f32(xs[w] & 0xffff), bf16_to_f32(ys[w] & 0xffff), acc);
-      acc = fmaf(bf16_to_f32(xs[w] >> 16), bf16_to_f32(ys[w] >> 16), acc);
-    }
-  }
-#pragma unroll
-  for (int m = LPV / 2; m > 0; m >>= 1) acc += __shfl_xor(acc, m);
-  if (ok && gid % LPV == 0) {
-    const int i = int(vec / a.Hq), h = int(vec % a.Hq);
-    a.Dd[size_t(h) * a.T + i] = -acc;
-    a.L2[size_t(h) * a.T + i] = a.lse[size_t(h) * a.T + i] * kLog2e;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// 2. dQ
+// 1. dQ (and the rows' -D and LSE * log2 e)
 // ---------------------------------------------------------------------------
 template <int D, bool IV>
 __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
@@ -105,19 +74,36 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
   const int qrow = qt * BQ + wave * 32 + c;
   const bool qok = qrow < T;
 
+  // Q and dO of the lane's row (d = ks*16 + g*8 .. +8), and D = <dO, O> of
+  // the row: this lane's half of the products, then the partner lane's
   bf16x8 qf[KS], df[KS];
+  float dsum = 0.f;
   {
     const size_t off = (size_t(qok ? qrow : 0) * a.Hq + h) * D + g * 8;
+    const uint4 z = make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      qf[ks] = as_bf16x8(qok ? ld16(a.q + off + ks * 16) : make_uint4(0, 0, 0, 0));
-      df[ks] = as_bf16x8(qok ? ld16(a.dout + off + ks * 16) : make_uint4(0, 0, 0, 0));
+      qf[ks] = as_bf16x8(qok ? ld16(a.q + off + ks * 16) : z);
+      const uint4 y = qok ? ld16(a.dout + off + ks * 16) : z;
+      const uint4 x = qok ? ld16(a.o + off + ks * 16) : z;
+      df[ks] = as_bf16x8(y);
+      const uint32_t xs[4] = {x.x, x.y, x.z, x.w}, ys[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        dsum = fmaf(bf16_to_f32(xs[w] & 0xffff), bf16_to_f32(ys[w] & 0xffff), dsum);
+        dsum = fmaf(bf16_to_f32(xs[w] >> 16), bf16_to_f32(ys[w] >> 16), dsum);
+      }
     }
   }
+  dsum += __shfl_xor(dsum, 32);
   const float lse2 = qok ? a.lse[size_t(h) * T + qrow] * kLog2e : 0.f;
+  const float nDi = -dsum;
+  if (qok && g == 0) {   // for the dK/dV pass
+    a.Dd[size_t(h) * T + qrow] = nDi;
+    a.L2[size_t(h) * T + qrow] = lse2;
+  }
   // -D_i in every element: the dP^T chain starts from it, so its MFMAs
   // deliver dP - D (lane = query row) and dS = P o (dP - D) is one multiply
-  const float nDi = qok ? a.Dd[size_t(h) * T + qrow] : 0.f;
   f32x16 negD;
 #pragma unroll
   for (int r = 0; r < 16; ++r) negD[r] = nDi;
@@ -289,7 +275,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// 3. dK / dV
+// 2. dK / dV
 // ---------------------------------------------------------------------------
 // One workgroup per (128-key tile, KV head) work item, 8 waves: on each SIMD a
 // score wave (waves 0-3) and an accumulating wave (waves 4-7) share 32 keys.
@@ -692,9 +678,7 @@ hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float 
   a.scale = scale;
   a.scale_log2 = scale * kLog2e;
 
-  const int64_t rows = int64_t(m.T) * Hq;
   const dim3 b256(256);
-  const dim3 g_pre(unsigned((rows * (D / 8) + 255) / 256));
   const int per_xcd_q = (m.n_qt + kNumXcd - 1) / kNumXcd;
   const dim3 g_dq(per_xcd_q * Hq * kNumXcd);
   const int per_xcd_kv = (a.n_items + kNumXcd - 1) / kNumXcd;
@@ -703,26 +687,25 @@ hipError_t launch_attn_bwd(const mv_view_mask& m, int Hq, int Hkv, int D, float 
   const dim3 g_red(unsigned(std::max(1, n_red * Hkv)));
   // the general predicate only when some key has further live intervals
   const bool iv = !m.iv.empty();
-  auto run = [&](auto pre, auto dkdv, auto red, auto dq) {
-    { ProfScope p("attn_bwd_pre", stream, profile);
-      hipLaunchKernelGGL(pre, g_pre, b256, 0, stream, a); }
+  // dQ first: it writes the rows' -D and LSE * log2 e that dK/dV reads
+  auto run = [&](auto dkdv, auto red, auto dq) {
+    { ProfScope p("attn_bwd_dq", stream, profile);
+      hipLaunchKernelGGL(dq, g_dq, b256, 0, stream, a); }
     { ProfScope p("attn_bwd_dkdv", stream, profile);
       hipLaunchKernelGGL(dkdv, g_kv, dim3(512), 0, stream, a); }
     if (n_red) {
       ProfScope p("attn_bwd_reduce", stream, profile);
       hipLaunchKernelGGL(red, g_red, b256, 0, stream, a, n_red);
     }
-    { ProfScope p("attn_bwd_dq", stream, profile);
-      hipLaunchKernelGGL(dq, g_dq, b256, 0, stream, a); }
   };
   if (D == 128 && iv)
-    run(bwd_pre_kernel<128>, bwd_dkdv_kernel<128, true>, bwd_reduce_kernel<128>, bwd_dq_kernel<128, true>);
+    run(bwd_dkdv_kernel<128, true>, bwd_reduce_kernel<128>, bwd_dq_kernel<128, true>);
   else if (D == 128)
-    run(bwd_pre_kernel<128>, bwd_dkdv_kernel<128, false>, bwd_reduce_kernel<128>, bwd_dq_kernel<128, false>);
+    run(bwd_dkdv_kernel<128, false>, bwd_reduce_kernel<128>, bwd_dq_kernel<128, false>);
   else if (iv)
-    run(bwd_pre_kernel<64>, bwd_dkdv_kernel<64, true>, bwd_reduce_kernel<64>, bwd_dq_kernel<64, true>);
+    run(bwd_dkdv_kernel<64, true>, bwd_reduce_kernel<64>, bwd_dq_kernel<64, true>);
   else
-    run(bwd_pre_kernel<64>, bwd_dkdv_kernel<64, false>, bwd_reduce_kernel<64>, bwd_dq_kernel<64, false>);
+    run(bwd_dkdv_kernel<64, false>, bwd_reduce_kernel<64>, bwd_dq_kernel<64, false>);
   return hipGetLastError();
 }
 

@@ -710,7 +710,7 @@ def sdcc_lambda(step: int, total_steps: int, lambda_max: float = 0.1,
 # ---------------------------------------------------------------------------
 # kernel timing
 # ---------------------------------------------------------------------------
-KERNELS = ["attn_fwd", "attn_bwd_pre", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq",
+KERNELS = ["attn_fwd", "attn_bwd_dkdv", "attn_bwd_reduce", "attn_bwd_dq",
            "lm_logits", "lm_target", "lm_combine", "lm_wt", "lm_grad", "lm_dh", "lm_dw",
            "kl_logits", "kl_combine", "kl_wt", "kl_grad", "kl_dh",
            "grpo", "grpo_prep", "grpo_finish", "pack", "unpack", "rope", "pack_rope",
