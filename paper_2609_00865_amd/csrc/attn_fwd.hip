@@ -98,13 +98,16 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   const int e0 = __builtin_amdgcn_readfirstlane(a.mask.q_ptr[qt]);
   const int n = __builtin_amdgcn_readfirstlane(a.mask.q_ptr[qt + 1]) - e0;   // >= 1
   const int* klist = a.mask.k_list + e0;
-  auto issue_k = [&](int t) {   // K tile t and its omega values (NLK loads)
-    const int kt = sload_i32(klist + t) >> 1;
+  // The list entry of tile t (key tile << 1 | full) is read once, with a
+  // scalar load right after a barrier (no LDS read outstanding then), and
+  // passed to the loads and the mask of that tile.
+  auto issue_k = [&](int t, int ent) {   // K tile t and its omega values (NLK loads)
+    const int kt = ent >> 1;
     ldr.issue_one(krs, kt, T, kv_row, lds_addr(sKbuf) + uint32_t(t & 1) * BK * D * 2);
     buf_lds4(omrs, uint32_t(kt * BK + lane) * 4, lds_addr(sOmbuf) + uint32_t(t & 3) * BK * 4);
   };
-  auto issue_v = [&](int t) {   // V tile t (NL loads)
-    const int kt = sload_i32(klist + t) >> 1;
+  auto issue_v = [&](int t, int ent) {   // V tile t (NL loads)
+    const int kt = ent >> 1;
     ldr.issue_one(vrs, kt, T, kv_row, lds_addr(sVbuf) + uint32_t(t & 1) * BK * D * 2);
   };
   auto ktile = [&](int t) { return reinterpret_cast<const char*>(sKbuf + (t & 1) * BK * D); };
@@ -120,8 +123,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   };
   // Mask of tile t's scores in set s (partial tiles only): invisible scores
   // become -inf.
-  auto mask_tile = [&](f32x16 (&s)[2], int t) {
-    const int ent = sload_i32(klist + t);
+  auto mask_tile = [&](f32x16 (&s)[2], int t, int ent) {
     if (!(ent & 1)) {   // block-uniform; per element a select, not a branch
       const int j0 = (ent >> 1) * BK;
       const int* sOm = sOmbuf + (t & 3) * BK;
@@ -206,9 +208,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   };
 
   // ---- prologue: K0, K1, V0 (the issue order the first wait assumes)
-  issue_k(0);
-  if (n > 1) issue_k(1);
-  issue_v(0);
+  const int ent0 = sload_i32(klist);
+  int ent1 = n > 1 ? sload_i32(klist + 1) : 0;   // entry of the next tile
+  issue_k(0, ent0);
+  if (n > 1) issue_k(1, ent1);
+  issue_v(0, ent0);
   if (n > 1)
     wait_vmcnt<NLK + NL>();
   else
@@ -220,7 +224,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     for (int j = 0; j < 2 * KS; ++j)
       sc[0][j & 1] = mfma32(kfrag(sK, j), qf[j >> 1], j < 2 ? f32x16{} : sc[0][j & 1]);
   }
-  mask_tile(sc[0], 0);
+  mask_tile(sc[0], 0, ent0);
   m_run = tile_max(sc[0]);
   // operands of a tile, elements 8k .. 8k+7 in pf[k]; elements 0..15 of the
   // next tile are computed during the current tile's PV products, with their
@@ -261,8 +265,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     // K[t] and V[t-1]; then K[t+2] and V[t+1] go into their buffers
     wait_vmcnt<0>();
     __syncthreads();
-    if (t + 2 < n) issue_k(t + 2);
-    if (next) issue_v(t + 1);
+    const int ent2 = t + 2 < n ? sload_i32(klist + t + 2) : 0;
+    if (t + 2 < n) issue_k(t + 2, ent2);
+    if (next) issue_v(t + 1, ent1);
 
     // phase 1: S^T of tile t+1 (2 KS MFMAs) with tile t's elements 16..31
     // (spread evenly over the MFMA slots) and their bf16 operands
@@ -306,7 +311,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
     if (__any(!(psum <= 65536.f) || (qok && m_run == -INFINITY))) slow_tile(cur, pf, psum);
     l_run += psum;
 
-    if (next) mask_tile(nxt, t + 1);
+    if (next) mask_tile(nxt, t + 1, ent1);
+    ent1 = ent2;
 
     // phase 2: O^T += V^T P^T of tile t (4 DB MFMAs, V^T read four ahead)
     // with tile t+1's elements 0..15; operand k of tile t+1 replaces tile
