@@ -173,6 +173,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
   auto pexp = [&](const f32x16 (&s)[2], int i, float mu) {
     return fast_exp2(fmaf(s[i >> 4][i & 15], a.scale_log2, -mu));
   };
+  // eight probabilities as one bf16 MFMA operand
+  auto pack8 = [](const float* p) {
+    uint4 w;
+    w.x = pack2(p[0], p[1]);
+    w.y = pack2(p[2], p[3]);
+    w.z = pack2(p[4], p[5]);
+    w.w = pack2(p[6], p[7]);
+    return as_bf16x8(w);
+  };
   // Slow path for the tile with scores s: its exact maximum; if that is above
   // the row's offset, O and l are rescaled to it; then the tile's 32
   // probabilities are recomputed from the scores (kept unchanged until the
@@ -198,12 +207,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
         p[u] = pexp(s, 8 * k + u, mu);
         psum += p[u];
       }
-      uint4 w;
-      w.x = pack2(p[0], p[1]);
-      w.y = pack2(p[2], p[3]);
-      w.z = pack2(p[4], p[5]);
-      w.w = pack2(p[6], p[7]);
-      pf[k] = as_bf16x8(w);
+      pf[k] = pack8(p);
     }
   };
 
@@ -241,12 +245,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
         p[u] = pexp(sc[0], 8 * k + u, mu);
         psum_a += p[u];
       }
-      uint4 w;
-      w.x = pack2(p[0], p[1]);
-      w.y = pack2(p[2], p[3]);
-      w.z = pack2(p[4], p[5]);
-      w.w = pack2(p[6], p[7]);
-      pf[k] = as_bf16x8(w);
+      pf[k] = pack8(p);
     }
   }
 
@@ -293,12 +292,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
         }
         if (i1 / 8 != i0 / 8) {   // operand 2 + k (elements 16 + 8k ..) complete
           const int k = i1 / 8 - 1;
-          uint4 w;
-          w.x = pack2(p[8 * k + 0], p[8 * k + 1]);
-          w.y = pack2(p[8 * k + 2], p[8 * k + 3]);
-          w.z = pack2(p[8 * k + 4], p[8 * k + 5]);
-          w.w = pack2(p[8 * k + 6], p[8 * k + 7]);
-          pf[2 + k] = as_bf16x8(w);
+          pf[2 + k] = pack8(p + 8 * k);
           // an empty asm that consumes the operand keeps its computation in
           // this phase (the compiler would otherwise sink it past the
           // barrier, next to the MFMAs that read it)
@@ -342,12 +336,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdArgs a) {
         // MFMAs reading tile t's operand k (slots DB k .. DB k + DB - 1) are out
         if (i1 / 8 != i0 / 8) {
           const int k = i1 / 8 - 1;
-          uint4 w;
-          w.x = pack2(p[8 * k + 0], p[8 * k + 1]);
-          w.y = pack2(p[8 * k + 2], p[8 * k + 3]);
-          w.z = pack2(p[8 * k + 4], p[8 * k + 5]);
-          w.w = pack2(p[8 * k + 6], p[8 * k + 7]);
-          pf[k] = as_bf16x8(w);
+          pf[k] = pack8(p + 8 * k);
           asm volatile("" : "+v"(pf[k]));
         }
         __builtin_amdgcn_sched_barrier(0);
