@@ -113,8 +113,9 @@ def test_keys_that_re_enter(d, lens, seed):
     assert torch.equal(dev, OA.visibility(trajs))
 
 
+@pytest.mark.parametrize("d", [128, 64])
 @pytest.mark.parametrize("jump", [False, True])
-def test_scores_far_above_earlier_tiles(jump):
+def test_scores_far_above_earlier_tiles(jump, d):
     """One key every 64 positions scores 20 base-2 units above the previous
     such key, so that most tiles exceed every score their rows have seen by
     more than 16 and take the forward's slow path (exact maximum, rescale);
@@ -123,7 +124,7 @@ def test_scores_far_above_earlier_tiles(jump):
     score.  (A steady ramp of all keys would make dQ ill-conditioned: a
     large key component common to the few keys of each softmax, under dS
     rows that sum to zero.)"""
-    d, hq, hkv, lens, seed = 128, 2, 1, [700, 300], 41
+    hq, hkv, lens, seed = 2, 1, [700, 300], 41
     rng = np.random.default_rng(seed)
     trajs = synth.random_trajectories(rng, lens, max_edits=5, max_span=60, summary_max=20)
     T = trajs[-1].end
@@ -140,7 +141,7 @@ def test_scores_far_above_earlier_tiles(jump):
     k = k.to(torch.bfloat16)
     v, do = torch.randn(T, hkv, d, generator=gen), torch.randn(T, hq, d, generator=gen)
     _check_full(trajs, q, k, v.to(torch.bfloat16), do.to(torch.bfloat16),
-                f"growing scores (jump={jump})")
+                f"growing scores (jump={jump}, d={d})")
 
 
 def test_no_compression_is_causal():
