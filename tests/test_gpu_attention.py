@@ -209,18 +209,19 @@ def _sampled_keys(trajs, death, rng, max_range, with_prompt_key):
 
 @pytest.mark.slow
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("workload,kv_heads,prompt_key", [("b4x32k", [0, 3], True),
-                                                          ("long128k", [5], True)])
-def test_full_size_sampled(workload, kv_heads, prompt_key):
+@pytest.mark.parametrize("workload,seed,kv_heads,prompt_key", [("b4x32k", 0, [0, 3], True),
+                                                               ("b4x32k", 1, [1, 2], True),
+                                                               ("long128k", 0, [5], True)])
+def test_full_size_sampled(workload, seed, kv_heads, prompt_key):
     """At the benchmark's size: sampled rows (O, LSE, dQ) and sampled keys
     (dK, dV, over every row that sees them) against the oracle.  The prompt
     key of the 128K trajectory is seen by all its 131072 rows: its key tile
     is cut into 64 items whose fp32 partials the reduce pass sums."""
-    trajs = synth.make_trajectories(workload, 0)
+    trajs = synth.make_trajectories(workload, seed)
     wl = synth.ATTN_WORKLOADS[workload]
     G = wl.n_heads_q // wl.n_heads_kv
-    q, k, v, do = synth.make_attn_tensors(workload, 0, device="cuda")
-    print(f"[gpu] {workload} full size", flush=True)
+    q, k, v, do = synth.make_attn_tensors(workload, seed, device="cuda")
+    print(f"[gpu] {workload} seed {seed} full size", flush=True)
     m = mv.ViewMask(trajs).upload()
     o, lse = mv.attn_fwd(m, q, k, v)
     dq, dk, dv = mv.attn_bwd(m, q, k, v, o, do, lse)
@@ -228,7 +229,7 @@ def test_full_size_sampled(workload, kv_heads, prompt_key):
     qc, kc, vc, dc = (x.cpu() for x in (q, k, v, do))
     oc, lc, dqc, dkc, dvc = (x.cpu() for x in (o, lse, dq, dk, dv))
     del q, k, v, do, o, lse, dq, dk, dv
-    rng = np.random.default_rng(7)
+    rng = np.random.default_rng(7 + seed)
     rows = _sample_rows(trajs, rng)
     heads = [hk * G + i for hk in kv_heads for i in (0, G - 1)]
     O, L = OA.rows(trajs, qc, kc, vc, rows, heads=heads)
